@@ -1,0 +1,328 @@
+/* oracle.c -- plain fp64 CPU oracle for pair-biased, gated multi-head attention.
+ *
+ * TEST INFRASTRUCTURE. Only the tests, the smoke check and the benchmark's
+ * CPU-baseline leg may load or call this library. It shares no code, header,
+ * table or helper with the GPU path, and the GPU path never calls it.
+ *
+ * What it computes (every formula is evaluated exactly as written, in fp64, on
+ * the exact input values; bf16 and fp32 inputs convert to fp64 without error):
+ *
+ *   Paper, Methods, "RFDiffusion 3 preliminaries and notation": every
+ *   token-level attention block adds a per-head pair bias B = f_B(Z), a
+ *   learned projection of the pair track, to the logits before the softmax,
+ *   softmax(Q K^T / sqrt(d) + B).
+ *   Paper, Methods, "1D row-sharding", Eq. (cross_attn): a stripe of query
+ *   rows attends to keys and values projected from the full single track S,
+ *   with the bias taken from the stripe's own rows of Z.
+ *   The projection f_B is read as Linear(LayerNorm(z)) over the c_z channels
+ *   of one pair (biased variance, eps inside the square root, affine gamma and
+ *   beta), and the output is gated elementwise by sigmoid(W_g s_i); the paper
+ *   states neither, so both are readings.
+ *
+ *   q_i = W_q s_i, k_j = W_k s_j, v_j = W_v s_j, g_i = sigmoid(W_g s_i), each
+ *   reshaped [H, d] with flat index h*d + e;
+ *   b[i,j,h] = sum_c W_b[h,c] (gamma_c (z[i,j,c] - mu) / sqrt(var + eps) + beta_c) + b_b[h];
+ *   l[h,i,j] = q_{i,h} . k_{j,h} / sqrt(d) + b[i,j,h], or -inf for a masked key;
+ *   out[i, h*d+e] = g_i[h*d+e] * sum_j softmax_j(l[h,i,:]) v_{j,h,e}; a row
+ *   with every key masked gives 0.
+ *
+ *   Blocked form (self-tests only), Paper, Methods, "2D grid context
+ *   parallelism" and Appendix "Q/K/V layout and the ring loop": keys are split
+ *   into blocks by the chunk rule of Appendix "Chunk distribution algorithm";
+ *   each block yields a partial state (m, l, acc) with m the block's maximum
+ *   logit, l = sum exp(l - m) and acc = sum exp(l - m) v, and the partials are
+ *   folded one by one, in increasing block order, into a running total with the
+ *   online-softmax rule (Related Work, "IO-efficient attention": running
+ *   softmax statistics).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* Appendix "Chunk distribution algorithm": part p of `total` items over
+ * `parts` parts has floor(total/parts) items plus one when p < total mod parts,
+ * and starts at p*floor(total/parts) + min(p, total mod parts). */
+void oracle_chunk(int64_t total, int64_t parts, int64_t p, int64_t* size, int64_t* start) {
+  const int64_t q = total / parts, r = total % parts;
+  *size = q + (p < r ? 1 : 0);
+  *start = p * q + (p < r ? p : r);
+}
+
+/* Input decoding: element idx of a buffer holding fp32 (dtype 0) or bf16 (dtype 1). */
+static double load_elem(const void* buf, int dtype, int64_t idx) {
+  if (dtype == 0) return (double)((const float*)buf)[idx];
+  uint32_t bits = (uint32_t)((const uint16_t*)buf)[idx] << 16;
+  float f;
+  memcpy(&f, &bits, 4);
+  return (double)f;
+}
+
+static double sigmoid(double x) { return 1.0 / (1.0 + exp(-x)); }
+
+/* y[t, o] = sum_c w[o, c] x[t, c]  (nn.Linear layout, no bias). */
+void oracle_linear(int64_t n_tok, int n_in, int n_out, const double* x, const double* w, double* y) {
+#pragma omp parallel for schedule(static)
+  for (int64_t t = 0; t < n_tok; ++t)
+    for (int o = 0; o < n_out; ++o) {
+      double acc = 0.0;
+      for (int c = 0; c < n_in; ++c) acc += w[(int64_t)o * n_in + c] * x[t * n_in + c];
+      y[t * n_out + o] = acc;
+    }
+}
+
+/* LayerNorm of one pair's c_z channels, then the linear map to H heads. */
+static void pair_bias(const void* z, int dtype, int64_t off, int c_z, int n_heads, const double* w_b,
+                      const double* b_b, const double* gamma, const double* beta, double eps, double* ln,
+                      double* b_out) {
+  double mu = 0.0;
+  for (int c = 0; c < c_z; ++c) mu += load_elem(z, dtype, off + c);
+  mu /= c_z;
+  double var = 0.0;
+  for (int c = 0; c < c_z; ++c) {
+    const double t = load_elem(z, dtype, off + c) - mu;
+    var += t * t;
+  }
+  var /= c_z;
+  const double inv = 1.0 / sqrt(var + eps);
+  for (int c = 0; c < c_z; ++c) {
+    const double xhat = (load_elem(z, dtype, off + c) - mu) * inv;
+    ln[c] = (gamma ? gamma[c] : 1.0) * xhat + (beta ? beta[c] : 0.0);
+  }
+  for (int h = 0; h < n_heads; ++h) {
+    double acc = 0.0;
+    for (int c = 0; c < c_z; ++c) acc += w_b[(int64_t)h * c_z + c] * ln[c];
+    b_out[h] = acc + (b_b ? b_b[h] : 0.0);
+  }
+}
+
+/* bias[r, c, h] for pairs z[r*row_stride + c*c_z + ...], r < n_rows, c < n_cols. */
+int oracle_bias(int64_t n_rows, int64_t n_cols, int c_z, int n_heads, const void* z, int dtype,
+                int64_t row_stride, const double* w_b, const double* b_b, const double* gamma,
+                const double* beta, double eps, double* out) {
+  if (!z || !w_b || !out || c_z <= 0 || n_heads <= 0) return -1;
+#pragma omp parallel
+  {
+    double* ln = (double*)malloc(sizeof(double) * (size_t)c_z);
+#pragma omp for schedule(static)
+    for (int64_t r = 0; r < n_rows; ++r)
+      for (int64_t c = 0; c < n_cols; ++c)
+        pair_bias(z, dtype, r * row_stride + c * c_z, c_z, n_heads, w_b, b_b, gamma, beta, eps, ln,
+                  out + (r * n_cols + c) * n_heads);
+    free(ln);
+  }
+  return 0;
+}
+
+/* Logits of one query row for head h over keys [k0, k1); masked keys get -inf. */
+static void row_logits(int64_t k0, int64_t k1, int n_heads, int d, int h, const double* q_row,
+                       const double* k, const double* bias_row, const uint8_t* mask, double* logit) {
+  const int hd = n_heads * d;
+  const double scale = 1.0 / sqrt((double)d);
+  for (int64_t j = k0; j < k1; ++j) {
+    if (mask && !mask[j]) {
+      logit[j - k0] = -INFINITY;
+      continue;
+    }
+    double dot = 0.0;
+    for (int e = 0; e < d; ++e) dot += q_row[h * d + e] * k[j * hd + h * d + e];
+    logit[j - k0] = dot * scale + bias_row[j * n_heads + h];
+  }
+}
+
+/* Plain softmax attention of one query row against all n_tok keys, then the gate. */
+static void attend_row(int64_t n_tok, int n_heads, int d, const double* q_row, const double* k,
+                       const double* v, const double* bias_row, const uint8_t* mask, const double* g_row,
+                       double* logit, double* out_row) {
+  for (int h = 0; h < n_heads; ++h) {
+    row_logits(0, n_tok, n_heads, d, h, q_row, k, bias_row, mask, logit);
+    double mx = -INFINITY;
+    for (int64_t j = 0; j < n_tok; ++j)
+      if (logit[j] > mx) mx = logit[j];
+    for (int e = 0; e < d; ++e) out_row[h * d + e] = 0.0;
+    if (mx == -INFINITY) continue; /* every key masked: output 0 */
+    double den = 0.0;
+    for (int64_t j = 0; j < n_tok; ++j) den += exp(logit[j] - mx);
+    for (int e = 0; e < d; ++e) {
+      double num = 0.0;
+      for (int64_t j = 0; j < n_tok; ++j)
+        num += exp(logit[j] - mx) * v[j * (int64_t)n_heads * d + h * d + e];
+      out_row[h * d + e] = g_row[h * d + e] * (num / den);
+    }
+  }
+}
+
+/* Attention given every ingredient: q, g_pre (pre-sigmoid gate) [n_rows, H*d],
+ * k, v [n_tok, H*d], bias [n_rows, n_tok, H], mask [n_tok] or NULL. */
+int oracle_attend(int64_t n_rows, int64_t n_tok, int n_heads, int d, const double* q, const double* k,
+                  const double* v, const double* g_pre, const double* bias, const uint8_t* mask,
+                  double* out) {
+  if (!q || !k || !v || !g_pre || !bias || !out) return -1;
+  const int hd = n_heads * d;
+#pragma omp parallel
+  {
+    double* logit = (double*)malloc(sizeof(double) * (size_t)n_tok);
+    double* g_row = (double*)malloc(sizeof(double) * (size_t)hd);
+#pragma omp for schedule(dynamic, 1)
+    for (int64_t r = 0; r < n_rows; ++r) {
+      for (int x = 0; x < hd; ++x) g_row[x] = sigmoid(g_pre[r * hd + x]);
+      attend_row(n_tok, n_heads, d, q + r * hd, k, v, bias + r * n_tok * n_heads, mask, g_row, logit,
+                 out + r * hd);
+    }
+    free(logit);
+    free(g_row);
+  }
+  return 0;
+}
+
+/* Partial state of one query row over keys [k0, k1): m[h], l[h], acc[h*d+e]. */
+static void partial_row(int64_t k0, int64_t k1, int n_heads, int d, const double* q_row, const double* k,
+                        const double* v, const double* bias_row, const uint8_t* mask, double* logit,
+                        double* m, double* l, double* acc) {
+  for (int h = 0; h < n_heads; ++h) {
+    row_logits(k0, k1, n_heads, d, h, q_row, k, bias_row, mask, logit);
+    double mx = -INFINITY;
+    for (int64_t j = 0; j < k1 - k0; ++j)
+      if (logit[j] > mx) mx = logit[j];
+    m[h] = mx;
+    l[h] = 0.0;
+    for (int e = 0; e < d; ++e) acc[h * d + e] = 0.0;
+    if (mx == -INFINITY) continue;
+    for (int64_t j = 0; j < k1 - k0; ++j) {
+      const double w = exp(logit[j] - mx);
+      l[h] += w;
+      for (int e = 0; e < d; ++e) acc[h * d + e] += w * v[(k0 + j) * (int64_t)n_heads * d + h * d + e];
+    }
+  }
+}
+
+/* Online-softmax fold of one partial (mb, lb, accb) into the running total (m, l, acc). */
+static void fold(int d, double* m, double* l, double* acc, double mb, double lb, const double* accb) {
+  if (mb == -INFINITY) return; /* empty partial: the identity */
+  if (*m == -INFINITY) {
+    *m = mb;
+    *l = lb;
+    for (int e = 0; e < d; ++e) acc[e] = accb[e];
+    return;
+  }
+  const double mn = mb > *m ? mb : *m;
+  const double a = exp(*m - mn), b = exp(mb - mn);
+  *l = a * *l + b * lb;
+  for (int e = 0; e < d; ++e) acc[e] = a * acc[e] + b * accb[e];
+  *m = mn;
+}
+
+/* Merge n_parts partial states, in increasing part order.
+ * m, l: [n_parts, H, n_rows]; acc: [n_parts, n_rows, H, d]; gate: [n_rows, H*d] post-sigmoid or NULL.
+ * Outputs (each may be NULL): m_out, l_out [H, n_rows]; acc_out [n_rows, H, d];
+ * out [n_rows, H*d] = gate * acc / l (0 where l == 0). */
+int oracle_merge(int n_parts, int64_t n_rows, int n_heads, int d, const double* m, const double* l,
+                 const double* acc, const double* gate, double* m_out, double* l_out, double* acc_out,
+                 double* out) {
+  if (n_parts < 1 || !m || !l || !acc) return -1;
+  const int hd = n_heads * d;
+#pragma omp parallel
+  {
+    double* run = (double*)malloc(sizeof(double) * (size_t)d);
+#pragma omp for schedule(static)
+    for (int64_t r = 0; r < n_rows; ++r)
+      for (int h = 0; h < n_heads; ++h) {
+        double rm = -INFINITY, rl = 0.0;
+        for (int e = 0; e < d; ++e) run[e] = 0.0;
+        for (int p = 0; p < n_parts; ++p)
+          fold(d, &rm, &rl, run, m[((int64_t)p * n_heads + h) * n_rows + r], l[((int64_t)p * n_heads + h) * n_rows + r],
+               acc + (((int64_t)p * n_rows + r) * n_heads + h) * d);
+        if (m_out) m_out[(int64_t)h * n_rows + r] = rm;
+        if (l_out) l_out[(int64_t)h * n_rows + r] = rl;
+        for (int e = 0; e < d; ++e) {
+          if (acc_out) acc_out[(r * n_heads + h) * d + e] = run[e];
+          if (out) out[r * hd + h * d + e] = rl > 0.0 ? (gate ? gate[r * hd + h * d + e] : 1.0) * run[e] / rl : 0.0;
+        }
+      }
+    free(run);
+  }
+  return 0;
+}
+
+/* The whole definition for the query tokens rows[0..n_rows): projections, LN
+ * bias from each row's z (z_rows[r] = z[rows[r], :, :]), attention, gate.
+ * s [n_tok, c_s]; weights fp64 in nn.Linear layout; gamma, beta, b_b may be NULL.
+ * n_blocks == 1: the plain softmax; n_blocks > 1: the blocked form, and the
+ * per-block partials are returned when m_parts/l_parts/acc_parts are non-NULL
+ * (layout as in oracle_merge, with n_rows rows). */
+int oracle_attention(int64_t n_tok, int c_s, int c_z, int n_heads, int d, const double* s, const void* z_rows,
+                     int z_dtype, const int64_t* rows, int64_t n_rows, const uint8_t* mask, const double* w_q,
+                     const double* w_k, const double* w_v, const double* w_g, const double* w_b,
+                     const double* b_b, const double* gamma, const double* beta, double eps, int n_blocks,
+                     double* out, double* m_parts, double* l_parts, double* acc_parts) {
+  if (!s || !z_rows || !rows || !w_q || !w_k || !w_v || !w_g || !w_b || !out) return -1;
+  if (n_tok <= 0 || n_rows < 0 || n_blocks < 1 || n_blocks > n_tok) return -1;
+  const int hd = n_heads * d;
+  double* k = (double*)malloc(sizeof(double) * (size_t)(n_tok * hd));
+  double* v = (double*)malloc(sizeof(double) * (size_t)(n_tok * hd));
+  double* sq = (double*)malloc(sizeof(double) * (size_t)((n_rows ? n_rows : 1) * c_s));
+  double* q = (double*)malloc(sizeof(double) * (size_t)((n_rows ? n_rows : 1) * hd));
+  double* gp = (double*)malloc(sizeof(double) * (size_t)((n_rows ? n_rows : 1) * hd));
+  for (int64_t r = 0; r < n_rows; ++r) memcpy(sq + r * c_s, s + rows[r] * c_s, sizeof(double) * (size_t)c_s);
+  oracle_linear(n_tok, c_s, hd, s, w_k, k);
+  oracle_linear(n_tok, c_s, hd, s, w_v, v);
+  oracle_linear(n_rows, c_s, hd, sq, w_q, q);
+  oracle_linear(n_rows, c_s, hd, sq, w_g, gp);
+  double* pm = m_parts ? m_parts : (n_blocks > 1 ? (double*)malloc(sizeof(double) * (size_t)(n_blocks * n_heads * n_rows)) : NULL);
+  double* pl = l_parts ? l_parts : (n_blocks > 1 ? (double*)malloc(sizeof(double) * (size_t)(n_blocks * n_heads * n_rows)) : NULL);
+  double* pa = acc_parts ? acc_parts : (n_blocks > 1 ? (double*)malloc(sizeof(double) * (size_t)(n_blocks * n_rows * hd)) : NULL);
+#pragma omp parallel
+  {
+    double* bias_row = (double*)malloc(sizeof(double) * (size_t)(n_tok * n_heads));
+    double* logit = (double*)malloc(sizeof(double) * (size_t)n_tok);
+    double* ln = (double*)malloc(sizeof(double) * (size_t)c_z);
+    double* g_row = (double*)malloc(sizeof(double) * (size_t)hd);
+    double* bm = (double*)malloc(sizeof(double) * (size_t)n_heads);
+    double* bl = (double*)malloc(sizeof(double) * (size_t)n_heads);
+    double* ba = (double*)malloc(sizeof(double) * (size_t)hd);
+#pragma omp for schedule(dynamic, 1)
+    for (int64_t r = 0; r < n_rows; ++r) {
+      const int64_t zoff = r * n_tok * (int64_t)c_z;
+      for (int64_t j = 0; j < n_tok; ++j)
+        pair_bias(z_rows, z_dtype, zoff + j * c_z, c_z, n_heads, w_b, b_b, gamma, beta, eps, ln,
+                  bias_row + j * n_heads);
+      for (int x = 0; x < hd; ++x) g_row[x] = sigmoid(gp[r * hd + x]);
+      if (n_blocks == 1) {
+        attend_row(n_tok, n_heads, d, q + r * hd, k, v, bias_row, mask, g_row, logit, out + r * hd);
+        continue;
+      }
+      for (int b = 0; b < n_blocks; ++b) {
+        int64_t size, start;
+        oracle_chunk(n_tok, n_blocks, b, &size, &start);
+        partial_row(start, start + size, n_heads, d, q + r * hd, k, v, bias_row, mask, logit, bm, bl, ba);
+        for (int h = 0; h < n_heads; ++h) {
+          pm[((int64_t)b * n_heads + h) * n_rows + r] = bm[h];
+          pl[((int64_t)b * n_heads + h) * n_rows + r] = bl[h];
+          for (int e = 0; e < d; ++e) pa[(((int64_t)b * n_rows + r) * n_heads + h) * d + e] = ba[h * d + e];
+        }
+      }
+    }
+    free(bias_row);
+    free(logit);
+    free(ln);
+    free(g_row);
+    free(bm);
+    free(bl);
+    free(ba);
+  }
+  if (n_blocks > 1) {
+    double* gate = (double*)malloc(sizeof(double) * (size_t)((n_rows ? n_rows : 1) * hd));
+    for (int64_t x = 0; x < n_rows * hd; ++x) gate[x] = sigmoid(gp[x]);
+    oracle_merge(n_blocks, n_rows, n_heads, d, pm, pl, pa, gate, NULL, NULL, NULL, out);
+    free(gate);
+    if (!m_parts) free(pm);
+    if (!l_parts) free(pl);
+    if (!acc_parts) free(pa);
+  }
+  free(k);
+  free(v);
+  free(sq);
+  free(q);
+  free(gp);
+  return 0;
+}

@@ -1,0 +1,294 @@
+"""Seeded synthetic inputs for pair-biased attention (tests and benchmark).
+
+This module is shared by the fp64 oracle's tests and by the GPU path's tests
+and benchmark. It holds no attention arithmetic: it only draws numbers.
+
+Definition (the numpy functions below are the reference; ``csrc/synth_host.c``
+and ``csrc/synth_dev.hip`` are bit-identical twins, checked by tests):
+
+* ``fin``: the SplitMix64 output function (Steele, Lea and Flood, 2014).
+* ``key(seed, t) = fin(fin(seed + G) + t*G)`` with ``G = 0x9E3779B97F4A7C15``;
+  one independent stream per tensor id ``t``.
+* ``word(k, n) = fin(k + (n+1)*G)``: counter-based SplitMix64.
+* ``normal(k, e)``: the twelve 16-bit fields of ``word(k, 3e..3e+2)`` summed
+  (Irwin-Hall(12)), minus 393210, over 65536. Mean 0, variance 1 - 2^-32,
+  range about +-6. Every value is an exact fp32 number.
+* bf16 tensors take round-to-nearest-even of that fp32 value.
+
+The workloads are the synthetic stand-ins for the paper's icosahedral RFD3
+sampling runs (60 copies of a subunit, c_s = 384, c_z = 128, 16 heads); the
+paper's own runs need trained weights and are not reproducible here.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Dict, Optional, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+G = np.uint64(0x9E3779B97F4A7C15)
+_M1 = np.uint64(0xBF58476D1CE4E5B9)
+_M2 = np.uint64(0x94D049BB133111EB)
+
+# Tensor ids: one independent stream each.
+T_S, T_Z, T_WQ, T_WK, T_WV, T_WG, T_WB, T_ZBASE, T_MASK, T_GAMMA, T_BETA, T_BB = range(1, 13)
+
+
+# ----------------------------------------------------------------------------- numpy definition
+def _fin(x: np.ndarray) -> np.ndarray:
+    x = np.asarray(x, dtype=np.uint64)
+    x = x ^ (x >> np.uint64(30))
+    x = x * _M1
+    x = x ^ (x >> np.uint64(27))
+    x = x * _M2
+    return x ^ (x >> np.uint64(31))
+
+
+def key(seed: int, tensor_id: int) -> int:
+    with np.errstate(over="ignore"):
+        k = _fin(np.array([seed], dtype=np.uint64) + G)
+        k = _fin(k + np.uint64(tensor_id) * G)
+    return int(k[0])
+
+
+def word_np(k: int, n: np.ndarray) -> np.ndarray:
+    with np.errstate(over="ignore"):
+        return _fin(np.uint64(k) + (np.asarray(n, dtype=np.uint64) + np.uint64(1)) * G)
+
+
+def normal_np(k: int, start: int, count: int) -> np.ndarray:
+    """fp32 normals ``normal(k, start + i)`` for i < count (reference definition)."""
+    return normal_np_at(k, np.arange(count, dtype=np.uint64) + np.uint64(start))
+
+
+def normal_np_at(k: int, e: np.ndarray) -> np.ndarray:
+    """fp32 normals ``normal(k, e[i])`` at arbitrary element indices."""
+    e = np.asarray(e, dtype=np.uint64)
+    s = np.zeros(e.shape, dtype=np.int64)
+    for j in range(3):
+        w = word_np(k, np.uint64(3) * e + np.uint64(j))
+        for t in range(4):
+            s += ((w >> np.uint64(16 * t)) & np.uint64(0xFFFF)).astype(np.int64)
+    return ((s - 393210).astype(np.float32) * np.float32(1.0 / 65536.0)).astype(np.float32)
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """Round fp32 to bf16 (nearest, ties to even); returns the 16-bit patterns."""
+    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    b = b + np.uint64(0x7FFF) + ((b >> np.uint64(16)) & np.uint64(1))
+    return (b >> np.uint64(16)).astype(np.uint16)
+
+
+def bf16_to_f32(bits: np.ndarray) -> np.ndarray:
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def z_rows_np(k_z: int, k_base: int, period: int, n_tok: int, c_z: int, rows: Sequence[int],
+              bf16: bool) -> np.ndarray:
+    """Reference definition of rows of z (small sizes only)."""
+    out = []
+    for i in rows:
+        e0 = int(i) * n_tok * c_z
+        v = normal_np(k_z, e0, n_tok * c_z).reshape(n_tok, c_z)
+        if period > 0:
+            j = np.arange(n_tok)
+            eb = ((int(i) % period) * period + (j % period))[:, None] * c_z + np.arange(c_z)[None, :]
+            base = normal_np_at(k_base, eb.astype(np.uint64))
+            v = (base + (np.float32(0.1) * v).astype(np.float32)).astype(np.float32)
+        out.append(bf16_round(v) if bf16 else v)
+    return np.stack(out)
+
+
+# ----------------------------------------------------------------------------- fast C twin
+_host_lib = None
+
+
+def _host() -> ctypes.CDLL:
+    global _host_lib
+    if _host_lib is None:
+        path = os.path.join(_HERE, "libsynth_host.so")
+        if not os.path.exists(path):
+            from . import build as _b
+            _b.build_host()
+        lib = ctypes.CDLL(path)
+        u64, i64, i32, vp = ctypes.c_uint64, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
+        lib.synth_key.restype = u64
+        lib.synth_key.argtypes = [u64, u64]
+        lib.synth_word.restype = u64
+        lib.synth_word.argtypes = [u64, u64]
+        lib.synth_normal_f32.argtypes = [u64, u64, i64, vp]
+        lib.synth_normal_bf16.argtypes = [u64, u64, i64, vp]
+        lib.synth_z_rows.argtypes = [u64, u64, i64, i64, i32, vp, i64, i32, vp]
+        _host_lib = lib
+    return _host_lib
+
+
+def normal(k: int, start: int, count: int, bf16: bool = False) -> np.ndarray:
+    out = np.empty(count, dtype=np.uint16 if bf16 else np.float32)
+    fn = _host().synth_normal_bf16 if bf16 else _host().synth_normal_f32
+    fn(k, start, count, out.ctypes.data)
+    return out
+
+
+def z_rows(k_z: int, k_base: int, period: int, n_tok: int, c_z: int, rows: Sequence[int],
+           bf16: bool) -> np.ndarray:
+    r = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+    out = np.empty((len(r), n_tok, c_z), dtype=np.uint16 if bf16 else np.float32)
+    _host().synth_z_rows(k_z, k_base, period, n_tok, c_z, r.ctypes.data, len(r), int(bf16), out.ctypes.data)
+    return out
+
+
+# ----------------------------------------------------------------------------- workloads
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    n_tok: int
+    c_s: int
+    c_z: int
+    n_heads: int
+    head_dim: int
+    dtype: str                      # "f32" or "bf16": dtype of s and z
+    n_key_blocks: int               # key blocks per call (the paper's ring steps)
+    stripes: Tuple[Tuple[int, int], ...]  # (q_row0, n_q) per call
+    mask: str = "none"              # "none" | "tail:K" | "random:K"
+    z_period: int = 0               # 0: iid z; P > 0: z = base[i%P, j%P] + 0.1 noise
+    seed: int = 0
+    note: str = ""
+
+    @property
+    def bf16(self) -> bool:
+        return self.dtype == "bf16"
+
+    @property
+    def elem_bytes(self) -> int:
+        return 2 if self.bf16 else 4
+
+
+def _w(name, n, c_s, c_z, h, d, dtype, n_kb, stripes, mask="none", period=0, note=""):
+    return Workload(name, n, c_s, c_z, h, d, dtype, n_kb, stripes, mask, period, 0, note)
+
+
+WORKLOADS: Dict[str, Workload] = {
+    w.name: w
+    for w in [
+        _w("tiny128_f32", 128, 128, 32, 4, 32, "f32", 1, ((0, 128),),
+           note="tiny fp32 case; one key block (also run with 4 for the blocked check)"),
+        _w("pad1024_bf16", 1024, 384, 128, 16, 24, "bf16", 4, ((0, 1024),), "tail:4",
+           note="12 copies x 85-token subunit + 4 masked padding tokens; 4 key blocks of 256"),
+        _w("ico4800_bf16", 4800, 384, 128, 16, 24, "bf16", 10, ((0, 4800),), "random:240", 80,
+           note="60 copies x 80 tokens, 60-fold z structure, 5% random key mask, 10 key blocks of 480"),
+        _w("grid12000_bf16", 12000, 384, 128, 16, 24, "bf16", 4,
+           ((0, 3000), (3000, 3000), (6000, 3000), (9000, 3000)),
+           note="one GPU's share of a 4x4 grid: 4 query stripes x 4 key blocks of 3000"),
+        _w("asm24000_bf16", 24000, 384, 128, 16, 24, "bf16", 6, ((0, 24000),), "tail:480",
+           note="whole 60 x 400 assembly, z = 147 GB bf16, last 480 tokens masked, 6 key blocks of 4000"),
+    ]
+}
+
+
+def weights(wl: Workload, affine: bool = False) -> Dict[str, Optional[np.ndarray]]:
+    """fp32 weights in nn.Linear layout [out, in], drawn N(0, 1/fan_in).
+
+    ``affine=False`` gives the workloads' LayerNorm (gamma = 1, beta = 0, no
+    projection bias); ``affine=True`` draws gamma, beta and b_b too (tests).
+    """
+    hd = wl.n_heads * wl.head_dim
+    out: Dict[str, Optional[np.ndarray]] = {}
+    for name, tid, rows, fan in (("w_q", T_WQ, hd, wl.c_s), ("w_k", T_WK, hd, wl.c_s),
+                                 ("w_v", T_WV, hd, wl.c_s), ("w_g", T_WG, hd, wl.c_s),
+                                 ("w_b", T_WB, wl.n_heads, wl.c_z)):
+        scale = np.float32(1.0 / np.sqrt(fan))
+        out[name] = (normal(key(wl.seed, tid), 0, rows * fan) * scale).astype(np.float32).reshape(rows, fan)
+    if affine:
+        out["ln_gamma"] = (np.float32(1.0) + np.float32(0.25) * normal(key(wl.seed, T_GAMMA), 0, wl.c_z)
+                           ).astype(np.float32)
+        out["ln_beta"] = normal(key(wl.seed, T_BETA), 0, wl.c_z)
+        out["b_b"] = normal(key(wl.seed, T_BB), 0, wl.n_heads)
+    else:
+        out["ln_gamma"] = None
+        out["ln_beta"] = None
+        out["b_b"] = None
+    return out
+
+
+def s_host(wl: Workload) -> np.ndarray:
+    """Single track s[N, c_s]: bf16 bit patterns (uint16) or fp32."""
+    return normal(key(wl.seed, T_S), 0, wl.n_tok * wl.c_s, bf16=wl.bf16).reshape(wl.n_tok, wl.c_s)
+
+
+def mask_host(wl: Workload) -> Optional[np.ndarray]:
+    """Key mask [N] uint8 (1 = attend), or None when every key attends."""
+    if wl.mask == "none":
+        return None
+    kind, k = wl.mask.split(":")
+    k = int(k)
+    m = np.ones(wl.n_tok, dtype=np.uint8)
+    if kind == "tail":
+        m[wl.n_tok - k:] = 0
+    elif kind == "random":
+        idx = np.arange(wl.n_tok, dtype=np.uint64)
+        w = word_np(key(wl.seed, T_MASK), idx)
+        order = np.lexsort((idx, w))  # by word, ties by index
+        m[order[:k]] = 0
+    else:
+        raise ValueError(wl.mask)
+    return m
+
+
+def z_keys(wl: Workload) -> Tuple[int, int]:
+    return key(wl.seed, T_Z), key(wl.seed, T_ZBASE)
+
+
+def z_host(wl: Workload, rows: Sequence[int]) -> np.ndarray:
+    """Rows of z[N, N, c_z] on the host, shape [len(rows), N, c_z]."""
+    kz, kb = z_keys(wl)
+    return z_rows(kz, kb, wl.z_period, wl.n_tok, wl.c_z, rows, wl.bf16)
+
+
+# ----------------------------------------------------------------------------- device twin
+_dev_lib = None
+
+
+def _dev() -> ctypes.CDLL:
+    global _dev_lib
+    if _dev_lib is None:
+        path = os.path.join(_HERE, "libsynth_dev.so")
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is not built; run __graft_entry__.build()")
+        lib = ctypes.CDLL(path)
+        u64, i64, i32, vp = ctypes.c_uint64, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
+        lib.synth_dev_z_rows.argtypes = [u64, u64, i64, i64, i32, i64, i64, i32, vp, vp]
+        lib.synth_dev_normal.argtypes = [u64, u64, i64, i32, vp, vp]
+        lib.synth_dev_copy.argtypes = [vp, vp, i64, vp]
+        lib.synth_dev_read.argtypes = [vp, i64, vp, vp]
+        for f in (lib.synth_dev_z_rows, lib.synth_dev_normal, lib.synth_dev_copy, lib.synth_dev_read):
+            f.restype = ctypes.c_int
+        _dev_lib = lib
+    return _dev_lib
+
+
+def z_fill_device(wl: Workload, ptr: int, row0: int, n_rows: int, stream: int) -> None:
+    """Write rows [row0, row0+n_rows) of z into device memory at ``ptr``."""
+    kz, kb = z_keys(wl)
+    rc = _dev().synth_dev_z_rows(kz, kb, wl.z_period, wl.n_tok, wl.c_z, row0, n_rows, int(wl.bf16), ptr, stream)
+    if rc != 0:
+        raise RuntimeError(f"synth_dev_z_rows failed ({rc})")
+
+
+def normal_fill_device(k: int, start: int, count: int, bf16: bool, ptr: int, stream: int) -> None:
+    rc = _dev().synth_dev_normal(k, start, count, int(bf16), ptr, stream)
+    if rc != 0:
+        raise RuntimeError(f"synth_dev_normal failed ({rc})")
+
+
+def device_copy(src: int, dst: int, nbytes: int, stream: int) -> None:
+    if _dev().synth_dev_copy(src, dst, nbytes, stream) != 0:
+        raise RuntimeError("synth_dev_copy failed")
+
+
+def device_read(src: int, nbytes: int, sink: int, stream: int) -> None:
+    if _dev().synth_dev_read(src, nbytes, sink, stream) != 0:
+        raise RuntimeError("synth_dev_read failed")

@@ -1,0 +1,401 @@
+"""Pins that tie the fp64 oracle to things other than itself.
+
+Each ``pin_*`` function raises AssertionError when the oracle (whatever
+library ``oracle._lib`` currently holds) disagrees with:
+
+* the paper's chunk rule, worked out by hand (tests/golden/chunk_distribution.txt);
+* library routines that compute a special case: torch's ``layer_norm`` and
+  ``linear`` for the pair bias, torch's ``scaled_dot_product_attention`` for
+  the softmax attention with an additive float mask, all in fp64 on the CPU;
+* closed forms (uniform attention, a single token, one dominant key, all keys
+  masked);
+* invariants the definition implies (blocked equals unblocked, per-row bias
+  constants and LayerNorm shifts do not matter, token permutation
+  equivariance, a masked key equals a deleted one);
+* brute force at 40 significant digits on tiny inputs (mpmath).
+
+``tests/test_oracle_mutants.py`` plants plausible mistakes in copies of the
+oracle's C source and checks that every one of them fails at least one pin.
+"""
+from __future__ import annotations
+
+import os
+
+import mpmath
+import numpy as np
+import torch
+import torch.nn.functional as F
+
+import oracle
+import synth
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+def _case(seed=0, n=9, c_s=6, c_z=8, h=3, d=4, affine=True, mask_frac=0.3, dtype="f32"):
+    """Small random case: s, z (all rows), weights, mask."""
+    r = _rng(seed)
+    s = r.standard_normal((n, c_s)).astype(np.float32)
+    z = r.standard_normal((n, n, c_z)).astype(np.float32)
+    if dtype == "bf16":
+        s = synth.bf16_round(s)
+        z = synth.bf16_round(z)
+    w = {
+        "w_q": (r.standard_normal((h * d, c_s)) / np.sqrt(c_s)).astype(np.float32),
+        "w_k": (r.standard_normal((h * d, c_s)) / np.sqrt(c_s)).astype(np.float32),
+        "w_v": (r.standard_normal((h * d, c_s)) / np.sqrt(c_s)).astype(np.float32),
+        "w_g": (r.standard_normal((h * d, c_s)) / np.sqrt(c_s)).astype(np.float32),
+        "w_b": (r.standard_normal((h, c_z)) / np.sqrt(c_z)).astype(np.float32),
+        "ln_gamma": (1 + 0.3 * r.standard_normal(c_z)).astype(np.float32) if affine else None,
+        "ln_beta": (0.5 * r.standard_normal(c_z)).astype(np.float32) if affine else None,
+        "b_b": r.standard_normal(h).astype(np.float32) if affine else None,
+    }
+    mask = (r.random(n) >= mask_frac).astype(np.uint8)
+    mask[r.integers(n)] = 1  # at least one valid key
+    return s, z, w, mask
+
+
+def _torch_pipeline(s, z, w, mask, h, d, eps=1e-5):
+    """The definition composed from torch library routines (fp64, CPU)."""
+    t = lambda a: None if a is None else torch.from_numpy(oracle.decode(np.asarray(a)) if np.asarray(a).dtype == np.uint16 else np.asarray(a, dtype=np.float64))
+    S, Z = t(s), t(z)
+    n = S.shape[0]
+    c_z = Z.shape[-1]
+    q = F.linear(S, t(w["w_q"])).view(n, h, d).transpose(0, 1)
+    k = F.linear(S, t(w["w_k"])).view(n, h, d).transpose(0, 1)
+    v = F.linear(S, t(w["w_v"])).view(n, h, d).transpose(0, 1)
+    g = torch.sigmoid(F.linear(S, t(w["w_g"])))
+    ln = F.layer_norm(Z, (c_z,), t(w.get("ln_gamma")), t(w.get("ln_beta")), eps)
+    b = F.linear(ln, t(w["w_b"]), t(w.get("b_b")))  # [n, n, h]
+    bias = b.permute(2, 0, 1).contiguous()  # [h, i, j]
+    if mask is not None:
+        bias = bias.masked_fill(torch.from_numpy(mask == 0)[None, None, :], float("-inf"))
+    o = F.scaled_dot_product_attention(q.contiguous(), k.contiguous(), v.contiguous(), attn_mask=bias)
+    return (g * o.transpose(0, 1).reshape(n, h * d)).numpy()
+
+
+def _rel(a, b):
+    return float(np.max(np.abs(a - b)) / max(np.max(np.abs(b)), 1e-300))
+
+
+# ----------------------------------------------------------------------------- chunk rule
+def pin_chunk_golden():
+    with open(os.path.join(GOLDEN, "chunk_distribution.txt")) as f:
+        for line in f:
+            if not line.strip() or line.startswith("#"):
+                continue
+            left, right = line.split("|")
+            nums = [int(x) for x in left.split()]
+            total, parts, sizes = nums[0], nums[1], nums[2:]
+            starts = [int(x) for x in right.split()]
+            got = [oracle.chunk(total, parts, p) for p in range(parts)]
+            assert [g[0] for g in got] == sizes, (total, parts, got)
+            assert [g[1] for g in got] == starts, (total, parts, got)
+
+
+def pin_chunk_properties():
+    for total in (1, 2, 7, 100, 4800, 24000, 12347):
+        for parts in range(1, min(total, 17) + 1):
+            got = [oracle.chunk(total, parts, p) for p in range(parts)]
+            sizes = [g[0] for g in got]
+            assert sum(sizes) == total
+            assert max(sizes) - min(sizes) <= 1
+            assert got[0][1] == 0
+            for p in range(parts - 1):
+                assert got[p + 1][1] == got[p][1] + got[p][0]
+            assert sizes == sorted(sizes, reverse=True)
+
+
+# ----------------------------------------------------------------------------- library pins
+def pin_layer_norm_torch():
+    """With W_b = I (H = c_z) the bias is LayerNorm(z) itself."""
+    r = _rng(1)
+    c_z = 12
+    z = (3.0 + 2.0 * r.standard_normal((4, 5, c_z))).astype(np.float32)
+    gamma = (1 + 0.5 * r.standard_normal(c_z)).astype(np.float32)
+    beta = r.standard_normal(c_z).astype(np.float32)
+    for eps in (1e-5, 0.3):
+        got = oracle.bias(z, np.eye(c_z, dtype=np.float32), None, gamma, beta, eps)
+        ref = F.layer_norm(torch.from_numpy(z.astype(np.float64)), (c_z,),
+                           torch.from_numpy(gamma.astype(np.float64)), torch.from_numpy(beta.astype(np.float64)),
+                           eps).numpy()
+        assert _rel(got, ref) <= 1e-12, _rel(got, ref)
+
+
+def pin_bias_torch():
+    for dtype in ("f32", "bf16"):
+        s, z, w, _ = _case(2, n=6, c_z=16, h=5, dtype=dtype)
+        got = oracle.bias(z, w["w_b"], w["b_b"], w["ln_gamma"], w["ln_beta"], 1e-5)
+        Z = torch.from_numpy(oracle.decode(z))
+        ref = F.linear(F.layer_norm(Z, (16,), torch.from_numpy(w["ln_gamma"].astype(np.float64)),
+                                    torch.from_numpy(w["ln_beta"].astype(np.float64)), 1e-5),
+                       torch.from_numpy(w["w_b"].astype(np.float64)),
+                       torch.from_numpy(w["b_b"].astype(np.float64))).numpy()
+        assert _rel(got, ref) <= 1e-12, _rel(got, ref)
+
+
+def pin_attend_sdpa():
+    """Softmax attention with an explicit bias equals torch SDPA with a float mask."""
+    r = _rng(3)
+    n_rows, n, h, d = 5, 11, 3, 4
+    q = r.standard_normal((n_rows, h * d))
+    k = r.standard_normal((n, h * d))
+    v = r.standard_normal((n, h * d))
+    gp = r.standard_normal((n_rows, h * d))
+    b = 2.0 * r.standard_normal((n_rows, n, h))
+    mask = (r.random(n) > 0.3).astype(np.uint8)
+    mask[0] = 1
+    got = oracle.attend(q, k, v, gp, b, mask, h, d)
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a))
+    am = T(b).permute(2, 0, 1).masked_fill(T(mask == 0)[None, None, :], float("-inf"))
+    o = F.scaled_dot_product_attention(T(q).view(n_rows, h, d).transpose(0, 1).contiguous(),
+                                       T(k).view(n, h, d).transpose(0, 1).contiguous(),
+                                       T(v).view(n, h, d).transpose(0, 1).contiguous(), attn_mask=am)
+    ref = (torch.sigmoid(T(gp)) * o.transpose(0, 1).reshape(n_rows, h * d)).numpy()
+    assert _rel(got, ref) <= 1e-12, _rel(got, ref)
+
+
+def pin_pipeline_torch():
+    """The whole definition equals its composition from torch library routines."""
+    for seed, dtype, affine in ((4, "f32", True), (5, "bf16", True), (6, "f32", False)):
+        s, z, w, mask = _case(seed, n=10, c_s=7, c_z=8, h=3, d=4, affine=affine, dtype=dtype)
+        rows = np.arange(10)
+        got = oracle.attention(s, z, rows, mask, w, 3, 4)
+        ref = _torch_pipeline(s, z, w, mask, 3, 4)
+        assert _rel(got, ref) <= 1e-12, (seed, _rel(got, ref))
+    # a row stripe: rows 3..6 of the same tensors
+    s, z, w, mask = _case(7, n=10, c_s=7, c_z=8, h=3, d=4)
+    rows = np.arange(3, 7)
+    got = oracle.attention(s, z[rows], rows, mask, w, 3, 4)
+    ref = _torch_pipeline(s, z, w, mask, 3, 4)[rows]
+    assert _rel(got, ref) <= 1e-12
+
+
+# ----------------------------------------------------------------------------- closed forms
+def pin_uniform_attention():
+    """W_b = 0 and W_q = 0: every valid key gets the same weight."""
+    s, z, w, mask = _case(8, n=12, h=2, d=3)
+    w = dict(w)
+    w["w_b"] = np.zeros_like(w["w_b"])
+    w["w_q"] = np.zeros_like(w["w_q"])
+    rows = np.arange(12)
+    got = oracle.attention(s, z, rows, mask, w, 2, 3)
+    S = s.astype(np.float64)
+    v = S @ w["w_v"].astype(np.float64).T
+    g = 1.0 / (1.0 + np.exp(-(S @ w["w_g"].astype(np.float64).T)))
+    ref = g * v[mask == 1].mean(axis=0)[None, :]
+    assert _rel(got, ref) <= 1e-13, _rel(got, ref)
+
+
+def pin_single_token():
+    s, z, w, _ = _case(9, n=1, h=2, d=3)
+    got = oracle.attention(s, z, [0], None, w, 2, 3)
+    S = s.astype(np.float64)
+    ref = (1.0 / (1.0 + np.exp(-(S @ w["w_g"].astype(np.float64).T)))) * (S @ w["w_v"].astype(np.float64).T)
+    assert _rel(got, ref) <= 1e-14, _rel(got, ref)
+
+
+def pin_dominant_key():
+    r = _rng(10)
+    n, h, d = 20, 2, 3
+    q = r.standard_normal((1, h * d))
+    k = r.standard_normal((n, h * d))
+    v = r.standard_normal((n, h * d))
+    gp = r.standard_normal((1, h * d))
+    b = np.zeros((1, n, h))
+    b[0, 7, :] = 50.0
+    got = oracle.attend(q, k, v, gp, b, None, h, d)
+    ref = (1.0 / (1.0 + np.exp(-gp))) * v[7][None, :]
+    # every other key's weight is below exp(-50 + spread of q.k/sqrt(d)) < exp(-40)
+    tol = (n * np.exp(-40.0) + 1e-15) * np.max(np.abs(v))
+    assert np.max(np.abs(got - ref)) <= tol
+
+
+def pin_all_masked_is_zero():
+    s, z, w, _ = _case(11, n=6, h=2, d=3)
+    got = oracle.attention(s, z, np.arange(6), np.zeros(6, np.uint8), w, 2, 3)
+    assert np.all(got == 0.0)
+    got4 = oracle.attention(s, z, np.arange(6), np.zeros(6, np.uint8), w, 2, 3, n_blocks=3)
+    assert np.all(got4 == 0.0)
+
+
+# ----------------------------------------------------------------------------- invariants
+def pin_blocked_equals_unblocked():
+    s, z, w, mask = _case(12, n=17, h=3, d=4, mask_frac=0.2)
+    mask[:6] = 0  # first blocks entirely masked for several partitions
+    rows = np.arange(17)
+    ref = oracle.attention(s, z, rows, mask, w, 3, 4)
+    for nb in (2, 3, 5, 17):
+        got, (pm, pl, pa) = oracle.attention(s, z, rows, mask, w, 3, 4, n_blocks=nb, return_parts=True)
+        assert _rel(got, ref) <= 1e-12, (nb, _rel(got, ref))
+        # each partial's maximum is the block's largest logit (torch logits)
+        assert pm.shape == (nb, 3, 17)
+        assert np.all(pl[np.isneginf(pm)] == 0.0)
+
+
+def pin_partial_state_torch():
+    """Per-block (m, l, acc) against the torch logits of the same block."""
+    s, z, w, mask = _case(13, n=8, h=2, d=3, mask_frac=0.25)
+    rows = np.arange(8)
+    nb = 3
+    _, (pm, pl, pa) = oracle.attention(s, z, rows, mask, w, 2, 3, n_blocks=nb, return_parts=True)
+    S, Z = torch.from_numpy(s.astype(np.float64)), torch.from_numpy(z.astype(np.float64))
+    q = F.linear(S, torch.from_numpy(w["w_q"].astype(np.float64))).view(8, 2, 3)
+    k = F.linear(S, torch.from_numpy(w["w_k"].astype(np.float64))).view(8, 2, 3)
+    v = F.linear(S, torch.from_numpy(w["w_v"].astype(np.float64))).view(8, 2, 3)
+    ln = F.layer_norm(Z, (8,), torch.from_numpy(w["ln_gamma"].astype(np.float64)),
+                      torch.from_numpy(w["ln_beta"].astype(np.float64)), 1e-5)
+    b = F.linear(ln, torch.from_numpy(w["w_b"].astype(np.float64)), torch.from_numpy(w["b_b"].astype(np.float64)))
+    logits = torch.einsum("ihe,jhe->hij", q, k) / np.sqrt(3.0) + b.permute(2, 0, 1)
+    logits = logits.masked_fill(torch.from_numpy(mask == 0)[None, None, :], float("-inf")).numpy()
+    vv = v.numpy()
+    for p in range(nb):
+        size, start = oracle.chunk(8, nb, p)
+        blk = logits[:, :, start:start + size]
+        m = blk.max(axis=2)
+        for h in range(2):
+            for i in range(8):
+                if np.isneginf(m[h, i]):
+                    assert np.isneginf(pm[p, h, i]) and pl[p, h, i] == 0.0
+                    continue
+                wts = np.exp(blk[h, i] - m[h, i])
+                assert abs(pm[p, h, i] - m[h, i]) <= 1e-12 * max(1.0, abs(m[h, i]))
+                assert abs(pl[p, h, i] - wts.sum()) <= 1e-12 * wts.sum()
+                acc = (wts[:, None] * vv[start:start + size, h, :]).sum(axis=0)
+                assert np.max(np.abs(pa[p, i, h] - acc)) <= 1e-12 * max(1.0, np.max(np.abs(acc)))
+
+
+def pin_merge_identity_and_split():
+    r = _rng(14)
+    n_rows, h, d = 4, 2, 3
+    m = r.standard_normal((3, h, n_rows)) * 3
+    l = r.random((3, h, n_rows)) + 0.5
+    acc = r.standard_normal((3, n_rows, h, d))
+    gate = r.random((n_rows, h * d))
+    m_ref, l_ref, a_ref, o_ref = oracle.merge(m, l, acc, gate)
+    # an empty partial (-inf, 0, 0) anywhere is the identity
+    m2 = np.concatenate([m[:1], np.full((1, h, n_rows), -np.inf), m[1:]])
+    l2 = np.concatenate([l[:1], np.zeros((1, h, n_rows)), l[1:]])
+    a2 = np.concatenate([acc[:1], np.zeros((1, n_rows, h, d)), acc[1:]])
+    _, _, _, o2 = oracle.merge(m2, l2, a2, gate)
+    assert _rel(o2, o_ref) <= 1e-15
+    # closed form of the merge: weights exp(m_p - max m)
+    M = m.max(axis=0)
+    wts = np.exp(m - M[None])
+    L = (wts * l).sum(axis=0)
+    A = (wts.transpose(0, 2, 1)[..., None] * acc).sum(axis=0)
+    assert _rel(l_ref, L) <= 1e-14 and np.array_equal(m_ref, M)
+    assert _rel(a_ref, A) <= 1e-14
+    O = gate * (A / L.T[:, :, None]).reshape(n_rows, h * d)
+    assert _rel(o_ref, O) <= 1e-14
+    # all-empty merge gives zeros
+    _, l0, _, o0 = oracle.merge(np.full((2, h, n_rows), -np.inf), np.zeros((2, h, n_rows)),
+                                np.zeros((2, n_rows, h, d)), gate)
+    assert np.all(o0 == 0.0) and np.all(l0 == 0.0)
+
+
+def pin_bias_row_constant():
+    """Adding c[i, h] to every key's bias leaves the output unchanged."""
+    r = _rng(15)
+    n_rows, n, h, d = 4, 9, 3, 2
+    q, k, v = r.standard_normal((n_rows, h * d)), r.standard_normal((n, h * d)), r.standard_normal((n, h * d))
+    gp, b = r.standard_normal((n_rows, h * d)), r.standard_normal((n_rows, n, h))
+    c = 5.0 * r.standard_normal((n_rows, 1, h))
+    mask = np.ones(n, np.uint8)
+    mask[3] = 0
+    a = oracle.attend(q, k, v, gp, b, mask, h, d)
+    b2 = oracle.attend(q, k, v, gp, b + c, mask, h, d)
+    assert _rel(b2, a) <= 1e-13
+
+
+def pin_affine_constants_irrelevant():
+    """beta and b_b add per-head constants to the bias, so the output ignores them."""
+    s, z, w, mask = _case(16, n=8, h=2, d=3)
+    w0 = dict(w, ln_beta=None, b_b=None)
+    a = oracle.attention(s, z, np.arange(8), mask, w, 2, 3)
+    b = oracle.attention(s, z, np.arange(8), mask, w0, 2, 3)
+    assert _rel(a, b) <= 1e-13
+    # ... but they do change the bias itself
+    assert np.max(np.abs(oracle.bias(z, w["w_b"], w["b_b"], w["ln_gamma"], w["ln_beta"])
+                         - oracle.bias(z, w["w_b"], None, w["ln_gamma"], None))) > 1e-3
+
+
+def pin_layer_norm_shift_scale():
+    r = _rng(17)
+    # values on a 1/64 grid so that the shifted and scaled inputs stay exact in fp32
+    zz = (np.round(r.standard_normal((3, 4, 8)) * 64) / 64).astype(np.float32)
+    wb = r.standard_normal((2, 8))
+    b0 = oracle.bias(zz, wb)
+    b_shift = oracle.bias((zz + np.float32(7.25)).astype(np.float32), wb)  # LN(z + c) = LN(z)
+    assert _rel(b_shift, b0) <= 1e-13
+    b_scale = oracle.bias((zz * np.float32(4.0)).astype(np.float32), wb, eps=1e-5 * 16)
+    assert _rel(b_scale, oracle.bias(zz, wb, eps=1e-5)) <= 1e-13
+
+
+def pin_permutation_equivariance():
+    s, z, w, mask = _case(18, n=10, h=2, d=3)
+    perm = _rng(19).permutation(10)
+    a = oracle.attention(s, z, np.arange(10), mask, w, 2, 3)
+    zp = np.ascontiguousarray(z[perm][:, perm])
+    b = oracle.attention(np.ascontiguousarray(s[perm]), zp, np.arange(10), mask[perm], w, 2, 3)
+    assert _rel(b, a[perm]) <= 1e-13
+
+
+def pin_masked_equals_deleted():
+    s, z, w, mask = _case(20, n=9, h=2, d=3, mask_frac=0.0)
+    mask = np.ones(9, np.uint8)
+    mask[[2, 5]] = 0
+    keep = np.flatnonzero(mask)
+    a = oracle.attention(s, z, np.arange(9), mask, w, 2, 3)
+    sub = oracle.attention(np.ascontiguousarray(s[keep]), np.ascontiguousarray(z[keep][:, keep]),
+                           np.arange(len(keep)), None, w, 2, 3)
+    assert _rel(a[keep], sub) <= 1e-13
+    z2 = z.copy()
+    z2[:, [2, 5], :] = 1e3 * _rng(21).standard_normal((9, 2, z.shape[2])).astype(np.float32)
+    b = oracle.attention(s, z2, np.arange(9), mask, w, 2, 3)
+    assert np.array_equal(a, b)
+
+
+# ----------------------------------------------------------------------------- brute force
+def pin_bruteforce_mpmath():
+    """The definition at 40 digits on tiny inputs."""
+    mpmath.mp.dps = 40
+    for seed, n, c_s, c_z, h, d in ((22, 4, 3, 5, 2, 3), (23, 5, 2, 6, 1, 4), (24, 3, 4, 3, 2, 2)):
+        s, z, w, mask = _case(seed, n=n, c_s=c_s, c_z=c_z, h=h, d=d, mask_frac=0.2)
+        got = oracle.attention(s, z, np.arange(n), mask, w, h, d)
+        M = lambda a: [[mpmath.mpf(float(x)) for x in row] for row in np.atleast_2d(a)]
+        S, Wq, Wk, Wv, Wg, Wb = (M(a) for a in (s, w["w_q"], w["w_k"], w["w_v"], w["w_g"], w["w_b"]))
+        gam = [mpmath.mpf(float(x)) for x in w["ln_gamma"]]
+        bet = [mpmath.mpf(float(x)) for x in w["ln_beta"]]
+        bb = [mpmath.mpf(float(x)) for x in w["b_b"]]
+        eps = mpmath.mpf(1e-5)
+        lin = lambda W, x: [mpmath.fsum(W[o][c] * x[c] for c in range(len(x))) for o in range(len(W))]
+        for i in range(n):
+            qi, gi = lin(Wq, S[i]), [1 / (1 + mpmath.exp(-t)) for t in lin(Wg, S[i])]
+            for hh in range(h):
+                logits = []
+                for j in range(n):
+                    if not mask[j]:
+                        continue
+                    zz = [mpmath.mpf(float(x)) for x in z[i, j]]
+                    mu = mpmath.fsum(zz) / c_z
+                    var = mpmath.fsum((x - mu) ** 2 for x in zz) / c_z
+                    lnv = [gam[c] * (zz[c] - mu) / mpmath.sqrt(var + eps) + bet[c] for c in range(c_z)]
+                    b = mpmath.fsum(Wb[hh][c] * lnv[c] for c in range(c_z)) + bb[hh]
+                    kj = lin(Wk, S[j])
+                    dot = mpmath.fsum(qi[hh * d + e] * kj[hh * d + e] for e in range(d))
+                    logits.append((j, dot / mpmath.sqrt(d) + b))
+                mx = max(x for _, x in logits)
+                wts = [(j, mpmath.exp(x - mx)) for j, x in logits]
+                den = mpmath.fsum(x for _, x in wts)
+                for e in range(d):
+                    num = mpmath.fsum(x * lin(Wv, S[j])[hh * d + e] for j, x in wts)
+                    ref = gi[hh * d + e] * num / den
+                    assert abs(float(ref) - got[i, hh * d + e]) <= 1e-13 * max(1.0, abs(float(ref))), (seed, i, hh, e)
+
+
+ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]
