@@ -1,0 +1,260 @@
+#!/usr/bin/env python3
+"""Benchmark of the pair-biased gated attention layer on one MI355X.
+
+One step = one full layer call (q/k/v/g projection, the fused LayerNorm-bias
+attention over all key blocks, the block merge) for every query stripe of the
+workload, with all inputs already resident in HBM. Default workload: the
+whole-assembly case, N = 24000 tokens (60 x 400), bf16 z[N, N, 128] = 147 GB,
+16 heads of width 24, 6 key blocks, last 480 tokens masked.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "ms/layer + achieved HBM GB/s (% peak) for pair-biased attention at N tokens"
+PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, published
+KERNEL_SOURCES = ("paper_2607_05439_amd/csrc/fast.hip", "paper_2607_05439_amd/csrc/cdna4.h")
+
+
+def progress(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+class Hip:
+    """hipEvent helpers (timing on the library's launch stream)."""
+
+    def __init__(self):
+        self.lib = ctypes.CDLL("libamdhip64.so")
+        self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def event(self):
+        ev = ctypes.c_void_p()
+        assert self.lib.hipEventCreate(ctypes.byref(ev)) == 0
+        return ev.value
+
+    def elapsed_ms(self, a, b):
+        assert self.lib.hipEventSynchronize(b) == 0
+        ms = ctypes.c_float()
+        assert self.lib.hipEventElapsedTime(ctypes.byref(ms), a, b) == 0
+        return ms.value
+
+    def record(self, ev, stream):
+        assert self.lib.hipEventRecord(ctypes.c_void_p(ev), ctypes.c_void_p(stream)) == 0
+
+    def destroy(self, ev):
+        self.lib.hipEventDestroy(ev)
+
+
+def kernel_source_sha():
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(workload):
+    """HBM bytes per launch from committed rocprofv3 counters, if they were
+    taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_attn_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("kernel_source_sha") != kernel_source_sha():
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(wl, s_host, w_host, mask, seconds):
+    """The fp64 oracle, as it stands, on a bounded sample of query rows;
+    extrapolated to the whole layer (fixed projection cost + N x per-row)."""
+    import numpy as np
+    import oracle
+    import synth
+    threads = ctypes.CDLL("libgomp.so.1").omp_get_max_threads()
+    s64 = oracle.decode(s_host)
+    t0 = time.perf_counter()
+    oracle.linear(s64, w_host["w_k"])
+    oracle.linear(s64, w_host["w_v"])
+    t_fixed = time.perf_counter() - t0
+    # first a small batch to size the sample, then the sample itself
+    rows = list(range(0, wl.n_tok, max(1, wl.n_tok // threads)))[:threads]
+    z = synth.z_host(wl, rows)
+    t0 = time.perf_counter()
+    oracle.attention(s_host, z, rows, mask, w_host, wl.n_heads, wl.head_dim)
+    t_small = time.perf_counter() - t0
+    per_row = max((t_small - t_fixed) / len(rows), 1e-9)
+    n_rows = int(min(wl.n_tok, max(len(rows), (seconds - t_small) / per_row)))
+    n_rows = max(threads, n_rows // threads * threads)
+    rng = np.random.default_rng(1)
+    rows = sorted(int(x) for x in rng.choice(wl.n_tok, size=min(n_rows, wl.n_tok), replace=False))
+    z = synth.z_host(wl, rows)
+    t0 = time.perf_counter()
+    oracle.attention(s_host, z, rows, mask, w_host, wl.n_heads, wl.head_dim)
+    t_run = time.perf_counter() - t0
+    per_row = (t_run - t_fixed) / len(rows)
+    n_q_total = sum(nq for _, nq in wl.stripes)
+    t_layer = t_fixed * len(wl.stripes) + per_row * n_q_total
+    return {"t_layer_s": t_layer, "rows": len(rows), "t_run_s": t_run, "threads": threads, "t_fixed_s": t_fixed}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="asm24000_bf16")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-bytes", type=int, default=1 << 31,
+                    help="bytes for the plain-copy calibration kernel (counter scaling)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(see DESIGN.md for how the layer would shard); run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2607_05439_amd as dcp
+    import synth
+
+    wl = synth.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    n, cz = wl.n_tok, wl.c_z
+    progress(f"workload {wl.name}: N={n} c_z={cz} H={wl.n_heads} d={wl.head_dim} n_kb={wl.n_key_blocks} "
+             f"z={n * n * cz * wl.elem_bytes / 1e9:.1f} GB")
+    zdt = torch.bfloat16 if wl.bf16 else torch.float32
+    z = torch.empty((n, n, cz), dtype=zdt, device=dev)
+    synth.z_fill_device(wl, z.data_ptr(), 0, n, sp)
+    s_host = synth.s_host(wl)
+    w_host = synth.weights(wl)
+    mask_host = synth.mask_host(wl)
+    if wl.bf16:
+        s = torch.from_numpy(s_host.view(np.int16)).view(torch.bfloat16).to(dev)
+    else:
+        s = torch.from_numpy(s_host).to(dev)
+    w = {k: (None if v is None else torch.from_numpy(v).to(dev)) for k, v in w_host.items()}
+    mask = None if mask_host is None else torch.from_numpy(mask_host).to(dev)
+    out_dtype = dcp.DCP_BF16 if wl.bf16 else dcp.DCP_F32
+    shape = dcp.make_shape(n, wl.c_s, cz, wl.n_heads, wl.head_dim, dcp.DCP_BF16 if wl.bf16 else dcp.DCP_F32,
+                           out_dtype, 1e-5)
+    weights = dcp.make_weights(w["w_q"], w["w_k"], w["w_v"], w["w_g"], w["w_b"], w["b_b"], w["ln_gamma"],
+                               w["ln_beta"])
+    hd = wl.n_heads * wl.head_dim
+    ws_bytes = max(dcp.dcp_workspace_size(shape, nq, wl.n_key_blocks) for _, nq in wl.stripes)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    outs = [torch.empty((nq, hd), dtype=torch.bfloat16 if wl.bf16 else torch.float32, device=dev)
+            for _, nq in wl.stripes]
+    n_valid = n if mask_host is None else int(mask_host.sum())
+    bytes_per_launch = [nq * n_valid * cz * wl.elem_bytes for _, nq in wl.stripes]
+    bytes_per_step = sum(bytes_per_launch)
+    torch.cuda.synchronize()
+
+    hip = Hip()
+
+    def step(evs=None):
+        for i, (q0, nq) in enumerate(wl.stripes):
+            if evs is not None:
+                dcp.dcp_set_timing_events(*evs[i])
+            dcp.dcp_pair_bias_attention(shape, weights, s, z.data_ptr() + q0 * n * cz * wl.elem_bytes, mask, q0,
+                                        nq, wl.n_key_blocks, outs[i], ws, ws_bytes, sp)
+        if evs is not None:
+            dcp.dcp_set_timing_events(None, None)
+
+    # calibration kernels (outside the timed region): a plain copy of known size
+    # for counter scaling, and a plain streaming read of z for achievable bandwidth
+    cal = min(args.calibrate_bytes, z.numel() * z.element_size() // 2 // 16 * 16)
+    sink = torch.zeros(4, dtype=torch.int32, device=dev)
+    e0, e1 = hip.event(), hip.event()
+    scratch = torch.empty(cal, dtype=torch.uint8, device=dev)
+    synth.device_copy(z.data_ptr(), scratch.data_ptr(), cal, sp)
+    torch.cuda.synchronize()
+    del scratch
+    read_bytes = z.numel() * z.element_size() // 16 * 16
+    synth.device_read(z.data_ptr(), read_bytes, sink.data_ptr(), sp)  # warm
+    torch.cuda.synchronize()
+    hip.record(e0, sp)
+    synth.device_read(z.data_ptr(), read_bytes, sink.data_ptr(), sp)
+    hip.record(e1, sp)
+    read_gbps = read_bytes / (hip.elapsed_ms(e0, e1) * 1e-3) / 1e9
+    progress(f"streaming read of z: {read_gbps:.0f} GB/s")
+
+    progress(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    kernel_evs = [[(hip.event(), hip.event()) for _ in wl.stripes] for _ in range(args.steps)]
+    progress(f"timing {args.steps} steps")
+    t_start, t_stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for k in range(args.steps):
+        step(kernel_evs[k])
+    t_stop.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t_start.elapsed_time(t_stop) / args.steps
+    k_ms = [hip.elapsed_ms(a, b) for evs in kernel_evs for (a, b) in evs]
+    avg_kernel_ms = sum(k_ms) / len(k_ms)
+    achieved = (bytes_per_step / len(wl.stripes)) / (avg_kernel_ms * 1e-3) / 1e9
+    value = bytes_per_step / (ms_per_step * 1e-3) / 1e9
+    progress(f"{ms_per_step:.3f} ms/layer, attention kernel {avg_kernel_ms:.3f} ms/launch, "
+             f"{achieved:.0f} GB/s in the kernel ({achieved / PEAK_HBM_GBPS:.1%} of peak)")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        progress(f"cpu baseline: oracle on sampled rows (~{args.cpu_seconds:.0f} s)")
+        cb = cpu_baseline(wl, s_host, w_host, mask_host, args.cpu_seconds)
+        cpu = {"value": round(bytes_per_step / cb["t_layer_s"] / 1e9, 6), "unit": "GB/s", "cores": cb["threads"],
+               "kind": "oracle",
+               "sample": f"{cb['rows']} of {sum(nq for _, nq in wl.stripes)} query rows in {cb['t_run_s']:.1f} s "
+                         f"(fp64, includes the k/v projection of all {n} keys, {cb['t_fixed_s']:.1f} s); "
+                         f"extrapolated layer time {cb['t_layer_s']:.1f} s",
+               "ms_per_layer_extrapolated": round(cb["t_layer_s"] * 1e3, 1)}
+
+    traffic = stored_traffic(wl.name)
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.bf16 else "f32",
+        "data": "synthetic (seeded; stands in for RFD3 icosahedral-assembly pair tensors)",
+        "config": {"workload": wl.name, "n_tokens": n, "valid_keys": n_valid, "c_s": wl.c_s, "c_z": cz,
+                   "n_heads": wl.n_heads, "head_dim": wl.head_dim, "n_key_blocks": wl.n_key_blocks,
+                   "stripes": [list(x) for x in wl.stripes], "z_bytes": n * n * cz * wl.elem_bytes,
+                   "algorithmic_bytes_per_step": bytes_per_step},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic,
+                     "kernel": "attn_kernel", "kernel_ms": round(avg_kernel_ms, 4),
+                     "algorithmic_bytes_per_launch": bytes_per_launch[0]},
+        "streaming_read_GBps": round(read_gbps, 1),
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,162 @@
+/* dcp.h -- pair-biased, gated multi-head attention on one AMD MI355X (gfx950).
+ *
+ * The operation (paper: Design-CP, arXiv 2607.05439):
+ *   Methods, "RFDiffusion 3 preliminaries and notation": inside every
+ *   token-level attention block a learned projection of the pair track Z gives
+ *   a per-head bias B that is added to the logits, softmax(Q K^T / sqrt(d) + B).
+ *   Methods, "1D row-sharding", Eq. (cross_attn): a stripe of query rows
+ *   attends to keys and values projected from the full single track S, with
+ *   the bias drawn from the stripe's own rows of Z.
+ *   Methods, "2D grid context parallelism", and Appendix "Q/K/V layout and the
+ *   ring loop": keys are visited block by block and each block's partial
+ *   result is folded into a running total with an online softmax.
+ * Readings where the paper is silent: the projection is
+ *   b[i,j,h] = sum_c W_b[h,c] LayerNorm(z[i,j,:])_c + b_b[h]
+ * (biased variance, eps inside the square root, affine gamma/beta over c_z),
+ * and the output is gated, out_i = sigmoid(W_g s_i) * attention_i.
+ *
+ * For query rows i in [q_row0, q_row0 + n_q) and heads h (flat index h*d + e):
+ *   q_i = W_q s_i, k_j = W_k s_j, v_j = W_v s_j, g_i = sigmoid(W_g s_i),
+ *   l[h,i,j] = q_{i,h} . k_{j,h} / sqrt(d) + b[i,j,h]   (-inf for a masked key),
+ *   out[i - q_row0, h*d + e] = g_i[h*d+e] * sum_j softmax_j(l[h,i,:]) v_{j,h,e};
+ *   a row whose keys are all masked gives 0.
+ *
+ * Conventions for every entry point:
+ *  - Tensor pointers are DEVICE pointers owned by the caller; the descriptor
+ *    structs are host memory read during the call only. The library never
+ *    allocates or frees memory: scratch comes from `workspace`.
+ *  - Calls are asynchronous on `stream` (a hipStream_t passed as void*, NULL =
+ *    the null stream) and never synchronise. All arguments are validated on
+ *    the host before anything is launched; a non-OK status means nothing was
+ *    launched (DCP_ERR_HIP: a launch failed after validation) and
+ *    dcp_last_error() describes it. No C++ exception crosses this interface.
+ *  - Layouts are row-major and contiguous; weights are fp32 in nn.Linear layout
+ *    [out_features, in_features].
+ *  - NaN or Inf in unmasked inputs propagate to the outputs; masked keys' s and
+ *    z are never read into the result.
+ *  - Results are deterministic: the same call on the same inputs gives the
+ *    same bits (no atomics, fixed reduction order).
+ */
+#ifndef DCP_H
+#define DCP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { DCP_F32 = 0, DCP_BF16 = 1 } dcp_dtype;
+
+enum {
+  DCP_OK = 0,
+  DCP_ERR_INVALID_ARGUMENT = -1, /* null/misaligned pointer, bad size or range      */
+  DCP_ERR_UNSUPPORTED = -2,      /* shape/dtype combination not built (see below)  */
+  DCP_ERR_WORKSPACE = -3,        /* workspace missing, misaligned or too small     */
+  DCP_ERR_HIP = -4               /* a kernel launch failed                         */
+};
+
+typedef struct {
+  int64_t n_tokens;  /* N: rows of s, number of keys, columns of z                */
+  int32_t c_s;       /* single-track channels                                     */
+  int32_t c_z;       /* pair-track channels                                       */
+  int32_t n_heads;   /* H                                                         */
+  int32_t head_dim;  /* d                                                         */
+  int32_t act_dtype; /* dcp_dtype of s and z                                      */
+  int32_t out_dtype; /* dcp_dtype of out                                          */
+  float ln_eps;      /* LayerNorm epsilon (PyTorch default 1e-5), >= 0            */
+} dcp_shape;
+
+typedef struct {
+  const float* w_q;      /* [H*d, c_s]                                            */
+  const float* w_k;      /* [H*d, c_s]                                            */
+  const float* w_v;      /* [H*d, c_s]                                            */
+  const float* w_g;      /* [H*d, c_s]                                            */
+  const float* w_b;      /* [H, c_z]                                              */
+  const float* b_b;      /* [H] or NULL (= 0)                                     */
+  const float* ln_gamma; /* [c_z] or NULL (= 1)                                   */
+  const float* ln_beta;  /* [c_z] or NULL (= 0)                                   */
+} dcp_weights;
+
+/* Supported shapes. A fused MFMA path serves act_dtype = BF16 with c_z = 128,
+ * H = 16, d = 24 and c_s a multiple of 32 (at most 4096). A general fp32 path
+ * serves every other combination with c_z <= 256, H <= 16, d <= 64,
+ * H*d <= 128 and c_s <= 4096, for either act_dtype. Anything else returns
+ * DCP_ERR_UNSUPPORTED. */
+
+/* Workspace bytes that dcp_pair_bias_attention needs for these arguments
+ * (written to *bytes). Host-only; launches nothing. */
+int dcp_workspace_size(const dcp_shape* shape, int64_t n_q, int32_t n_key_blocks, size_t* bytes);
+
+/* Pair-biased gated attention of the query stripe [q_row0, q_row0 + n_q)
+ * against all N keys (Methods, Eq. (cross_attn)).
+ *   s           [N, c_s] act_dtype, 16-byte aligned
+ *   z_rows      [n_q, N, c_z] act_dtype: the stripe's rows of z, i.e.
+ *               &z[q_row0, 0, 0] of a contiguous z[N, N, c_z]; 16-byte aligned
+ *   key_mask    [N] uint8, 1 = attend, 0 = masked; NULL = every key attends
+ *   n_q         0 <= n_q, q_row0 >= 0, q_row0 + n_q <= N (n_q = 0 is a no-op)
+ *   n_key_blocks in [1, N]: keys are split into this many blocks by the
+ *               paper's chunk rule (Appendix "Chunk distribution algorithm":
+ *               block p has floor(N/P) + [p < N mod P] keys) and the blocks'
+ *               partial states are merged in increasing order, as the ring
+ *               steps of the paper's 2D scheme do. Any value gives the same
+ *               result up to fp32 rounding order.
+ *   out         [n_q, H*d] out_dtype, 16-byte aligned
+ *   workspace   device scratch of at least dcp_workspace_size() bytes,
+ *               256-byte aligned; contents on entry are ignored.
+ * The gate and softmax statistics are fp32. On the fused bf16 path, z, s and
+ * the projected q, k, v, the softmax weights and the bias weights enter the
+ * matrix cores as bf16 (the bias weights as a bf16 hi+lo pair) with fp32
+ * accumulation. */
+int dcp_pair_bias_attention(const dcp_shape* shape, const dcp_weights* weights, const void* s,
+                            const void* z_rows, const uint8_t* key_mask, int64_t q_row0, int64_t n_q,
+                            int32_t n_key_blocks, void* out, void* workspace, size_t workspace_bytes,
+                            void* stream);
+
+/* The pair bias alone (Methods, "RFDiffusion 3 preliminaries and notation":
+ * B = f_B(Z)), materialised: bias_out[r, c, h] = sum_k W_b[h,k] LN(z_tile[r, c, :])_k + b_b[h]
+ * including gamma, beta and b_b, for r < n_rows, c < n_cols. Pair (r, c) is
+ * read at z_tile + (r*row_stride_elems + c*c_z) elements (row_stride_elems >=
+ * n_cols*c_z; it is N*c_z for a tile of a full z). bias_out is fp32 [n_rows,
+ * n_cols, H], contiguous and 16-byte aligned. Only w_b, b_b, ln_gamma and
+ * ln_beta of `weights` are read; c_s, head_dim, out_dtype and n_tokens of
+ * `shape` are ignored. Needs no workspace. n_rows = 0 or n_cols = 0 is a no-op. */
+int dcp_bias_project(const dcp_shape* shape, const dcp_weights* weights, const void* z_tile, int64_t n_rows,
+                     int64_t n_cols, int64_t row_stride_elems, float* bias_out, void* stream);
+
+/* Online-softmax merge of partial attention states, in increasing part order
+ * (Appendix "Q/K/V layout and the ring loop": each ring step's partial output
+ * is merged into a running total; Related Work, "IO-efficient attention").
+ * A partial over a key subset K_p holds m = max_{j in K_p} l_j (natural log
+ * units), l = sum exp(l_j - m) and acc = sum exp(l_j - m) v_j; (-inf, 0, 0) is
+ * the empty partial.
+ *   m_parts, l_parts  [n_parts, H, n_rows] fp32
+ *   acc_parts         [n_parts, n_rows, H, d] fp32
+ *   m_out, l_out      [H, n_rows] fp32, or NULL
+ *   acc_out           [n_rows, H, d] fp32 (unnormalised), or NULL
+ *   gate              [n_rows, H*d] fp32 (already sigmoid), or NULL (= 1)
+ *   out               [n_rows, H*d] out_dtype = gate * acc / l (0 where l = 0), or NULL
+ * Limits: 1 <= n_parts, 1 <= H, 1 <= d, H*d <= 4096. n_rows = 0 is a no-op.
+ * Output buffers must not overlap the inputs. */
+int dcp_block_merge(int32_t n_parts, int64_t n_rows, int32_t n_heads, int32_t head_dim, const float* m_parts,
+                    const float* l_parts, const float* acc_parts, float* m_out, float* l_out, float* acc_out,
+                    const float* gate, void* out, int32_t out_dtype, void* stream);
+
+/* Optional timing hook: when both are non-NULL hipEvent_t handles, the calling
+ * thread's next dcp_pair_bias_attention calls record `start` just before and
+ * `stop` just after the fused attention kernel, on that call's stream. Pass
+ * NULL, NULL to clear. Host-only. */
+int dcp_set_timing_events(void* start_event, void* stop_event);
+
+/* Message for the calling thread's last non-OK status ("" if none). */
+const char* dcp_last_error(void);
+
+/* Library version string. */
+const char* dcp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DCP_H */

@@ -1,0 +1,85 @@
+// CDNA4 (gfx950) building blocks shared by the fused kernels: vector types,
+// matrix-core wrappers, cross-lane exchanges and the bias-tile transpose.
+//
+// Matrix-core layouts (64 lanes, lane L, n = L % 16, g = L / 16):
+// v_mfma_f32_16x16x32_bf16: A holds row n, k-slots 8g..8g+7; B holds column n,
+// k-slots 8g..8g+7; the accumulator holds rows 4g..4g+3 of column n.
+// v_mfma_f32_16x16x16_bf16: the same with k-slots 4g..4g+3.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dcp {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 u) { return __builtin_bit_cast(bf16x8, u); }
+__device__ __forceinline__ bf16x4 as_bf16x4(u32x2 u) { return __builtin_bit_cast(bf16x4, u); }
+__device__ __forceinline__ bf16x2 as_bf16x2(uint32_t u) { return __builtin_bit_cast(bf16x2, u); }
+
+__device__ __forceinline__ f32x4 mfma32(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma16(bf16x4 a, bf16x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+
+// Exchange between lane halves: x's lanes 32..63 <-> y's lanes 0..31.
+__device__ __forceinline__ void swap32(float& x, float& y) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+  x = __uint_as_float(r[0]);
+  y = __uint_as_float(r[1]);
+}
+// Exchange between 16-lane rows: x's odd rows <-> y's even rows.
+__device__ __forceinline__ void swap16(float& x, float& y) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+  x = __uint_as_float(r[0]);
+  y = __uint_as_float(r[1]);
+}
+
+// Sum / max over the four lanes n, n+16, n+32, n+48; every lane gets the same bits.
+__device__ __forceinline__ float sum4(float x) {
+  float a = x, b = x;
+  swap32(a, b);
+  x = a + b;
+  a = x;
+  b = x;
+  swap16(a, b);
+  return a + b;
+}
+__device__ __forceinline__ float max4(float x) {
+  float a = x, b = x;
+  swap32(a, b);
+  x = fmaxf(a, b);
+  a = x;
+  b = x;
+  swap16(a, b);
+  return fmaxf(a, b);
+}
+
+// b[k][i] holds (row n, head 4g+i, key k) for the tile's 16 keys. After this,
+// b[4a + r][i] holds (row n, head 4a+i, key 4g+r): the QK^T accumulator layout
+// of head 4a+i. A 4x4 exchange of 4x4 blocks between the lane groups, done
+// with two rounds of cross-lane swaps (bit 1 of the group, then bit 0).
+__device__ __forceinline__ void transpose_bias(float (&b)[16][4]) {
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) swap32(b[4 * c + r][i], b[4 * (c + 2) + r][i]);
+#pragma unroll
+  for (int c = 0; c < 4; c += 2)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) swap16(b[4 * c + r][i], b[4 * (c + 1) + r][i]);
+}
+
+}  // namespace dcp

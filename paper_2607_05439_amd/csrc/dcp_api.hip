@@ -1,0 +1,388 @@
+// C-ABI of the library (include/dcp.h): argument validation, workspace
+// layout, path selection and kernel launches. Every check runs on the host
+// before the first launch, so a rejected call touches neither the GPU nor the
+// HIP runtime.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+
+#include "dcp.h"
+#include "dcp_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+thread_local void* g_ev_start = nullptr;
+thread_local void* g_ev_stop = nullptr;
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int ok() {
+  g_err[0] = '\0';
+  return DCP_OK;
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+enum Path { kPathFast, kPathGeneric };
+
+int check_shape(const dcp_shape* sh) {
+  if (!sh) return fail(DCP_ERR_INVALID_ARGUMENT, "shape is NULL");
+  if (sh->n_tokens < 1) return fail(DCP_ERR_INVALID_ARGUMENT, "n_tokens must be >= 1 (got %lld)", (long long)sh->n_tokens);
+  if (sh->c_s < 1 || sh->c_z < 1 || sh->n_heads < 1 || sh->head_dim < 1)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "c_s, c_z, n_heads and head_dim must be >= 1");
+  if ((sh->act_dtype != DCP_F32 && sh->act_dtype != DCP_BF16) || (sh->out_dtype != DCP_F32 && sh->out_dtype != DCP_BF16))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "act_dtype and out_dtype must be DCP_F32 or DCP_BF16");
+  if (!(sh->ln_eps >= 0.0f) || !isfinite(sh->ln_eps)) return fail(DCP_ERR_INVALID_ARGUMENT, "ln_eps must be finite and >= 0");
+  if (sh->n_tokens > (int64_t)1 << 40) return fail(DCP_ERR_INVALID_ARGUMENT, "n_tokens too large");
+  return DCP_OK;
+}
+
+int pick_path(const dcp_shape* sh, Path* p) {
+  if (sh->act_dtype == DCP_BF16 && sh->c_z == dcp::kFastCz && sh->n_heads == dcp::kFastH &&
+      sh->head_dim == dcp::kFastD && sh->c_s % 32 == 0 && sh->c_s <= dcp::kMaxCs) {
+    *p = kPathFast;
+    return DCP_OK;
+  }
+  if (sh->c_z <= dcp::kGenMaxCz && sh->n_heads <= dcp::kGenMaxH && sh->head_dim <= dcp::kGenMaxD &&
+      sh->n_heads * sh->head_dim <= dcp::kGenMaxHD && sh->c_s <= dcp::kMaxCs) {
+    *p = kPathGeneric;
+    return DCP_OK;
+  }
+  return fail(DCP_ERR_UNSUPPORTED,
+              "unsupported shape (dtype %d, c_s %d, c_z %d, H %d, d %d): the fused path needs bf16, c_z=128, "
+              "H=16, d=24, c_s%%32==0; the general path needs c_z<=256, H<=16, d<=64, H*d<=128, c_s<=4096",
+              sh->act_dtype, sh->c_s, sh->c_z, sh->n_heads, sh->head_dim);
+}
+
+// Segments per key block on the fused path: enough waves to give every SIMD
+// several, without segments shorter than 64 keys.
+int fast_segments(int64_t n_tok, int64_t n_q, int32_t n_kb) {
+  const int64_t waves = (n_q + dcp::kTileQ - 1) / dcp::kTileQ * (int64_t)n_kb;
+  const int64_t target = 4 * 1024;
+  int64_t seg = (target + waves - 1) / waves;
+  const int64_t min_block = n_tok / n_kb;
+  int64_t cap = min_block / 64;
+  if (cap < 1) cap = 1;
+  if (seg > cap) seg = cap;
+  if (seg > 64) seg = 64;
+  if (seg < 1) seg = 1;
+  return (int)seg;
+}
+
+struct Layout {
+  Path path;
+  int n_seg, n_parts;
+  int64_t nq_pad, n_pad;
+  size_t off_q, off_k, off_v, off_g, off_m, off_l, off_acc, total;
+};
+
+void make_layout(const dcp_shape* sh, Path path, int64_t n_q, int32_t n_kb, Layout* L) {
+  const int64_t hd = (int64_t)sh->n_heads * sh->head_dim;
+  L->path = path;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = round_up(off + bytes, 256);
+    return o;
+  };
+  if (path == kPathFast) {
+    L->n_seg = fast_segments(sh->n_tokens, n_q, n_kb);
+    L->n_parts = n_kb * L->n_seg;
+    L->nq_pad = (n_q + 15) / 16 * 16;
+    L->n_pad = (sh->n_tokens + 15) / 16 * 16;
+    L->off_q = take((size_t)dcp::kFastH * L->nq_pad * dcp::kFastDp * 2);
+    L->off_k = take((size_t)dcp::kFastH * L->n_pad * dcp::kFastDp * 2);
+    L->off_v = take((size_t)dcp::kFastH * L->n_pad * dcp::kFastDp * 2);
+  } else {
+    L->n_seg = 1;
+    L->n_parts = n_kb;
+    L->nq_pad = n_q;
+    L->n_pad = sh->n_tokens;
+    L->off_q = take((size_t)n_q * hd * 4);
+    L->off_k = take((size_t)sh->n_tokens * hd * 4);
+    L->off_v = take((size_t)sh->n_tokens * hd * 4);
+  }
+  L->off_g = take((size_t)n_q * hd * 4);
+  L->off_m = take((size_t)L->n_parts * sh->n_heads * n_q * 4);
+  L->off_l = take((size_t)L->n_parts * sh->n_heads * n_q * 4);
+  L->off_acc = take((size_t)L->n_parts * n_q * hd * 4);
+  L->total = off;
+}
+
+int check_call(const dcp_shape* sh, int64_t n_q, int32_t n_kb, Path* path) {
+  int rc = check_shape(sh);
+  if (rc) return rc;
+  if (n_q < 0) return fail(DCP_ERR_INVALID_ARGUMENT, "n_q must be >= 0 (got %lld)", (long long)n_q);
+  if (n_q > sh->n_tokens) return fail(DCP_ERR_INVALID_ARGUMENT, "n_q exceeds n_tokens");
+  if (n_kb < 1 || n_kb > sh->n_tokens)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "n_key_blocks must be in [1, n_tokens] (got %d)", n_kb);
+  return pick_path(sh, path);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dcp_last_error(void) { return g_err; }
+
+const char* dcp_version(void) { return "dcp-mi355x 0.1 (gfx950)"; }
+
+int dcp_set_timing_events(void* start_event, void* stop_event) {
+  if ((start_event == nullptr) != (stop_event == nullptr))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "timing events must both be set or both be NULL");
+  g_ev_start = start_event;
+  g_ev_stop = stop_event;
+  return ok();
+}
+
+int dcp_workspace_size(const dcp_shape* shape, int64_t n_q, int32_t n_key_blocks, size_t* bytes) {
+  if (!bytes) return fail(DCP_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  Path path;
+  const int rc = check_call(shape, n_q, n_key_blocks, &path);
+  if (rc) return rc;
+  if (n_q == 0) {
+    *bytes = 0;
+    return ok();
+  }
+  Layout L;
+  make_layout(shape, path, n_q, n_key_blocks, &L);
+  *bytes = L.total;
+  return ok();
+}
+
+int dcp_pair_bias_attention(const dcp_shape* shape, const dcp_weights* w, const void* s, const void* z_rows,
+                            const uint8_t* key_mask, int64_t q_row0, int64_t n_q, int32_t n_key_blocks, void* out,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  Path path;
+  int rc = check_call(shape, n_q, n_key_blocks, &path);
+  if (rc) return rc;
+  if (q_row0 < 0 || q_row0 > shape->n_tokens - n_q)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "need 0 <= q_row0 and q_row0 + n_q <= n_tokens (q_row0 %lld, n_q %lld)",
+                (long long)q_row0, (long long)n_q);
+  if (!w) return fail(DCP_ERR_INVALID_ARGUMENT, "weights is NULL");
+  if (!w->w_q || !w->w_k || !w->w_v || !w->w_g || !w->w_b)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "w_q, w_k, w_v, w_g and w_b are required");
+  if (!s || !z_rows || !out) return fail(DCP_ERR_INVALID_ARGUMENT, "s, z_rows and out are required");
+  if (n_q == 0) return ok();
+  if (!aligned(s, 16) || !aligned(z_rows, 16) || !aligned(out, 16))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "s, z_rows and out must be 16-byte aligned");
+  if (path == kPathFast && (!aligned(w->w_q, 16) || !aligned(w->w_k, 16) || !aligned(w->w_v, 16) ||
+                            !aligned(w->w_g, 16)))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "w_q, w_k, w_v and w_g must be 16-byte aligned");
+  Layout L;
+  make_layout(shape, path, n_q, n_key_blocks, &L);
+  if (!workspace || !aligned(workspace, 256))
+    return fail(DCP_ERR_WORKSPACE, "workspace must be a 256-byte aligned device pointer");
+  if (workspace_bytes < L.total)
+    return fail(DCP_ERR_WORKSPACE, "workspace too small: %zu bytes given, %zu needed", workspace_bytes, L.total);
+
+  char* ws = static_cast<char*>(workspace);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t N = shape->n_tokens;
+  const int hd = shape->n_heads * shape->head_dim;
+  const bool act_bf16 = shape->act_dtype == DCP_BF16;
+  hipError_t e;
+  const int32_t log2_units = path == kPathFast ? 1 : 0;
+  if (path == kPathFast) {
+    dcp::FastProjArgs pa{};
+    pa.s = static_cast<const uint16_t*>(s);
+    pa.w_q = w->w_q;
+    pa.w_k = w->w_k;
+    pa.w_v = w->w_v;
+    pa.w_g = w->w_g;
+    pa.mask = key_mask;
+    pa.n_tok = N;
+    pa.q_row0 = q_row0;
+    pa.n_q = n_q;
+    pa.nq_pad = L.nq_pad;
+    pa.n_pad = L.n_pad;
+    pa.c_s = shape->c_s;
+    pa.q = reinterpret_cast<uint16_t*>(ws + L.off_q);
+    pa.k = reinterpret_cast<uint16_t*>(ws + L.off_k);
+    pa.vt = reinterpret_cast<uint16_t*>(ws + L.off_v);
+    pa.g = reinterpret_cast<float*>(ws + L.off_g);
+    if ((e = dcp::launch_fast_proj(pa, st)) != hipSuccess)
+      return fail(DCP_ERR_HIP, "projection launch failed: %s", hipGetErrorString(e));
+    dcp::FastAttnArgs aa{};
+    aa.z = static_cast<const uint16_t*>(z_rows);
+    aa.mask = key_mask;
+    aa.w_b = w->w_b;
+    aa.gamma = w->ln_gamma;
+    aa.q = pa.q;
+    aa.k = pa.k;
+    aa.vt = pa.vt;
+    aa.n_tok = N;
+    aa.n_q = n_q;
+    aa.nq_pad = L.nq_pad;
+    aa.n_pad = L.n_pad;
+    aa.n_kb = n_key_blocks;
+    aa.n_seg = L.n_seg;
+    aa.eps = shape->ln_eps;
+    aa.m_parts = reinterpret_cast<float*>(ws + L.off_m);
+    aa.l_parts = reinterpret_cast<float*>(ws + L.off_l);
+    aa.acc_parts = reinterpret_cast<float*>(ws + L.off_acc);
+    if (g_ev_start && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_start), st)) != hipSuccess)
+      return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
+    if ((e = dcp::launch_fast_attn(aa, st)) != hipSuccess)
+      return fail(DCP_ERR_HIP, "attention launch failed: %s", hipGetErrorString(e));
+    if (g_ev_stop && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_stop), st)) != hipSuccess)
+      return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
+  } else {
+    dcp::GenProjArgs pa{};
+    pa.s = s;
+    pa.s_bf16 = act_bf16;
+    pa.w_q = w->w_q;
+    pa.w_k = w->w_k;
+    pa.w_v = w->w_v;
+    pa.w_g = w->w_g;
+    pa.n_tok = N;
+    pa.q_row0 = q_row0;
+    pa.n_q = n_q;
+    pa.c_s = shape->c_s;
+    pa.hd = hd;
+    pa.q = reinterpret_cast<float*>(ws + L.off_q);
+    pa.k = reinterpret_cast<float*>(ws + L.off_k);
+    pa.v = reinterpret_cast<float*>(ws + L.off_v);
+    pa.g = reinterpret_cast<float*>(ws + L.off_g);
+    if ((e = dcp::launch_gen_proj(pa, st)) != hipSuccess)
+      return fail(DCP_ERR_HIP, "projection launch failed: %s", hipGetErrorString(e));
+    dcp::GenAttnArgs aa{};
+    aa.z = z_rows;
+    aa.z_bf16 = act_bf16;
+    aa.mask = key_mask;
+    aa.w_b = w->w_b;
+    aa.gamma = w->ln_gamma;
+    aa.q = pa.q;
+    aa.k = pa.k;
+    aa.v = pa.v;
+    aa.n_tok = N;
+    aa.n_q = n_q;
+    aa.c_z = shape->c_z;
+    aa.n_heads = shape->n_heads;
+    aa.head_dim = shape->head_dim;
+    aa.n_kb = n_key_blocks;
+    aa.eps = shape->ln_eps;
+    aa.m_parts = reinterpret_cast<float*>(ws + L.off_m);
+    aa.l_parts = reinterpret_cast<float*>(ws + L.off_l);
+    aa.acc_parts = reinterpret_cast<float*>(ws + L.off_acc);
+    if (g_ev_start && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_start), st)) != hipSuccess)
+      return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
+    if ((e = dcp::launch_gen_attn(aa, st)) != hipSuccess)
+      return fail(DCP_ERR_HIP, "attention launch failed: %s", hipGetErrorString(e));
+    if (g_ev_stop && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_stop), st)) != hipSuccess)
+      return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
+  }
+  dcp::MergeArgs ma{};
+  ma.n_parts = L.n_parts;
+  ma.n_heads = shape->n_heads;
+  ma.head_dim = shape->head_dim;
+  ma.n_rows = n_q;
+  ma.m = reinterpret_cast<const float*>(ws + L.off_m);
+  ma.l = reinterpret_cast<const float*>(ws + L.off_l);
+  ma.acc = reinterpret_cast<const float*>(ws + L.off_acc);
+  ma.gate = reinterpret_cast<const float*>(ws + L.off_g);
+  ma.out = out;
+  ma.out_bf16 = shape->out_dtype == DCP_BF16;
+  ma.log2_units = log2_units;
+  if ((e = dcp::launch_merge(ma, st)) != hipSuccess)
+    return fail(DCP_ERR_HIP, "merge launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int dcp_bias_project(const dcp_shape* shape, const dcp_weights* w, const void* z_tile, int64_t n_rows, int64_t n_cols,
+                     int64_t row_stride_elems, float* bias_out, void* stream) {
+  if (!shape) return fail(DCP_ERR_INVALID_ARGUMENT, "shape is NULL");
+  if (shape->c_z < 1 || shape->n_heads < 1) return fail(DCP_ERR_INVALID_ARGUMENT, "c_z and n_heads must be >= 1");
+  if (shape->act_dtype != DCP_F32 && shape->act_dtype != DCP_BF16)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "act_dtype must be DCP_F32 or DCP_BF16");
+  if (!(shape->ln_eps >= 0.0f) || !isfinite(shape->ln_eps)) return fail(DCP_ERR_INVALID_ARGUMENT, "ln_eps must be finite and >= 0");
+  if (n_rows < 0 || n_cols < 0) return fail(DCP_ERR_INVALID_ARGUMENT, "n_rows and n_cols must be >= 0");
+  if (!w || !w->w_b) return fail(DCP_ERR_INVALID_ARGUMENT, "w_b is required");
+  if (!z_tile || !bias_out) return fail(DCP_ERR_INVALID_ARGUMENT, "z_tile and bias_out are required");
+  if (row_stride_elems < n_cols * (int64_t)shape->c_z)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "row_stride_elems must be >= n_cols * c_z");
+  const bool fast = shape->act_dtype == DCP_BF16 && shape->c_z == dcp::kFastCz && shape->n_heads == dcp::kFastH;
+  if (!fast && (shape->c_z > dcp::kGenMaxCz || shape->n_heads > dcp::kGenMaxH))
+    return fail(DCP_ERR_UNSUPPORTED, "unsupported bias shape (c_z %d, H %d)", shape->c_z, shape->n_heads);
+  if (n_rows == 0 || n_cols == 0) return ok();
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  if (fast) {
+    if (!aligned(z_tile, 16) || !aligned(bias_out, 16) || row_stride_elems % 8 != 0)
+      return fail(DCP_ERR_INVALID_ARGUMENT, "z_tile and bias_out must be 16-byte aligned, row_stride_elems a multiple of 8");
+    dcp::FastBiasArgs a{};
+    a.z = static_cast<const uint16_t*>(z_tile);
+    a.w_b = w->w_b;
+    a.b_b = w->b_b;
+    a.gamma = w->ln_gamma;
+    a.beta = w->ln_beta;
+    a.n_rows = n_rows;
+    a.n_cols = n_cols;
+    a.row_stride = row_stride_elems;
+    a.cols_per_wave = 64;
+    a.eps = shape->ln_eps;
+    a.out = bias_out;
+    e = dcp::launch_fast_bias(a, st);
+  } else {
+    if (!aligned(bias_out, 4)) return fail(DCP_ERR_INVALID_ARGUMENT, "bias_out must be 4-byte aligned");
+    dcp::GenBiasArgs a{};
+    a.z = z_tile;
+    a.z_bf16 = shape->act_dtype == DCP_BF16;
+    a.w_b = w->w_b;
+    a.b_b = w->b_b;
+    a.gamma = w->ln_gamma;
+    a.beta = w->ln_beta;
+    a.n_rows = n_rows;
+    a.n_cols = n_cols;
+    a.row_stride = row_stride_elems;
+    a.c_z = shape->c_z;
+    a.n_heads = shape->n_heads;
+    a.eps = shape->ln_eps;
+    a.out = bias_out;
+    e = dcp::launch_gen_bias(a, st);
+  }
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "bias launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int dcp_block_merge(int32_t n_parts, int64_t n_rows, int32_t n_heads, int32_t head_dim, const float* m_parts,
+                    const float* l_parts, const float* acc_parts, float* m_out, float* l_out, float* acc_out,
+                    const float* gate, void* out, int32_t out_dtype, void* stream) {
+  if (n_parts < 1 || n_heads < 1 || head_dim < 1 || n_rows < 0)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "need n_parts, n_heads, head_dim >= 1 and n_rows >= 0");
+  if ((int64_t)n_heads * head_dim > 4096) return fail(DCP_ERR_UNSUPPORTED, "H*d must be <= 4096");
+  if (out_dtype != DCP_F32 && out_dtype != DCP_BF16)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "out_dtype must be DCP_F32 or DCP_BF16");
+  if (!m_parts || !l_parts || !acc_parts) return fail(DCP_ERR_INVALID_ARGUMENT, "m_parts, l_parts and acc_parts are required");
+  if (n_rows == 0) return ok();
+  dcp::MergeArgs a{};
+  a.n_parts = n_parts;
+  a.n_heads = n_heads;
+  a.head_dim = head_dim;
+  a.n_rows = n_rows;
+  a.m = m_parts;
+  a.l = l_parts;
+  a.acc = acc_parts;
+  a.gate = gate;
+  a.m_out = m_out;
+  a.l_out = l_out;
+  a.acc_out = acc_out;
+  a.out = out;
+  a.out_bf16 = out_dtype == DCP_BF16;
+  a.log2_units = 0;
+  const hipError_t e = dcp::launch_merge(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "merge launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,129 @@
+// Internal launch interface between the C-ABI layer (dcp_api.hip) and the
+// kernels. Not installed; the public interface is include/dcp.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dcp {
+
+// Shape of the fused MFMA path.
+constexpr int kFastCz = 128;   // pair channels
+constexpr int kFastH = 16;     // heads
+constexpr int kFastD = 24;     // head dim
+constexpr int kFastDp = 32;    // head dim padded to the MFMA k width
+constexpr int kTileQ = 16;     // query rows per wave
+constexpr int kTileK = 16;     // keys per tile
+
+// Limits of the general fp32 path.
+constexpr int kGenMaxCz = 256;
+constexpr int kGenMaxH = 16;
+constexpr int kGenMaxHD = 128;
+constexpr int kGenMaxD = 64;
+constexpr int kMaxCs = 4096;
+
+// The paper's chunk rule (Appendix "Chunk distribution algorithm"): part p of
+// `total` items over `parts` parts has floor(total/parts) items, plus one when
+// p < total mod parts, and starts at p*floor(total/parts) + min(p, total mod parts).
+__host__ __device__ inline void chunk_of(int64_t total, int64_t parts, int64_t p, int64_t* size, int64_t* start) {
+  const int64_t q = total / parts, r = total % parts;
+  *size = q + (p < r ? 1 : 0);
+  *start = p * q + (p < r ? p : r);
+}
+
+// Key range of internal part `part` = (block b, segment s): the keys are split
+// into n_kb blocks by the chunk rule, and each block into n_seg segments by the
+// same rule. Parts are ordered block-major, so merging them in index order
+// merges the blocks in increasing order.
+__host__ __device__ inline void part_range(int64_t n_tok, int n_kb, int n_seg, int part, int64_t* start,
+                                           int64_t* end) {
+  const int b = part / n_seg, s = part % n_seg;
+  int64_t bs, b0, ss, s0;
+  chunk_of(n_tok, n_kb, b, &bs, &b0);
+  chunk_of(bs, n_seg, s, &ss, &s0);
+  *start = b0 + s0;
+  *end = b0 + s0 + ss;
+}
+
+struct FastProjArgs {
+  const uint16_t* s;  // [N, c_s] bf16
+  const float *w_q, *w_k, *w_v, *w_g;
+  const uint8_t* mask;  // [N] or null
+  int64_t n_tok, q_row0, n_q, nq_pad, n_pad;
+  int32_t c_s;
+  uint16_t* q;   // [H][nq_pad][32] bf16, scaled by log2(e)/sqrt(d)
+  uint16_t* k;   // [H][n_pad][32] bf16
+  uint16_t* vt;  // [H][n_pad/16][2][64][4] bf16: V^T tiles with a row of ones at e = 24
+  float* g;      // [n_q][H*d] fp32, sigmoid applied
+};
+
+struct FastAttnArgs {
+  const uint16_t* z;  // [n_q][N][128] bf16
+  const uint8_t* mask;
+  const float *w_b, *gamma;
+  const uint16_t *q, *k, *vt;
+  int64_t n_tok, n_q, nq_pad, n_pad;
+  int32_t n_kb, n_seg;
+  float eps;
+  float *m_parts, *l_parts, *acc_parts;  // [P][H][n_q], [P][H][n_q], [P][n_q][H][d]
+};
+
+struct FastBiasArgs {
+  const uint16_t* z;
+  const float *w_b, *b_b, *gamma, *beta;
+  int64_t n_rows, n_cols, row_stride;
+  int32_t cols_per_wave;
+  float eps;
+  float* out;  // [n_rows][n_cols][16]
+};
+
+struct GenProjArgs {
+  const void* s;
+  int32_t s_bf16;
+  const float *w_q, *w_k, *w_v, *w_g;
+  int64_t n_tok, q_row0, n_q;
+  int32_t c_s, hd;
+  float *q, *k, *v, *g;  // q, g: [n_q][hd]; k, v: [N][hd]; g holds the sigmoid
+};
+
+struct GenAttnArgs {
+  const void* z;
+  int32_t z_bf16;
+  const uint8_t* mask;
+  const float *w_b, *gamma;
+  const float *q, *k, *v;
+  int64_t n_tok, n_q;
+  int32_t c_z, n_heads, head_dim, n_kb;
+  float eps;
+  float *m_parts, *l_parts, *acc_parts;
+};
+
+struct GenBiasArgs {
+  const void* z;
+  int32_t z_bf16;
+  const float *w_b, *b_b, *gamma, *beta;
+  int64_t n_rows, n_cols, row_stride;
+  int32_t c_z, n_heads;
+  float eps;
+  float* out;
+};
+
+struct MergeArgs {
+  int32_t n_parts, n_heads, head_dim;
+  int64_t n_rows;
+  const float *m, *l, *acc, *gate;
+  float *m_out, *l_out, *acc_out;
+  void* out;
+  int32_t out_bf16;
+  int32_t log2_units;  // 1: m is in base-2 units with integer differences
+};
+
+hipError_t launch_fast_proj(const FastProjArgs& a, hipStream_t st);
+hipError_t launch_fast_attn(const FastAttnArgs& a, hipStream_t st);
+hipError_t launch_fast_bias(const FastBiasArgs& a, hipStream_t st);
+hipError_t launch_gen_proj(const GenProjArgs& a, hipStream_t st);
+hipError_t launch_gen_attn(const GenAttnArgs& a, hipStream_t st);
+hipError_t launch_gen_bias(const GenBiasArgs& a, hipStream_t st);
+hipError_t launch_merge(const MergeArgs& a, hipStream_t st);
+
+}  // namespace dcp

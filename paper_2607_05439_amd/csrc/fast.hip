@@ -1,0 +1,402 @@
+// Fused bf16 path for c_z = 128, H = 16, d = 24 on gfx950 (CDNA4).
+//
+// Three kernels:
+//   proj_kernel  q, k, v, g projections of the single track (MFMA, fp32 weights
+//                split into a bf16 hi+lo pair), written in the layouts the
+//                attention kernel's matrix-core operands want.
+//   attn_kernel  the hot loop: one wave owns 16 query rows and one key range
+//                (a ring step of the paper's 2D scheme, or a slice of one). Per
+//                key it reads the 16 rows' pair vectors z[i, j, :] once from
+//                HBM, forms LayerNorm statistics and the c_z -> H bias
+//                projection on the matrix cores, then per 16-key tile runs
+//                QK^T and PV on the matrix cores with an fp32 online softmax.
+//                It writes one partial state (m, l, acc) per (row, head).
+//   bias_kernel  the pair bias alone, materialised (dcp_bias_project).
+//
+// Matrix-core operand layouts (v_mfma_f32_16x16x32_bf16, 64 lanes, lane L,
+// n = L % 16, g = L / 16): A holds row n with k-slots 8g..8g+7, B holds
+// column n with the same k-slots, and the accumulator holds rows 4g..4g+3 of
+// column n. The 16x16x16 form holds k-slots 4g..4g+3. Because A and B share
+// the k-slot numbering, the channel order inside k is free; it is chosen so
+// each lane's loads are contiguous.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "cdna4.h"
+#include "dcp_internal.h"
+
+namespace dcp {
+namespace {
+
+constexpr int kCz = kFastCz, kH = kFastH, kD = kFastD, kDp = kFastDp;
+constexpr int kPre = 4;  // keys of z in flight per wave (registers)
+constexpr float kLog2e = 1.44269504088896340736f;
+// Logits in base-2 units are offset by this constant inside the QK^T
+// accumulator, so every logit of moderate size lands in [128, 256) and is
+// rounded to a multiple of 2^-16 there. With integer running maxima, the
+// subtraction logit - max is then exact, the softmax weights do not depend on
+// which keys were seen before, and rescaling factors are exact powers of two:
+// key blocks of any size give the same weights.
+constexpr float kShift = 192.0f;
+
+// Bias weights as A operands: row = head (lane % 16), k-step s holds channels
+// 32s + 8g .. 32s + 8g + 7. W' = scale * W_b * diag(gamma), centred per head
+// (subtracting its mean over channels makes sum_c W''_hc z_c = sum_c W'_hc
+// (z_c - mean z)), then split into bf16 hi + lo so the pair carries about 16
+// significant bits.
+__device__ void bias_weights(const float* __restrict__ w_b, const float* __restrict__ gamma, float scale, int lane,
+                             bf16x8 (&hi)[4], bf16x8 (&lo)[4]) {
+  const int h = lane & 15, g = lane >> 4;
+  float w[4][8];
+  float rs = 0.f;
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int c = 32 * s + 8 * g + i;
+      w[s][i] = w_b[h * kCz + c] * (gamma ? gamma[c] : 1.0f) * scale;
+      rs += w[s][i];
+    }
+  const float mean = sum4(rs) * (1.0f / kCz);
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float c = w[s][i] - mean;
+      const __bf16 x = (__bf16)c;
+      hi[s][i] = x;
+      lo[s][i] = (__bf16)(c - (float)x);
+    }
+}
+
+// One key for the wave's 16 rows: z B operands (k-step s = channels 32s+8g..+7
+// of row n) -> rstd of the pair and the unnormalised projection acc[i] =
+// sum_c W''[4g+i, c] z_c (accumulator rows = heads 4g..4g+3, column = row n).
+__device__ __forceinline__ void pair_bias(const u32x4 (&zb)[4], const bf16x8 (&whi)[4], const bf16x8 (&wlo)[4],
+                                          float eps, f32x4& acc, float& rstd) {
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const bf16x2 v = as_bf16x2(zb[s][p]);
+      s1 = __builtin_amdgcn_fdot2_f32_bf16(v, ones, s1, false);
+      s2 = __builtin_amdgcn_fdot2_f32_bf16(v, v, s2, false);
+    }
+  s1 = sum4(s1);
+  s2 = sum4(s2);
+  const float mu = s1 * (1.0f / kCz);
+  const float var = fmaxf(s2 * (1.0f / kCz) - mu * mu, 0.0f);
+  rstd = __builtin_amdgcn_rsqf(var + eps);
+  acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    acc = mfma32(whi[s], as_bf16x8(zb[s]), acc);
+    acc = mfma32(wlo[s], as_bf16x8(zb[s]), acc);
+  }
+}
+
+// ----------------------------------------------------------------------------- projections
+// grid (tiles of 16 tokens, H, 4 projections {q, k, v, g}); one wave each.
+__global__ void __launch_bounds__(64) proj_kernel(FastProjArgs a) {
+  const int lane = threadIdx.x, n = lane & 15, g = lane >> 4;
+  const int h = blockIdx.y, which = blockIdx.z;  // 0 q, 1 k, 2 v, 3 g
+  const bool is_query = (which == 0 || which == 3);
+  const int64_t tile = blockIdx.x;
+  const int64_t limit = is_query ? a.nq_pad : a.n_pad;
+  if (tile * 16 >= limit) return;
+  const int64_t t0 = tile * 16;  // first token (relative to q_row0 for q/g)
+  const int64_t n_valid = is_query ? a.n_q : a.n_tok;
+  const int64_t base_tok = is_query ? a.q_row0 : 0;
+  const float* w = which == 0 ? a.w_q : which == 1 ? a.w_k : which == 2 ? a.w_v : a.w_g;
+
+  // s operand: token t0 + n (clamped; padded rows are zeroed on output).
+  const int64_t my_tok = base_tok + min(t0 + n, n_valid - 1);
+  const uint16_t* srow = a.s + my_tok * a.c_s + 8 * g;
+  // weight operand rows e = 16*et + n of head h (zero for e >= 24)
+  f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+  const bool swap_ab = (which == 2);  // v: accumulator [token][e]; others [e][token]
+  for (int k0 = 0; k0 < a.c_s; k0 += 32) {
+    const bf16x8 sv = as_bf16x8(*reinterpret_cast<const u32x4*>(srow + k0));
+#pragma unroll
+    for (int et = 0; et < 2; ++et) {
+      const int e = 16 * et + n;
+      bf16x8 whi, wlo;
+      if (e < kD) {
+        const float4* wp = reinterpret_cast<const float4*>(w + (int64_t)(h * kD + e) * a.c_s + k0 + 8 * g);
+        const float4 x0 = wp[0], x1 = wp[1];
+        const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const __bf16 hv = (__bf16)xs[i];
+          whi[i] = hv;
+          wlo[i] = (__bf16)(xs[i] - (float)hv);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          whi[i] = (__bf16)0.0f;
+          wlo[i] = (__bf16)0.0f;
+        }
+      }
+      if (swap_ab) {
+        acc[et] = mfma32(sv, whi, acc[et]);
+        acc[et] = mfma32(sv, wlo, acc[et]);
+      } else {
+        acc[et] = mfma32(whi, sv, acc[et]);
+        acc[et] = mfma32(wlo, sv, acc[et]);
+      }
+    }
+  }
+
+  if (which == 2) {
+    // acc[et][i] = v[token t0 + 4g + i][e = 16 et + n]: exactly the V^T tile
+    // operand (lane L, slot i) of rows e = 16 et + n, keys 4g + i.
+#pragma unroll
+    for (int et = 0; et < 2; ++et) {
+      const int e = 16 * et + n;
+      bf16x4 o;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t tok = t0 + 4 * g + i;
+        const bool valid = tok < a.n_tok && (a.mask == nullptr || a.mask[tok] != 0);
+        float val = valid ? acc[et][i] : 0.0f;
+        if (e == kD) val = valid ? 1.0f : 0.0f;  // row of ones: the softmax denominator
+        o[i] = (__bf16)val;
+      }
+      u32x2* dst = reinterpret_cast<u32x2*>(a.vt) + ((((int64_t)h * (a.n_pad / 16) + tile) * 2 + et) * 64 + lane);
+      *dst = __builtin_bit_cast(u32x2, o);
+    }
+    return;
+  }
+  // acc[et][i] = proj[e = 16 et + 4g + i][token t0 + n]
+  const int64_t tok = t0 + n;
+  if (which == 3) {
+    if (tok >= a.n_q) return;
+#pragma unroll
+    for (int et = 0; et < 2; ++et) {
+      const int e0 = 16 * et + 4 * g;
+      if (e0 >= kD) continue;
+      float4 o;
+      o.x = 1.0f / (1.0f + __expf(-acc[et][0]));
+      o.y = 1.0f / (1.0f + __expf(-acc[et][1]));
+      o.z = 1.0f / (1.0f + __expf(-acc[et][2]));
+      o.w = 1.0f / (1.0f + __expf(-acc[et][3]));
+      *reinterpret_cast<float4*>(a.g + tok * (kH * kD) + h * kD + e0) = o;
+    }
+    return;
+  }
+  bool valid;
+  float scale;
+  uint16_t* dst;
+  if (which == 0) {
+    valid = tok < a.n_q;
+    scale = kLog2e * 0.20412414523193150818f;  // log2(e) / sqrt(24)
+    dst = a.q + ((int64_t)h * a.nq_pad + tok) * kDp;
+  } else {
+    valid = tok < a.n_tok && (a.mask == nullptr || a.mask[tok] != 0);
+    scale = 1.0f;
+    dst = a.k + ((int64_t)h * a.n_pad + tok) * kDp;
+  }
+#pragma unroll
+  for (int et = 0; et < 2; ++et) {
+    bf16x4 o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[i] = (__bf16)(valid ? acc[et][i] * scale : 0.0f);  // rows >= 24 are 0
+    *reinterpret_cast<u32x2*>(dst + 16 * et + 4 * g) = __builtin_bit_cast(u32x2, o);
+  }
+}
+
+// ----------------------------------------------------------------------------- attention
+__device__ __forceinline__ uint32_t tile_bits(const uint8_t* __restrict__ mask, int64_t t, int64_t start,
+                                              int64_t end, int lane) {
+  const int64_t j = t * 16 + (lane & 15);
+  bool v = (j >= start) && (j < end);
+  if (v && mask) v = mask[j] != 0;
+  return (uint32_t)(__ballot(v) & 0xFFFFull);
+}
+
+__global__ void __launch_bounds__(64, 1) attn_kernel(FastAttnArgs a) {
+  const int lane = threadIdx.x, n = lane & 15, g = lane >> 4;
+  const int64_t q0 = (int64_t)blockIdx.x * kTileQ;
+  const int part = blockIdx.y;
+  int64_t start, end;
+  part_range(a.n_tok, a.n_kb, a.n_seg, part, &start, &end);
+
+  bf16x8 whi[4], wlo[4];
+  bias_weights(a.w_b, a.gamma, kLog2e, lane, whi, wlo);
+
+  bf16x8 qreg[kH];
+#pragma unroll
+  for (int h = 0; h < kH; ++h)
+    qreg[h] = as_bf16x8(*(reinterpret_cast<const u32x4*>(a.q) + ((int64_t)h * a.nq_pad + q0 + n) * 4 + g));
+
+  float m[kH];
+  f32x4 o[kH][2];
+#pragma unroll
+  for (int h = 0; h < kH; ++h) {
+    m[h] = -INFINITY;
+    o[h][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+    o[h][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  const u32x4* zrow = reinterpret_cast<const u32x4*>(a.z) + min(q0 + n, a.n_q - 1) * a.n_tok * (kCz / 8) + g;
+  const u32x4* kbase = reinterpret_cast<const u32x4*>(a.k);
+  const u32x2* vbase = reinterpret_cast<const u32x2*>(a.vt);
+  const int64_t n_tiles_all = a.n_pad / 16;
+
+  const int64_t t_begin = start >> 4, t_end = (end + 15) >> 4;
+  u32x4 zb[kPre][4];
+  uint32_t bits = (t_begin < t_end) ? tile_bits(a.mask, t_begin, start, end, lane) : 0u;
+#pragma unroll
+  for (int p = 0; p < kPre; ++p)
+    if ((bits >> p) & 1u) {
+      const int64_t j = t_begin * 16 + p;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) zb[p][s] = __builtin_nontemporal_load(zrow + j * 16 + 4 * s);
+    }
+
+  for (int64_t t = t_begin; t < t_end; ++t) {
+    const uint32_t bits_next = (t + 1 < t_end) ? tile_bits(a.mask, t + 1, start, end, lane) : 0u;
+    float b[16][4];
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      const int slot = kk % kPre;
+      if ((bits >> kk) & 1u) {
+        f32x4 acc;
+        float rstd;
+        pair_bias(zb[slot], whi, wlo, a.eps, acc, rstd);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) b[kk][i] = fmaf(acc[i], rstd, kShift);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) b[kk][i] = -INFINITY;
+      }
+      const int nk = kk + kPre;
+      if (nk < 16) {
+        if ((bits >> nk) & 1u) {
+          const int64_t j = t * 16 + nk;
+#pragma unroll
+          for (int s = 0; s < 4; ++s) zb[slot][s] = __builtin_nontemporal_load(zrow + j * 16 + 4 * s);
+        }
+      } else {
+        if ((bits_next >> (nk - 16)) & 1u) {
+          const int64_t j = (t + 1) * 16 + (nk - 16);
+#pragma unroll
+          for (int s = 0; s < 4; ++s) zb[slot][s] = __builtin_nontemporal_load(zrow + j * 16 + 4 * s);
+        }
+      }
+    }
+    transpose_bias(b);
+
+#pragma unroll
+    for (int h = 0; h < kH; ++h) {
+      const int ha = h >> 2, hi = h & 3;
+      const f32x4 cin = {b[4 * ha + 0][hi], b[4 * ha + 1][hi], b[4 * ha + 2][hi], b[4 * ha + 3][hi]};
+      const u32x4 kt = kbase[((int64_t)h * a.n_pad + t * 16 + n) * 4 + g];
+      const u32x2 v0 = vbase[(((int64_t)h * n_tiles_all + t) * 2 + 0) * 64 + lane];
+      const u32x2 v1 = vbase[(((int64_t)h * n_tiles_all + t) * 2 + 1) * 64 + lane];
+      // x[r]: logit (base 2, + kShift) of row n, key 4g + r
+      const f32x4 x = mfma32(as_bf16x8(kt), qreg[h], cin);
+      const float tmax = max4(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
+      const float mnew = fmaxf(m[h], ceilf(tmax));
+      const float muse = (mnew == -INFINITY) ? 0.0f : mnew;
+      const float alpha = (m[h] == -INFINITY) ? 0.0f : ldexpf(1.0f, (int)(m[h] - muse));
+      bf16x4 p;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) p[r] = (__bf16)__builtin_amdgcn_exp2f(x[r] - muse);
+      // the running maximum is an integer and rarely moves, so most tiles skip this
+      if (__any(alpha != 1.0f)) {
+        o[h][0] *= alpha;
+        o[h][1] *= alpha;
+      }
+      o[h][0] = mfma16(as_bf16x4(v0), p, o[h][0]);
+      o[h][1] = mfma16(as_bf16x4(v1), p, o[h][1]);
+      m[h] = mnew;
+    }
+    bits = bits_next;
+  }
+
+  // Partial state of rows q0 + n: o[h][0][i] = acc e = 4g+i, o[h][1][i] = acc
+  // e = 16+4g+i (e = 24 is the denominator l).
+  const int64_t row = q0 + n;
+  if (row >= a.n_q) return;
+#pragma unroll
+  for (int h = 0; h < kH; ++h) {
+    const float l = o[h][1][0];  // valid in lane group 2 (e = 24)
+    if (g == 2) {
+      const bool empty = !(l > 0.0f);
+      a.m_parts[((int64_t)part * kH + h) * a.n_q + row] = empty ? -INFINITY : m[h] - kShift;
+      a.l_parts[((int64_t)part * kH + h) * a.n_q + row] = empty ? 0.0f : l;
+    }
+    float* accp = a.acc_parts + (((int64_t)part * a.n_q + row) * kH + h) * kD;
+    *reinterpret_cast<float4*>(accp + 4 * g) = make_float4(o[h][0][0], o[h][0][1], o[h][0][2], o[h][0][3]);
+    if (g < 2)
+      *reinterpret_cast<float4*>(accp + 16 + 4 * g) = make_float4(o[h][1][0], o[h][1][1], o[h][1][2], o[h][1][3]);
+  }
+}
+
+// ----------------------------------------------------------------------------- bias only
+// grid (tiles of 16 rows, column chunks); each wave walks its columns.
+__global__ void __launch_bounds__(64) bias_kernel(FastBiasArgs a) {
+  const int lane = threadIdx.x, n = lane & 15, g = lane >> 4;
+  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  const int64_t c_begin = (int64_t)blockIdx.y * a.cols_per_wave;
+  const int64_t c_end = min(c_begin + (int64_t)a.cols_per_wave, a.n_cols);
+  bf16x8 whi[4], wlo[4];
+  bias_weights(a.w_b, a.gamma, 1.0f, lane, whi, wlo);
+  // per-head constant sum_c W_b[h,c] beta_c + b_b[h] for heads 4g..4g+3
+  float cst[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int h = 4 * g + i;
+    float c0 = a.b_b ? a.b_b[h] : 0.0f;
+    if (a.beta)
+      for (int c = 0; c < kCz; ++c) c0 = fmaf(a.w_b[h * kCz + c], a.beta[c], c0);
+    cst[i] = c0;
+  }
+  const int64_t row = r0 + n;
+  const int64_t rr = min(row, a.n_rows - 1);
+  const u32x4* zrow = reinterpret_cast<const u32x4*>(a.z + rr * a.row_stride) + g;
+  for (int64_t c = c_begin; c < c_end; ++c) {
+    u32x4 zb[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) zb[s] = __builtin_nontemporal_load(zrow + c * 16 + 4 * s);
+    f32x4 acc;
+    float rstd;
+    pair_bias(zb, whi, wlo, a.eps, acc, rstd);
+    if (row < a.n_rows) {
+      float4 o;
+      o.x = fmaf(acc[0], rstd, cst[0]);
+      o.y = fmaf(acc[1], rstd, cst[1]);
+      o.z = fmaf(acc[2], rstd, cst[2]);
+      o.w = fmaf(acc[3], rstd, cst[3]);
+      *reinterpret_cast<float4*>(a.out + (row * a.n_cols + c) * kH + 4 * g) = o;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_fast_proj(const FastProjArgs& a, hipStream_t st) {
+  const int64_t tiles = (a.n_pad > a.nq_pad ? a.n_pad : a.nq_pad) / 16;
+  hipLaunchKernelGGL(proj_kernel, dim3((unsigned)tiles, kH, 4), dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fast_attn(const FastAttnArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(attn_kernel, dim3((unsigned)(a.nq_pad / kTileQ), (unsigned)(a.n_kb * a.n_seg)), dim3(64), 0, st,
+                     a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fast_bias(const FastBiasArgs& a, hipStream_t st) {
+  const int64_t rt = (a.n_rows + 15) / 16;
+  const int64_t ct = (a.n_cols + a.cols_per_wave - 1) / a.cols_per_wave;
+  hipLaunchKernelGGL(bias_kernel, dim3((unsigned)rt, (unsigned)ct), dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace dcp

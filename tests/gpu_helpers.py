@@ -1,0 +1,134 @@
+"""Shared plumbing for the GPU tests: device inputs from the seeded generator,
+calls through the C-ABI binding, and the oracle on the same inputs."""
+from __future__ import annotations
+
+import dataclasses
+import sys
+from typing import Optional, Sequence
+
+import numpy as np
+
+import oracle
+import synth
+
+DCP_F32, DCP_BF16 = 0, 1
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def rel_err(got: np.ndarray, ref: np.ndarray) -> float:
+    """max |got - ref| / max |ref| (the acceptance metric)."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = np.max(np.abs(ref))
+    return float(np.max(np.abs(got - ref)) / (den if den > 0 else 1.0))
+
+
+def workload(name: str = "", **kw) -> synth.Workload:
+    """A registered workload, or an ad-hoc one with the given fields."""
+    if name in synth.WORKLOADS and not kw:
+        return synth.WORKLOADS[name]
+    base = dict(name=name or "adhoc", n_tok=64, c_s=384, c_z=128, n_heads=16, head_dim=24, dtype="bf16",
+                n_key_blocks=1, stripes=((0, 64),), mask="none", z_period=0, seed=0, note="")
+    if name in synth.WORKLOADS:
+        base.update(dataclasses.asdict(synth.WORKLOADS[name]))
+    base.update(kw)
+    return synth.Workload(**base)
+
+
+class Device:
+    """Device-resident inputs of one workload."""
+
+    def __init__(self, wl: synth.Workload, affine: bool = False, mask: Optional[np.ndarray] = "default",
+                 z_override: Optional[np.ndarray] = None):
+        import torch
+        self.torch = torch
+        self.wl = wl
+        self.dev = torch.device("cuda:0")
+        self.w_host = synth.weights(wl, affine=affine)
+        self.s_host = synth.s_host(wl)
+        self.mask_host = synth.mask_host(wl) if isinstance(mask, str) else mask
+        self.s = self._to_dev(self.s_host)
+        self.w = {k: (None if v is None else torch.from_numpy(np.ascontiguousarray(v)).to(self.dev))
+                  for k, v in self.w_host.items()}
+        self.mask = None if self.mask_host is None else torch.from_numpy(self.mask_host).to(self.dev)
+        n = wl.n_tok
+        if z_override is not None:
+            self.z = self._to_dev(z_override)
+        else:
+            dt = torch.bfloat16 if wl.bf16 else torch.float32
+            self.z = torch.empty((n, n, wl.c_z), dtype=dt, device=self.dev)
+            synth.z_fill_device(wl, self.z.data_ptr(), 0, n, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+
+    def _to_dev(self, a: np.ndarray):
+        torch = self.torch
+        if a.dtype == np.uint16:
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(self.dev)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(self.dev)
+
+    def shape(self, out_dtype: int = DCP_F32, eps: float = 1e-5):
+        import paper_2607_05439_amd as dcp
+        wl = self.wl
+        return dcp.make_shape(wl.n_tok, wl.c_s, wl.c_z, wl.n_heads, wl.head_dim,
+                              DCP_BF16 if wl.bf16 else DCP_F32, out_dtype, eps)
+
+    def weights(self, drop_affine: bool = False):
+        import paper_2607_05439_amd as dcp
+        w = self.w
+        if drop_affine:
+            return dcp.make_weights(w["w_q"], w["w_k"], w["w_v"], w["w_g"], w["w_b"], None, w["ln_gamma"], None)
+        return dcp.make_weights(w["w_q"], w["w_k"], w["w_v"], w["w_g"], w["w_b"], w["b_b"], w["ln_gamma"],
+                                w["ln_beta"])
+
+    def attention(self, q_row0: int, n_q: int, n_kb: int, out_dtype: int = DCP_F32, drop_affine: bool = False,
+                  z=None, mask="default", workspace=None):
+        """Run dcp_pair_bias_attention; returns the output as a device tensor."""
+        import paper_2607_05439_amd as dcp
+        torch = self.torch
+        shape = self.shape(out_dtype)
+        wl = self.wl
+        hd = wl.n_heads * wl.head_dim
+        out = torch.empty((max(n_q, 1), hd), dtype=torch.float32 if out_dtype == DCP_F32 else torch.bfloat16,
+                          device=self.dev)
+        nbytes = dcp.dcp_workspace_size(shape, n_q, n_kb)
+        ws = workspace if workspace is not None else torch.empty(max(nbytes, 256), dtype=torch.uint8,
+                                                                 device=self.dev)
+        zt = self.z if z is None else z
+        z_ptr = zt.data_ptr() + q_row0 * wl.n_tok * wl.c_z * zt.element_size()
+        m = self.mask if isinstance(mask, str) else mask
+        dcp.dcp_pair_bias_attention(shape, self.weights(drop_affine), self.s, z_ptr, m, q_row0, n_q, n_kb, out,
+                                    ws, ws.numel(), None)
+        return out
+
+    def oracle_rows(self, rows: Sequence[int], n_blocks: int = 1, drop_affine: bool = False) -> np.ndarray:
+        """fp64 oracle on the generator's host copy of the same inputs."""
+        z_rows = synth.z_host(self.wl, rows)
+        w = dict(self.w_host)
+        if drop_affine:
+            w["b_b"] = None
+            w["ln_beta"] = None
+        return oracle.attention(self.s_host, z_rows, rows, self.mask_host, w, self.wl.n_heads,
+                                self.wl.head_dim, n_blocks=n_blocks)
+
+
+def sample_rows(n_tok: int, stripes, n_kb: int, n_random: int, mask: Optional[np.ndarray], seed: int = 0):
+    """Rows the oracle checks at full size: the first and last row of every
+    stripe and key block, some masked (padding) rows, and random rows."""
+    rows = set()
+    for q0, nq in stripes:
+        rows.update({q0, q0 + nq - 1})
+    for p in range(n_kb):
+        size, start = oracle.chunk(n_tok, n_kb, p)
+        rows.update({start, start + size - 1})
+    if mask is not None:
+        masked = np.flatnonzero(mask == 0)
+        if len(masked):
+            rows.update(int(x) for x in masked[:: max(1, len(masked) // 8)][:8])
+            rows.add(int(masked[-1]))
+    r = np.random.default_rng(seed)
+    rows.update(int(x) for x in r.choice(n_tok, size=min(n_random, n_tok), replace=False))
+    return sorted(rows)

@@ -1,0 +1,141 @@
+"""The C-ABI boundary on the host (CPU only): the library loads, exports every
+declared entry point, sizes workspaces, and rejects bad arguments with the
+documented codes before anything reaches the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_05439_amd as dcp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x10000  # a 256-byte aligned non-null address; never dereferenced on these paths
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "dcp.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(dcp_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert set(names) == set(dcp.EXPORTS)
+    lib = dcp.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+    assert "gfx950" in dcp.dcp_version()
+
+
+def shape(**kw):
+    base = dict(n_tokens=24000, c_s=384, c_z=128, n_heads=16, head_dim=24, act_dtype=dcp.DCP_BF16,
+                out_dtype=dcp.DCP_F32, ln_eps=1e-5)
+    base.update(kw)
+    return dcp.make_shape(**base)
+
+
+def weights():
+    return dcp.make_weights(FAKE, FAKE, FAKE, FAKE, FAKE)
+
+
+def attention(sh, w=None, s=FAKE, z=FAKE, q_row0=0, n_q=24000, n_kb=6, out=FAKE, ws=FAKE, ws_bytes=1 << 40):
+    return dcp.lib().dcp_pair_bias_attention(ctypes.byref(sh), ctypes.byref(w or weights()), s, z, None, q_row0, n_q,
+                                             n_kb, out, ws, ws_bytes, None)
+
+
+def test_workspace_sizes():
+    big = dcp.dcp_workspace_size(shape(), 24000, 6)
+    # q, k, v tiles (3 x 16 x 24000 x 32 x 2 B) + gate + 6 partials: a few hundred MB
+    assert 200e6 < big < 400e6
+    assert dcp.dcp_workspace_size(shape(), 0, 6) == 0
+    small = dcp.dcp_workspace_size(shape(n_tokens=128, c_s=128, c_z=32, n_heads=4, head_dim=32,
+                                         act_dtype=dcp.DCP_F32), 128, 4)
+    assert 0 < small < 2e6
+    # more key blocks need more partial storage
+    assert dcp.dcp_workspace_size(shape(), 24000, 12) > big
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n_tokens=0), dcp.DCP_ERR_INVALID_ARGUMENT),
+    (dict(c_z=0), dcp.DCP_ERR_INVALID_ARGUMENT),
+    (dict(act_dtype=7), dcp.DCP_ERR_INVALID_ARGUMENT),
+    (dict(ln_eps=-1.0), dcp.DCP_ERR_INVALID_ARGUMENT),
+    (dict(ln_eps=float("nan")), dcp.DCP_ERR_INVALID_ARGUMENT),
+    (dict(c_z=512), dcp.DCP_ERR_UNSUPPORTED),
+    (dict(n_heads=32), dcp.DCP_ERR_UNSUPPORTED),
+    (dict(head_dim=100, n_heads=1), dcp.DCP_ERR_UNSUPPORTED),
+    (dict(c_s=5000), dcp.DCP_ERR_UNSUPPORTED),
+])
+def test_bad_shapes(kw, code):
+    sh = shape(**kw)
+    assert attention(sh) == code
+    assert len(dcp.dcp_last_error()) > 0
+    out = ctypes.c_size_t()
+    assert dcp.lib().dcp_workspace_size(ctypes.byref(sh), 100, 1, ctypes.byref(out)) == code
+
+
+def test_bad_ranges():
+    E = dcp.DCP_ERR_INVALID_ARGUMENT
+    sh = shape()
+    assert attention(sh, n_q=-1) == E
+    assert attention(sh, q_row0=-1, n_q=10) == E
+    assert attention(sh, q_row0=23990, n_q=11) == E
+    assert attention(sh, n_kb=0) == E
+    assert attention(sh, n_kb=24001) == E
+    assert attention(sh, s=0) == E
+    assert attention(sh, z=0) == E
+    assert attention(sh, out=0) == E
+    assert attention(sh, z=FAKE + 2) == E  # misaligned
+    w = dcp.make_weights(FAKE, FAKE, 0, FAKE, FAKE)
+    assert attention(sh, w=w) == E
+    assert dcp.lib().dcp_pair_bias_attention(None, ctypes.byref(weights()), FAKE, FAKE, None, 0, 1, 1, FAKE, FAKE,
+                                             1 << 40, None) == E
+
+
+def test_bad_workspace():
+    sh = shape()
+    need = dcp.dcp_workspace_size(sh, 24000, 6)
+    assert attention(sh, ws_bytes=need - 1) == dcp.DCP_ERR_WORKSPACE
+    assert attention(sh, ws=0) == dcp.DCP_ERR_WORKSPACE
+    assert attention(sh, ws=FAKE + 128) == dcp.DCP_ERR_WORKSPACE
+    assert "workspace" in dcp.dcp_last_error()
+
+
+def test_empty_stripe_is_ok_without_touching_the_gpu():
+    assert attention(shape(), q_row0=24000, n_q=0, ws=0, ws_bytes=0) == dcp.DCP_OK
+
+
+def test_bias_project_rejections():
+    L = dcp.lib()
+    sh, w = shape(), weights()
+    E = dcp.DCP_ERR_INVALID_ARGUMENT
+    assert L.dcp_bias_project(ctypes.byref(sh), ctypes.byref(w), FAKE, 4, 8, 8 * 128 - 1, FAKE, None) == E
+    assert L.dcp_bias_project(ctypes.byref(sh), ctypes.byref(w), 0, 4, 8, 1024, FAKE, None) == E
+    assert L.dcp_bias_project(ctypes.byref(sh), ctypes.byref(w), FAKE, -1, 8, 1024, FAKE, None) == E
+    assert L.dcp_bias_project(ctypes.byref(sh), ctypes.byref(w), FAKE, 0, 8, 1024, FAKE, None) == dcp.DCP_OK
+    bad = shape(c_z=1000)
+    assert L.dcp_bias_project(ctypes.byref(bad), ctypes.byref(w), FAKE, 4, 8, 8000, FAKE, None) == \
+        dcp.DCP_ERR_UNSUPPORTED
+
+
+def test_block_merge_rejections():
+    L = dcp.lib()
+    E = dcp.DCP_ERR_INVALID_ARGUMENT
+    assert L.dcp_block_merge(0, 4, 2, 3, FAKE, FAKE, FAKE, None, None, None, None, FAKE, 0, None) == E
+    assert L.dcp_block_merge(2, 4, 2, 3, 0, FAKE, FAKE, None, None, None, None, FAKE, 0, None) == E
+    assert L.dcp_block_merge(2, 4, 2, 3, FAKE, FAKE, FAKE, None, None, None, None, FAKE, 9, None) == E
+    assert L.dcp_block_merge(2, 4, 64, 128, FAKE, FAKE, FAKE, None, None, None, None, FAKE, 0, None) == \
+        dcp.DCP_ERR_UNSUPPORTED
+    assert L.dcp_block_merge(2, 0, 2, 3, FAKE, FAKE, FAKE, None, None, None, None, FAKE, 0, None) == dcp.DCP_OK
+
+
+def test_timing_events_pairing():
+    assert dcp.lib().dcp_set_timing_events(FAKE, None) == dcp.DCP_ERR_INVALID_ARGUMENT
+    assert dcp.lib().dcp_set_timing_events(None, None) == dcp.DCP_OK
+
+
+def test_binding_raises():
+    with pytest.raises(dcp.DcpError) as e:
+        dcp.dcp_workspace_size(shape(n_heads=0), 10, 1)
+    assert e.value.code == dcp.DCP_ERR_INVALID_ARGUMENT

@@ -1,0 +1,80 @@
+"""dcp_bias_project and dcp_block_merge against the oracle, and the device
+input generator against its host twin (GPU)."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_helpers import DCP_BF16, DCP_F32, Device, log, rel_err, workload
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available()
+    return torch
+
+
+@pytest.mark.parametrize("dtype,c_z,h,tol", [("bf16", 128, 16, 1e-4), ("f32", 32, 4, 1e-5), ("bf16", 48, 3, 1e-5)])
+def test_bias_project(torch_cuda, dtype, c_z, h, tol):
+    import paper_2607_05439_amd as dcp
+    log(f"case bias_project {dtype} c_z={c_z} H={h}")
+    wl = workload(n_tok=70, c_z=c_z, n_heads=h, head_dim=8, c_s=32, dtype=dtype)
+    d = Device(wl, affine=True)
+    r0, c0, nr, nc = 3, 5, 37, 61  # a tile of the full z
+    tile = d.z[r0:r0 + nr, c0:c0 + nc]
+    out = torch_cuda.empty((nr, nc, h), dtype=torch_cuda.float32, device="cuda")
+    dcp.dcp_bias_project(d.shape(), d.weights(), tile.data_ptr(), nr, nc, wl.n_tok * c_z, out)
+    z_host = synth.z_host(wl, range(r0, r0 + nr))[:, c0:c0 + nc]
+    w = d.w_host
+    ref = oracle.bias(np.ascontiguousarray(z_host), w["w_b"], w["b_b"], w["ln_gamma"], w["ln_beta"], 1e-5)
+    err = rel_err(out.cpu().numpy(), ref)
+    log(f"  rel err {err:.3e}")
+    assert err <= tol
+
+
+def test_block_merge(torch_cuda):
+    import paper_2607_05439_amd as dcp
+    log("case block_merge")
+    r = np.random.default_rng(5)
+    P, R, H, D = 5, 33, 4, 6
+    m = (3 * r.standard_normal((P, H, R))).astype(np.float32)
+    m[1, :, ::3] = -np.inf
+    m[:, 0, 7] = -np.inf  # a fully empty (row, head)
+    l = (r.random((P, H, R)) + 0.5).astype(np.float32)
+    l[np.isneginf(m)] = 0
+    acc = r.standard_normal((P, R, H, D)).astype(np.float32)
+    acc[np.isneginf(m).transpose(0, 2, 1)] = 0
+    gate = r.random((R, H * D)).astype(np.float32)
+    T = lambda a: torch_cuda.from_numpy(np.ascontiguousarray(a)).cuda()
+    mo = torch_cuda.empty((H, R), device="cuda")
+    lo = torch_cuda.empty((H, R), device="cuda")
+    ao = torch_cuda.empty((R, H, D), device="cuda")
+    out = torch_cuda.empty((R, H * D), device="cuda")
+    dcp.dcp_block_merge(P, R, H, D, T(m), T(l), T(acc), mo, lo, ao, T(gate), out, DCP_F32)
+    m_ref, l_ref, a_ref, o_ref = oracle.merge(m, l, acc, gate)
+    assert np.array_equal(mo.cpu().numpy(), m_ref.astype(np.float32))
+    assert rel_err(lo.cpu().numpy(), l_ref) <= 1e-6
+    assert rel_err(ao.cpu().numpy(), a_ref) <= 1e-6
+    assert rel_err(out.cpu().numpy(), o_ref) <= 1e-6
+    assert np.all(out.cpu().numpy()[7, 0:D] == 0.0)
+    out_bf = torch_cuda.empty((R, H * D), dtype=torch_cuda.bfloat16, device="cuda")
+    dcp.dcp_block_merge(P, R, H, D, T(m), T(l), T(acc), None, None, None, None, out_bf, DCP_BF16)
+    _, _, _, o_nogate = oracle.merge(m, l, acc, None)
+    assert rel_err(out_bf.float().cpu().numpy(), o_nogate) <= 1e-2
+
+
+@pytest.mark.parametrize("period,bf16", [(0, True), (80, True), (0, False), (7, False)])
+def test_device_generator_matches_host(torch_cuda, period, bf16):
+    log(f"case device generator period={period} bf16={bf16}")
+    wl = workload(n_tok=90, c_z=32, dtype="bf16" if bf16 else "f32", z_period=period)
+    rows = [0, 1, 45, 89]
+    dt = torch_cuda.bfloat16 if bf16 else torch_cuda.float32
+    z = torch_cuda.empty((90, 90, 32), dtype=dt, device="cuda")
+    synth.z_fill_device(wl, z.data_ptr(), 0, 90, torch_cuda.cuda.current_stream().cuda_stream)
+    host = synth.z_host(wl, rows)
+    dev = z[rows].cpu()
+    dev = dev.view(torch_cuda.int16).numpy().view(np.uint16) if bf16 else dev.numpy()
+    assert np.array_equal(dev.view(np.uint8), host.view(np.uint8))
