@@ -49,7 +49,8 @@ int check_shape(const dcp_shape* sh) {
 
 int pick_path(const dcp_shape* sh, Path* p) {
   if (sh->act_dtype == DCP_BF16 && sh->c_z == dcp::kFastCz && sh->n_heads == dcp::kFastH &&
-      sh->head_dim == dcp::kFastD && sh->c_s % 32 == 0 && sh->c_s <= dcp::kMaxCs) {
+      sh->head_dim == dcp::kFastD && sh->c_s % 32 == 0 && sh->c_s <= dcp::kMaxCs &&
+      sh->n_tokens <= dcp::kFastMaxTokens) {
     *p = kPathFast;
     return DCP_OK;
   }
@@ -83,7 +84,7 @@ struct Layout {
   Path path;
   int n_seg, n_parts;
   int64_t nq_pad, n_pad;
-  size_t off_q, off_k, off_v, off_g, off_m, off_l, off_acc, total;
+  size_t off_q, off_k, off_v, off_tv, off_g, off_m, off_l, off_acc, total;
 };
 
 void make_layout(const dcp_shape* sh, Path path, int64_t n_q, int32_t n_kb, Layout* L) {
@@ -103,6 +104,7 @@ void make_layout(const dcp_shape* sh, Path path, int64_t n_q, int32_t n_kb, Layo
     L->off_q = take((size_t)dcp::kFastH * L->nq_pad * dcp::kFastDp * 2);
     L->off_k = take((size_t)dcp::kFastH * L->n_pad * dcp::kFastDp * 2);
     L->off_v = take((size_t)dcp::kFastH * L->n_pad * dcp::kFastDp * 2);
+    L->off_tv = take((size_t)(L->n_pad / 16) * 4);
   } else {
     L->n_seg = 1;
     L->n_parts = n_kb;
@@ -111,6 +113,7 @@ void make_layout(const dcp_shape* sh, Path path, int64_t n_q, int32_t n_kb, Layo
     L->off_q = take((size_t)n_q * hd * 4);
     L->off_k = take((size_t)sh->n_tokens * hd * 4);
     L->off_v = take((size_t)sh->n_tokens * hd * 4);
+    L->off_tv = 0;
   }
   L->off_g = take((size_t)n_q * hd * 4);
   L->off_m = take((size_t)L->n_parts * sh->n_heads * n_q * 4);
@@ -211,6 +214,7 @@ int dcp_pair_bias_attention(const dcp_shape* shape, const dcp_weights* w, const 
     pa.k = reinterpret_cast<uint16_t*>(ws + L.off_k);
     pa.vt = reinterpret_cast<uint16_t*>(ws + L.off_v);
     pa.g = reinterpret_cast<float*>(ws + L.off_g);
+    pa.tile_valid = reinterpret_cast<uint32_t*>(ws + L.off_tv);
     if ((e = dcp::launch_fast_proj(pa, st)) != hipSuccess)
       return fail(DCP_ERR_HIP, "projection launch failed: %s", hipGetErrorString(e));
     dcp::FastAttnArgs aa{};
@@ -221,6 +225,7 @@ int dcp_pair_bias_attention(const dcp_shape* shape, const dcp_weights* w, const 
     aa.q = pa.q;
     aa.k = pa.k;
     aa.vt = pa.vt;
+    aa.tile_valid = pa.tile_valid;
     aa.n_tok = N;
     aa.n_q = n_q;
     aa.nq_pad = L.nq_pad;

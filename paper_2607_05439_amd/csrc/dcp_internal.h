@@ -14,6 +14,8 @@ constexpr int kFastD = 24;     // head dim
 constexpr int kFastDp = 32;    // head dim padded to the MFMA k width
 constexpr int kTileQ = 16;     // query rows per wave
 constexpr int kTileK = 16;     // keys per tile
+// 16 rows of z must be addressable with 31-bit byte offsets: 16 * N * 256 < 2^31
+constexpr int64_t kFastMaxTokens = 500000;
 
 // Limits of the general fp32 path.
 constexpr int kGenMaxCz = 256;
@@ -55,6 +57,7 @@ struct FastProjArgs {
   uint16_t* k;   // [H][n_pad][32] bf16
   uint16_t* vt;  // [H][n_pad/16][2][64][4] bf16: V^T tiles with a row of ones at e = 24
   float* g;      // [n_q][H*d] fp32, sigmoid applied
+  uint32_t* tile_valid;  // [n_pad/16]: bit i = key 16t+i exists and is not masked
 };
 
 struct FastAttnArgs {
@@ -62,6 +65,7 @@ struct FastAttnArgs {
   const uint8_t* mask;
   const float *w_b, *gamma;
   const uint16_t *q, *k, *vt;
+  const uint32_t* tile_valid;
   int64_t n_tok, n_q, nq_pad, n_pad;
   int32_t n_kb, n_seg;
   float eps;

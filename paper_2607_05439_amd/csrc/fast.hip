@@ -188,6 +188,12 @@ __global__ void __launch_bounds__(64) proj_kernel(FastProjArgs a) {
     }
     return;
   }
+  if (which == 1 && h == 0) {
+    // per-tile key mask: bit i = token t0 + i exists and attends
+    const bool kv_valid = tok < a.n_tok && (a.mask == nullptr || a.mask[tok] != 0);
+    const uint32_t bits = (uint32_t)(__ballot(kv_valid) & 0xFFFFull);
+    if (lane == 0) a.tile_valid[tile] = bits;
+  }
   bool valid;
   float scale;
   uint16_t* dst;
@@ -210,17 +216,46 @@ __global__ void __launch_bounds__(64) proj_kernel(FastProjArgs a) {
 }
 
 // ----------------------------------------------------------------------------- attention
-__device__ __forceinline__ uint32_t tile_bits(const uint8_t* __restrict__ mask, int64_t t, int64_t start,
-                                              int64_t end, int lane) {
-  const int64_t j = t * 16 + (lane & 15);
-  bool v = (j >= start) && (j < end);
-  if (v && mask) v = mask[j] != 0;
-  return (uint32_t)(__ballot(v) & 0xFFFFull);
+constexpr int kWaves = 4;   // waves per workgroup: 4 query tiles sharing one key range
+constexpr int kKvBufs = 3;  // K/V tiles staged in LDS: current, next, and one being written
+constexpr uint32_t kRawBufferFlags = 0x00020000u;
+constexpr int kOutOfRange = 0x7FFFFF00;  // buffer offset past every valid record: reads 0, no traffic
+
+// K and V^T tiles of one 16-key tile for all heads, in matrix-core operand order.
+struct KvTile {
+  u32x4 k[kH][64];     // lane L: keys' k (A operand of QK^T)
+  u32x2 v[kH][2][64];  // lane L: V^T rows 16*mt + L%16, keys 4(L/16)..+3 (A operand of PV)
+};
+
+typedef const __attribute__((address_space(4))) uint32_t* const_u32_ptr;
+
+// Valid keys of tile t: the per-tile key mask, restricted to [start, end). The
+// mask is read-only during the attention kernel, so it is read through the
+// constant address space: a scalar load that stays out of the vector-memory
+// queue (whose waits are in issue order).
+__device__ __forceinline__ uint32_t tile_valid_bits(const_u32_ptr tv, int64_t t, int64_t start, int64_t end) {
+  const int64_t lo = max(start - t * 16, (int64_t)0), hi = min(end - t * 16, (int64_t)16);
+  if (hi <= lo) return 0u;
+  const uint32_t range = (hi >= 16 ? 0xFFFFu : ((1u << hi) - 1u)) & ~((1u << lo) - 1u);
+  return tv[t] & range;
 }
 
-__global__ void __launch_bounds__(64, 1) attn_kernel(FastAttnArgs a) {
-  const int lane = threadIdx.x, n = lane & 15, g = lane >> 4;
-  const int64_t q0 = (int64_t)blockIdx.x * kTileQ;
+// One workgroup = 4 waves = 4 tiles of 16 query rows, all over the same key
+// range (one internal part). z is streamed per wave through registers kPre
+// keys ahead with buffer loads: an invalid (masked or out-of-range) key gets
+// an out-of-range offset, so the load returns zeros without touching memory
+// and every load is unconditional (exact wait counts, no drained pipeline).
+// K/V tiles are loaded one tile ahead, each wave fetching 4 heads, and shared
+// through LDS; one barrier per tile.
+__global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
+  __shared__ KvTile kv[kKvBufs];
+  __shared__ u32x4 qlds[kWaves][kH][64];  // each wave's Q^T operands, one per head
+  const int tid = threadIdx.x, lane = tid & 63, n = lane & 15, g = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int64_t n_qt = a.nq_pad / kTileQ;
+  const int64_t qt = (int64_t)blockIdx.x * kWaves + wave;
+  const bool active = qt < n_qt;
+  const int64_t q0 = (active ? qt : n_qt - 1) * kTileQ;
   const int part = blockIdx.y;
   int64_t start, end;
   part_range(a.n_tok, a.n_kb, a.n_seg, part, &start, &end);
@@ -228,10 +263,9 @@ __global__ void __launch_bounds__(64, 1) attn_kernel(FastAttnArgs a) {
   bf16x8 whi[4], wlo[4];
   bias_weights(a.w_b, a.gamma, kLog2e, lane, whi, wlo);
 
-  bf16x8 qreg[kH];
 #pragma unroll
   for (int h = 0; h < kH; ++h)
-    qreg[h] = as_bf16x8(*(reinterpret_cast<const u32x4*>(a.q) + ((int64_t)h * a.nq_pad + q0 + n) * 4 + g));
+    qlds[wave][h][lane] = *(reinterpret_cast<const u32x4*>(a.q) + ((int64_t)h * a.nq_pad + q0 + n) * 4 + g);
 
   float m[kH];
   f32x4 o[kH][2];
@@ -242,28 +276,64 @@ __global__ void __launch_bounds__(64, 1) attn_kernel(FastAttnArgs a) {
     o[h][1] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  const u32x4* zrow = reinterpret_cast<const u32x4*>(a.z) + min(q0 + n, a.n_q - 1) * a.n_tok * (kCz / 8) + g;
-  const u32x4* kbase = reinterpret_cast<const u32x4*>(a.k);
-  const u32x2* vbase = reinterpret_cast<const u32x2*>(a.vt);
-  const int64_t n_tiles_all = a.n_pad / 16;
+  // z rows q0 .. q0+15 of this wave: one buffer resource, 32-bit byte offsets.
+  const int64_t rows_here = min((int64_t)kTileQ, a.n_q - q0);
+  const int64_t row_bytes = a.n_tok * (kCz * 2);
+  const __amdgpu_buffer_rsrc_t zres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.z) + q0 * a.n_tok * kCz, 0, (int)(rows_here * row_bytes), kRawBufferFlags);
+  const int lane_off = (int)(n * row_bytes) + 16 * g;  // row n, channels 8g.. of k-step 0
 
   const int64_t t_begin = start >> 4, t_end = (end + 15) >> 4;
-  u32x4 zb[kPre][4];
-  uint32_t bits = (t_begin < t_end) ? tile_bits(a.mask, t_begin, start, end, lane) : 0u;
+  const int64_t n_tiles_all = a.n_pad / 16;
+  const const_u32_ptr tvres = (const_u32_ptr)(a.tile_valid);
+
+  // K/V tile t -> registers (this wave's 4 heads)
+  u32x4 kst[4];
+  u32x2 vst[4][2];
+  auto kv_load = [&](int64_t t) {
+    const int64_t tt = min(t, t_end - 1);
 #pragma unroll
-  for (int p = 0; p < kPre; ++p)
-    if ((bits >> p) & 1u) {
-      const int64_t j = t_begin * 16 + p;
+    for (int i = 0; i < 4; ++i) {
+      const int h = 4 * wave + i;
+      kst[i] = *(reinterpret_cast<const u32x4*>(a.k) + ((int64_t)h * a.n_pad + tt * 16 + n) * 4 + g);
 #pragma unroll
-      for (int s = 0; s < 4; ++s) zb[p][s] = __builtin_nontemporal_load(zrow + j * 16 + 4 * s);
+      for (int mt = 0; mt < 2; ++mt)
+        vst[i][mt] = *(reinterpret_cast<const u32x2*>(a.vt) + (((int64_t)h * n_tiles_all + tt) * 2 + mt) * 64 + lane);
     }
+  };
+  auto kv_store = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int h = 4 * wave + i;
+      kv[buf].k[h][lane] = kst[i];
+      kv[buf].v[h][0][lane] = vst[i][0];
+      kv[buf].v[h][1][lane] = vst[i][1];
+    }
+  };
+  auto z_load = [&](u32x4 (&dst)[4], int64_t j, bool valid) {
+    const int off = valid ? lane_off + (int)(j * (kCz * 2)) : kOutOfRange;
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      dst[s] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(zres, off, 64 * s, 0));
+  };
+
+  u32x4 zb[kPre][4];
+  uint32_t bits = t_begin < t_end ? tile_valid_bits(tvres, t_begin, start, end) : 0u;
+  if (t_begin < t_end) {
+    kv_load(t_begin);
+    kv_store((int)(t_begin % kKvBufs));
+  }
+#pragma unroll
+  for (int p = 0; p < kPre; ++p) z_load(zb[p], t_begin * 16 + p, (bits >> p) & 1u);
 
   for (int64_t t = t_begin; t < t_end; ++t) {
-    const uint32_t bits_next = (t + 1 < t_end) ? tile_bits(a.mask, t + 1, start, end, lane) : 0u;
+    const uint32_t bits_next = (t + 1 < t_end) ? tile_valid_bits(tvres, t + 1, start, end) : 0u;
     float b[16][4];
 #pragma unroll
     for (int kk = 0; kk < 16; ++kk) {
       const int slot = kk % kPre;
+      if (kk == 0) kv_load(t + 1);
+      if (kk == 8) kv_store((int)((t + 1) % kKvBufs));
       if ((bits >> kk) & 1u) {
         f32x4 acc;
         float rstd;
@@ -275,31 +345,24 @@ __global__ void __launch_bounds__(64, 1) attn_kernel(FastAttnArgs a) {
         for (int i = 0; i < 4; ++i) b[kk][i] = -INFINITY;
       }
       const int nk = kk + kPre;
-      if (nk < 16) {
-        if ((bits >> nk) & 1u) {
-          const int64_t j = t * 16 + nk;
-#pragma unroll
-          for (int s = 0; s < 4; ++s) zb[slot][s] = __builtin_nontemporal_load(zrow + j * 16 + 4 * s);
-        }
-      } else {
-        if ((bits_next >> (nk - 16)) & 1u) {
-          const int64_t j = (t + 1) * 16 + (nk - 16);
-#pragma unroll
-          for (int s = 0; s < 4; ++s) zb[slot][s] = __builtin_nontemporal_load(zrow + j * 16 + 4 * s);
-        }
-      }
+      if (nk < 16)
+        z_load(zb[slot], t * 16 + nk, (bits >> nk) & 1u);
+      else
+        z_load(zb[slot], (t + 1) * 16 + (nk - 16), (bits_next >> (nk - 16)) & 1u);
     }
+    __syncthreads();  // K/V tile t (written during the previous tile) is complete
+    const KvTile& cur = kv[t % kKvBufs];
     transpose_bias(b);
 
 #pragma unroll
     for (int h = 0; h < kH; ++h) {
       const int ha = h >> 2, hi = h & 3;
       const f32x4 cin = {b[4 * ha + 0][hi], b[4 * ha + 1][hi], b[4 * ha + 2][hi], b[4 * ha + 3][hi]};
-      const u32x4 kt = kbase[((int64_t)h * a.n_pad + t * 16 + n) * 4 + g];
-      const u32x2 v0 = vbase[(((int64_t)h * n_tiles_all + t) * 2 + 0) * 64 + lane];
-      const u32x2 v1 = vbase[(((int64_t)h * n_tiles_all + t) * 2 + 1) * 64 + lane];
+      const u32x4 kt = cur.k[h][lane];
+      const u32x2 v0 = cur.v[h][0][lane];
+      const u32x2 v1 = cur.v[h][1][lane];
       // x[r]: logit (base 2, + kShift) of row n, key 4g + r
-      const f32x4 x = mfma32(as_bf16x8(kt), qreg[h], cin);
+      const f32x4 x = mfma32(as_bf16x8(kt), as_bf16x8(qlds[wave][h][lane]), cin);
       const float tmax = max4(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
       const float mnew = fmaxf(m[h], ceilf(tmax));
       const float muse = (mnew == -INFINITY) ? 0.0f : mnew;
@@ -322,7 +385,7 @@ __global__ void __launch_bounds__(64, 1) attn_kernel(FastAttnArgs a) {
   // Partial state of rows q0 + n: o[h][0][i] = acc e = 4g+i, o[h][1][i] = acc
   // e = 16+4g+i (e = 24 is the denominator l).
   const int64_t row = q0 + n;
-  if (row >= a.n_q) return;
+  if (!active || row >= a.n_q) return;
 #pragma unroll
   for (int h = 0; h < kH; ++h) {
     const float l = o[h][1][0];  // valid in lane group 2 (e = 24)
@@ -387,8 +450,9 @@ hipError_t launch_fast_proj(const FastProjArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_fast_attn(const FastAttnArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(attn_kernel, dim3((unsigned)(a.nq_pad / kTileQ), (unsigned)(a.n_kb * a.n_seg)), dim3(64), 0, st,
-                     a);
+  const int64_t n_qt = a.nq_pad / kTileQ;
+  hipLaunchKernelGGL(attn_kernel, dim3((unsigned)((n_qt + kWaves - 1) / kWaves), (unsigned)(a.n_kb * a.n_seg)),
+                     dim3(64 * kWaves), 0, st, a);
   return hipGetLastError();
 }
 
