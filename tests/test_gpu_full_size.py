@@ -1,0 +1,47 @@
+"""The whole-assembly workload at full size (N = 24000, bf16 z = 147 GB) in the
+launch configuration bench.py times (6 key blocks), checked on sampled rows
+against the fp64 oracle, plus full-size properties (GPU)."""
+import numpy as np
+import pytest
+
+from gpu_helpers import DCP_BF16, DCP_F32, Device, log, rel_err, sample_rows, workload
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def big():
+    import torch
+    assert torch.cuda.is_available()
+    wl = workload("asm24000_bf16")
+    log("allocating and generating z for asm24000_bf16 (147 GB)")
+    d = Device(wl)
+    yield d
+    del d
+    torch.cuda.empty_cache()
+
+
+def test_asm24000_sampled_rows(big):
+    wl = big.wl
+    log("case asm24000_bf16 n_kb=6 bf16 out (the benchmark's call), sampled rows")
+    got = big.attention(0, wl.n_tok, wl.n_key_blocks, out_dtype=DCP_BF16).float().cpu().numpy()
+    rows = sample_rows(wl.n_tok, wl.stripes, wl.n_key_blocks, 96, big.mask_host)
+    ref = big.oracle_rows(rows)
+    err = rel_err(got[rows], ref)
+    log(f"  {len(rows)} rows rel err {err:.3e}")
+    assert err <= 1e-2
+
+
+def test_asm24000_blocked_and_deterministic(big):
+    import torch
+    wl = big.wl
+    log("case asm24000_bf16 fp32 out: n_kb=6 twice, n_kb=1")
+    a = big.attention(0, wl.n_tok, wl.n_key_blocks)
+    b = big.attention(0, wl.n_tok, wl.n_key_blocks)
+    assert torch.equal(a, b)
+    c = big.attention(0, wl.n_tok, 1)
+    err = rel_err(c.cpu().numpy(), a.cpu().numpy())
+    log(f"  blocked vs unblocked rel diff {err:.3e}")
+    assert err <= 1e-6
+    # padding (masked) query rows still produce outputs; masked keys are never used
+    assert torch.isfinite(a).all()
