@@ -82,4 +82,51 @@ __device__ __forceinline__ void transpose_bias(float (&b)[16][4]) {
       for (int i = 0; i < 4; ++i) swap16(b[4 * c + r][i], b[4 * (c + 1) + r][i]);
 }
 
+
+// ---- direct-to-LDS loads and explicit waits
+// The DMA loads below are issued from inline asm, so the compiler neither
+// counts them nor inserts waits for them: every wait on their data is an
+// explicit s_waitcnt with a compile-time count. (Ops the compiler cannot see
+// only make its own waits stricter, never looser, because vector-memory
+// loads complete in issue order.)
+constexpr uint32_t kRawBufferFlags = 0x00020000u;
+constexpr int kOutOfRange = 0x7FFFFF00;  // offset past every record: the load moves no data
+
+// 16 bytes per lane from buffer r at byte offset voff into LDS at
+// lds_base + 16 * lane (lds_base: wave-uniform LDS byte address). Waits for
+// this wave's outstanding LDS reads first, so a slot being refilled is never
+// still being read.
+__device__ __forceinline__ void dma_b128(__amdgpu_buffer_rsrc_t r, int voff, uint32_t lds_base) {
+  uint32_t saved;
+  asm volatile(
+      "s_waitcnt lgkmcnt(0)\n\t"
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "buffer_load_dwordx4 %1, %2, 0 offen lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(voff), "s"(r), "s"(lds_base)
+      : "memory");
+}
+
+// Wait until at most N of this wave's vector-memory loads are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Workgroup barrier without the memory-model fence (which would also wait for
+// every outstanding DMA load); LDS written by ds_write is complete because the
+// compiler waits lgkmcnt(0) before s_barrier.
+__device__ __forceinline__ void barrier_lds() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)reinterpret_cast<uintptr_t>(p);
+}
+
 }  // namespace dcp

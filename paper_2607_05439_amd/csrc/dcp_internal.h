@@ -55,7 +55,7 @@ struct FastProjArgs {
   int32_t c_s;
   uint16_t* q;   // [H][nq_pad][32] bf16, scaled by log2(e)/sqrt(d)
   uint16_t* k;   // [H][n_pad][32] bf16
-  uint16_t* vt;  // [H][n_pad/16][2][64][4] bf16: V^T tiles with a row of ones at e = 24
+  uint16_t* vt;  // [H][n_pad/16][64][2][4] bf16: V^T tiles (lane, M-tile) with a row of ones at e = 24
   float* g;      // [n_q][H*d] fp32, sigmoid applied
   uint32_t* tile_valid;  // [n_pad/16]: bit i = key 16t+i exists and is not masked
 };

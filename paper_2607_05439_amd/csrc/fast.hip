@@ -21,6 +21,7 @@
 // each lane's loads are contiguous.
 #include <hip/hip_runtime.h>
 #include <math.h>
+#include <stddef.h>
 #include <stdint.h>
 
 #include "cdna4.h"
@@ -166,7 +167,7 @@ __global__ void __launch_bounds__(64) proj_kernel(FastProjArgs a) {
         if (e == kD) val = valid ? 1.0f : 0.0f;  // row of ones: the softmax denominator
         o[i] = (__bf16)val;
       }
-      u32x2* dst = reinterpret_cast<u32x2*>(a.vt) + ((((int64_t)h * (a.n_pad / 16) + tile) * 2 + et) * 64 + lane);
+      u32x2* dst = reinterpret_cast<u32x2*>(a.vt) + ((((int64_t)h * (a.n_pad / 16) + tile) * 64 + lane) * 2 + et);
       *dst = __builtin_bit_cast(u32x2, o);
     }
     return;
@@ -216,23 +217,29 @@ __global__ void __launch_bounds__(64) proj_kernel(FastProjArgs a) {
 }
 
 // ----------------------------------------------------------------------------- attention
-constexpr int kWaves = 4;   // waves per workgroup: 4 query tiles sharing one key range
-constexpr int kKvBufs = 3;  // K/V tiles staged in LDS: current, next, and one being written
-constexpr uint32_t kRawBufferFlags = 0x00020000u;
-constexpr int kOutOfRange = 0x7FFFFF00;  // buffer offset past every valid record: reads 0, no traffic
+constexpr int kWaves = 4;           // waves per workgroup: 4 query tiles sharing one key range
+constexpr int kRing = 6;            // z slots per wave (LDS ring)
+constexpr int kAhead = kRing - 1;   // keys of z in flight ahead of the one being used
+constexpr int kKvDma = 8;           // DMA loads per wave per K/V tile (4 heads x K, V)
 
-// K and V^T tiles of one 16-key tile for all heads, in matrix-core operand order.
+// One key's z for a wave's 16 rows: [row][16-byte chunk], chunk index XOR row
+// (so the 16 rows of one operand read hit 16 different bank groups).
+struct ZSlot {
+  u32x4 c[16][16];
+};
+// K and V^T of one 16-key tile for all heads, in matrix-core operand order:
+// k[h][L] = lane L's QK^T A operand; v[h][L] = lane L's PV A operands (M-tile 0
+// in .xy, M-tile 1 in .zw).
 struct KvTile {
-  u32x4 k[kH][64];     // lane L: keys' k (A operand of QK^T)
-  u32x2 v[kH][2][64];  // lane L: V^T rows 16*mt + L%16, keys 4(L/16)..+3 (A operand of PV)
+  u32x4 k[kH][64];
+  u32x4 v[kH][64];
 };
 
 typedef const __attribute__((address_space(4))) uint32_t* const_u32_ptr;
 
 // Valid keys of tile t: the per-tile key mask, restricted to [start, end). The
 // mask is read-only during the attention kernel, so it is read through the
-// constant address space: a scalar load that stays out of the vector-memory
-// queue (whose waits are in issue order).
+// constant address space (a scalar load, outside the vector-memory queue).
 __device__ __forceinline__ uint32_t tile_valid_bits(const_u32_ptr tv, int64_t t, int64_t start, int64_t end) {
   const int64_t lo = max(start - t * 16, (int64_t)0), hi = min(end - t * 16, (int64_t)16);
   if (hi <= lo) return 0u;
@@ -240,18 +247,26 @@ __device__ __forceinline__ uint32_t tile_valid_bits(const_u32_ptr tv, int64_t t,
   return tv[t] & range;
 }
 
-// One workgroup = 4 waves = 4 tiles of 16 query rows, all over the same key
-// range (one internal part). z is streamed per wave through registers kPre
-// keys ahead with buffer loads: an invalid (masked or out-of-range) key gets
-// an out-of-range offset, so the load returns zeros without touching memory
-// and every load is unconditional (exact wait counts, no drained pipeline).
-// K/V tiles are loaded one tile ahead, each wave fetching 4 heads, and shared
-// through LDS; one barrier per tile.
+// Outstanding DMA loads allowed when waiting for key kk of a tile: the z loads
+// of the kAhead - 1 keys issued after it, plus the K/V tile loads when those
+// were issued after it (for the first kAhead keys, whose z was issued during
+// the previous tile).
+template <int KK>
+__device__ __forceinline__ void wait_key() {
+  wait_vm<4 * (kAhead - 1) + (KK < kAhead ? kKvDma : 0)>();
+}
+
+// One workgroup = 4 waves = 4 tiles of 16 query rows over the same key range
+// (one internal part). Each wave streams its rows' z through its own LDS ring
+// with direct-to-LDS loads issued kAhead keys ahead; an invalid (masked or
+// out-of-range) key gets an out-of-range offset, so its load moves no data and
+// every load is unconditional. K/V tiles are loaded into LDS one tile ahead,
+// each wave fetching 4 heads; one barrier per tile.
 __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
-  __shared__ KvTile kv[kKvBufs];
-  __shared__ u32x4 qlds[kWaves][kH][64];  // each wave's Q^T operands, one per head
+  __shared__ ZSlot zring[kWaves][kRing];  // 96 KB
+  __shared__ KvTile kv[2];                // 64 KB
   const int tid = threadIdx.x, lane = tid & 63, n = lane & 15, g = lane >> 4;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int64_t n_qt = a.nq_pad / kTileQ;
   const int64_t qt = (int64_t)blockIdx.x * kWaves + wave;
   const bool active = qt < n_qt;
@@ -259,13 +274,15 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
   const int part = blockIdx.y;
   int64_t start, end;
   part_range(a.n_tok, a.n_kb, a.n_seg, part, &start, &end);
+  const int64_t t_begin = start >> 4, t_end = (end + 15) >> 4;
+  const int64_t n_tiles_all = a.n_pad / 16;
 
   bf16x8 whi[4], wlo[4];
   bias_weights(a.w_b, a.gamma, kLog2e, lane, whi, wlo);
-
+  bf16x8 qreg[kH];
 #pragma unroll
   for (int h = 0; h < kH; ++h)
-    qlds[wave][h][lane] = *(reinterpret_cast<const u32x4*>(a.q) + ((int64_t)h * a.nq_pad + q0 + n) * 4 + g);
+    qreg[h] = as_bf16x8(*(reinterpret_cast<const u32x4*>(a.q) + ((int64_t)h * a.nq_pad + q0 + n) * 4 + g));
 
   float m[kH];
   f32x4 o[kH][2];
@@ -278,80 +295,89 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
 
   // z rows q0 .. q0+15 of this wave: one buffer resource, 32-bit byte offsets.
   const int64_t rows_here = min((int64_t)kTileQ, a.n_q - q0);
-  const int64_t row_bytes = a.n_tok * (kCz * 2);
+  const int row_bytes = (int)(a.n_tok * (kCz * 2));
   const __amdgpu_buffer_rsrc_t zres = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(a.z) + q0 * a.n_tok * kCz, 0, (int)(rows_here * row_bytes), kRawBufferFlags);
-  const int lane_off = (int)(n * row_bytes) + 16 * g;  // row n, channels 8g.. of k-step 0
+  // DMA instruction i of a key fills slot rows 4i..4i+3; lane L writes row
+  // 4i + L/16, physical chunk L%16, which holds logical chunk (L%16) ^ row.
+  int zoff[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 4 * i + (lane >> 4);
+    zoff[i] = row * row_bytes + 16 * ((lane & 15) ^ row);
+  }
+  const uint32_t ring_base = lds_addr(&zring[wave][0]);
+  auto z_dma = [&](int64_t j, bool valid, int slot) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      dma_b128(zres, valid ? zoff[i] + (int)j * (kCz * 2) : kOutOfRange,
+               ring_base + (uint32_t)slot * (uint32_t)sizeof(ZSlot) + 1024u * i);
+  };
+  // K/V tiles: this wave fetches heads 4*wave .. 4*wave+3.
+  const __amdgpu_buffer_rsrc_t kres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.k), 0, (int)(kH * a.n_pad * kDp * 2), kRawBufferFlags);
+  const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.vt), 0, (int)(kH * a.n_pad * kDp * 2), kRawBufferFlags);
+  auto kv_dma = [&](int64_t t) {
+    const uint32_t base = lds_addr(&kv[t & 1]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int h = 4 * wave + i;
+      dma_b128(kres, (int)((((int64_t)h * a.n_pad + t * 16 + n) * kDp + 8 * g) * 2),
+               base + (uint32_t)offsetof(KvTile, k) + (uint32_t)(h * 64 * 16));
+      dma_b128(vres, (int)((((int64_t)h * n_tiles_all + t) * 64 + lane) * 16),
+               base + (uint32_t)offsetof(KvTile, v) + (uint32_t)(h * 64 * 16));
+    }
+  };
 
-  const int64_t t_begin = start >> 4, t_end = (end + 15) >> 4;
-  const int64_t n_tiles_all = a.n_pad / 16;
   const const_u32_ptr tvres = (const_u32_ptr)(a.tile_valid);
-
-  // K/V tile t -> registers (this wave's 4 heads)
-  u32x4 kst[4];
-  u32x2 vst[4][2];
-  auto kv_load = [&](int64_t t) {
-    const int64_t tt = min(t, t_end - 1);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int h = 4 * wave + i;
-      kst[i] = *(reinterpret_cast<const u32x4*>(a.k) + ((int64_t)h * a.n_pad + tt * 16 + n) * 4 + g);
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-        vst[i][mt] = *(reinterpret_cast<const u32x2*>(a.vt) + (((int64_t)h * n_tiles_all + tt) * 2 + mt) * 64 + lane);
-    }
-  };
-  auto kv_store = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int h = 4 * wave + i;
-      kv[buf].k[h][lane] = kst[i];
-      kv[buf].v[h][0][lane] = vst[i][0];
-      kv[buf].v[h][1][lane] = vst[i][1];
-    }
-  };
-  auto z_load = [&](u32x4 (&dst)[4], int64_t j, bool valid) {
-    const int off = valid ? lane_off + (int)(j * (kCz * 2)) : kOutOfRange;
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-      dst[s] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(zres, off, 64 * s, 0));
-  };
-
-  u32x4 zb[kPre][4];
   uint32_t bits = t_begin < t_end ? tile_valid_bits(tvres, t_begin, start, end) : 0u;
   if (t_begin < t_end) {
-    kv_load(t_begin);
-    kv_store((int)(t_begin % kKvBufs));
-  }
+    // same issue order as the steady state: the first kAhead keys, then K/V
 #pragma unroll
-  for (int p = 0; p < kPre; ++p) z_load(zb[p], t_begin * 16 + p, (bits >> p) & 1u);
+    for (int p = 0; p < kAhead; ++p) z_dma(t_begin * 16 + p, (bits >> p) & 1u, (int)((t_begin * 16 + p) % kRing));
+    kv_dma(t_begin);
+  }
 
   for (int64_t t = t_begin; t < t_end; ++t) {
     const uint32_t bits_next = (t + 1 < t_end) ? tile_valid_bits(tvres, t + 1, start, end) : 0u;
+    const int slot0 = (int)((t * 16) % kRing);
     float b[16][4];
 #pragma unroll
     for (int kk = 0; kk < 16; ++kk) {
-      const int slot = kk % kPre;
-      if (kk == 0) kv_load(t + 1);
-      if (kk == 8) kv_store((int)((t + 1) % kKvBufs));
+      int slot = slot0 + kk % kRing;
+      if (slot >= kRing) slot -= kRing;
+      if (kk < kAhead)
+        wait_key<0>();
+      else
+        wait_key<kAhead>();
       if ((bits >> kk) & 1u) {
+        const ZSlot& zs = zring[wave][slot];
+        u32x4 zb[4];
+#pragma unroll
+        for (int st = 0; st < 4; ++st) zb[st] = zs.c[n][(4 * st + g) ^ n];
         f32x4 acc;
         float rstd;
-        pair_bias(zb[slot], whi, wlo, a.eps, acc, rstd);
+        pair_bias(zb, whi, wlo, a.eps, acc, rstd);
 #pragma unroll
         for (int i = 0; i < 4; ++i) b[kk][i] = fmaf(acc[i], rstd, kShift);
       } else {
 #pragma unroll
         for (int i = 0; i < 4; ++i) b[kk][i] = -INFINITY;
       }
-      const int nk = kk + kPre;
+      const int nk = kk + kAhead;
+      int nslot = slot + kAhead;
+      if (nslot >= kRing) nslot -= kRing;
       if (nk < 16)
-        z_load(zb[slot], t * 16 + nk, (bits >> nk) & 1u);
+        z_dma(t * 16 + nk, (bits >> nk) & 1u, nslot);
       else
-        z_load(zb[slot], (t + 1) * 16 + (nk - 16), (bits_next >> (nk - 16)) & 1u);
+        z_dma((t + 1) * 16 + (nk - 16), (bits_next >> (nk - 16)) & 1u, nslot);
     }
-    __syncthreads();  // K/V tile t (written during the previous tile) is complete
-    const KvTile& cur = kv[t % kKvBufs];
+    // K/V tile t is complete in this wave (its loads precede the last key's);
+    // after the barrier, in every wave. Tile t-1's K/V buffer is then free.
+    barrier_lds();
+    if (t + 1 < t_end) kv_dma(t + 1);
+    const KvTile& cur = kv[t & 1];
     transpose_bias(b);
 
 #pragma unroll
@@ -359,10 +385,9 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
       const int ha = h >> 2, hi = h & 3;
       const f32x4 cin = {b[4 * ha + 0][hi], b[4 * ha + 1][hi], b[4 * ha + 2][hi], b[4 * ha + 3][hi]};
       const u32x4 kt = cur.k[h][lane];
-      const u32x2 v0 = cur.v[h][0][lane];
-      const u32x2 v1 = cur.v[h][1][lane];
+      const u32x4 vv = cur.v[h][lane];
       // x[r]: logit (base 2, + kShift) of row n, key 4g + r
-      const f32x4 x = mfma32(as_bf16x8(kt), as_bf16x8(qlds[wave][h][lane]), cin);
+      const f32x4 x = mfma32(as_bf16x8(kt), qreg[h], cin);
       const float tmax = max4(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
       const float mnew = fmaxf(m[h], ceilf(tmax));
       const float muse = (mnew == -INFINITY) ? 0.0f : mnew;
@@ -375,12 +400,13 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
         o[h][0] *= alpha;
         o[h][1] *= alpha;
       }
-      o[h][0] = mfma16(as_bf16x4(v0), p, o[h][0]);
-      o[h][1] = mfma16(as_bf16x4(v1), p, o[h][1]);
+      o[h][0] = mfma16(as_bf16x4(u32x2{vv[0], vv[1]}), p, o[h][0]);
+      o[h][1] = mfma16(as_bf16x4(u32x2{vv[2], vv[3]}), p, o[h][1]);
       m[h] = mnew;
     }
     bits = bits_next;
   }
+  wait_vm<0>();  // the last tile's look-ahead loads (no data) before exit
 
   // Partial state of rows q0 + n: o[h][0][i] = acc e = 4g+i, o[h][1][i] = acc
   // e = 16+4g+i (e = 24 is the denominator l).

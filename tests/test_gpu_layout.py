@@ -19,6 +19,7 @@ def probe():
     for f in ("probe_mfma32", "probe_mfma16", "probe_swaps", "probe_transpose"):
         getattr(lib, f).argtypes = [ctypes.c_void_p]
     lib.probe_exp2.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]
+    lib.probe_dma.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
     return lib, torch
 
 
@@ -74,3 +75,21 @@ def test_exp2_of_integers_is_exact(probe):
     want = np.ldexp(np.float32(1.0), k.astype(np.int32)).astype(np.float32)
     want[k < -126] = 0.0  # the hardware flushes denormal results to zero
     assert np.array_equal(y.cpu().numpy(), want)
+
+
+def test_direct_to_lds_loads(probe):
+    lib, torch = probe
+    src = torch.arange(192 * 4, dtype=torch.int32, device="cuda") * 7 + 1
+    out = torch.zeros(256 * 4, dtype=torch.int32, device="cuda")
+    assert lib.probe_dma(src.data_ptr(), out.data_ptr()) == 0
+    s = src.cpu().numpy().reshape(192, 4)
+    o = out.cpu().numpy().reshape(256, 4)
+    lane = np.arange(64)
+    assert np.array_equal(o[:64], s[lane ^ 5])                    # lane L lands at base + 16 L
+    assert np.array_equal(o[64:128], s[64 + (lane ^ 9)])          # destination above 64 KB
+    assert np.array_equal(o[192:256], s[128 + (lane ^ 3)])        # near the top of 160 KB
+    oob = o[128:192]
+    zeros = np.all(oob == 0)
+    untouched = np.all(oob[:, 0].astype(np.uint32) == (0xDEAD0000 + 102400 // 16 + lane).astype(np.uint32))
+    print("out-of-range DMA:", "writes zeros" if zeros else "leaves LDS untouched" if untouched else "other")
+    assert zeros or untouched
