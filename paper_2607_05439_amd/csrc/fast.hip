@@ -74,29 +74,40 @@ __device__ void bias_weights(const float* __restrict__ w_b, const float* __restr
 // One key for the wave's 16 rows: z B operands (k-step s = channels 32s+8g..+7
 // of row n) -> rstd of the pair and the unnormalised projection acc[i] =
 // sum_c W''[4g+i, c] z_c (accumulator rows = heads 4g..4g+3, column = row n).
+// The LayerNorm statistics come from the matrix cores as well: ones . z gives
+// the row sum in every accumulator register, and the diagonal of the Gram tile
+// z . z^T (row n at lane group n/4, register n%4) gives the sum of squares;
+// bf16 products are exact in fp32.
 __device__ __forceinline__ void pair_bias(const u32x4 (&zb)[4], const bf16x8 (&whi)[4], const bf16x8 (&wlo)[4],
-                                          float eps, f32x4& acc, float& rstd) {
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-  float s1 = 0.f, s2 = 0.f;
+                                          float eps, int n, f32x4& acc, float& rstd) {
+  bf16x8 ones;
 #pragma unroll
-  for (int s = 0; s < 4; ++s)
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const bf16x2 v = as_bf16x2(zb[s][p]);
-      s1 = __builtin_amdgcn_fdot2_f32_bf16(v, ones, s1, false);
-      s2 = __builtin_amdgcn_fdot2_f32_bf16(v, v, s2, false);
-    }
-  s1 = sum4(s1);
-  s2 = sum4(s2);
-  const float mu = s1 * (1.0f / kCz);
-  const float var = fmaxf(s2 * (1.0f / kCz) - mu * mu, 0.0f);
-  rstd = __builtin_amdgcn_rsqf(var + eps);
+  for (int i = 0; i < 8; ++i) ones[i] = (__bf16)1.0f;
+  f32x4 s1 = {0.f, 0.f, 0.f, 0.f}, gram = {0.f, 0.f, 0.f, 0.f};
   acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
-    acc = mfma32(whi[s], as_bf16x8(zb[s]), acc);
-    acc = mfma32(wlo[s], as_bf16x8(zb[s]), acc);
+    const bf16x8 zv = as_bf16x8(zb[s]);
+    acc = mfma32(whi[s], zv, acc);
+    s1 = mfma32(ones, zv, s1);
+    acc = mfma32(wlo[s], zv, acc);
+    gram = mfma32(zv, zv, gram);
   }
+  // diagonal of the Gram tile: pick register n%4, then fetch it from lane group n/4
+  const float t0 = (n & 1) ? gram[1] : gram[0];
+  const float t1 = (n & 1) ? gram[3] : gram[2];
+  float d = (n & 2) ? t1 : t0;        // (row 4g + n%4, column n)
+  const int tg = n >> 2;               // the lane group holding row n
+  float lo = d, hi = d;
+  swap32(lo, hi);                      // lo: group g&1, hi: group (g&1)|2
+  d = (tg & 2) ? hi : lo;              // group (g&1) | (tg&2)
+  lo = d;
+  hi = d;
+  swap16(lo, hi);                      // lo: even group of the pair, hi: odd group
+  const float s2 = (tg & 1) ? hi : lo; // group tg: the diagonal entry
+  const float mu = s1[0] * (1.0f / kCz);
+  const float var = fmaxf(s2 * (1.0f / kCz) - mu * mu, 0.0f);
+  rstd = __builtin_amdgcn_rsqf(var + eps);
 }
 
 // ----------------------------------------------------------------------------- projections
@@ -218,7 +229,7 @@ __global__ void __launch_bounds__(64) proj_kernel(FastProjArgs a) {
 
 // ----------------------------------------------------------------------------- attention
 constexpr int kWaves = 4;           // waves per workgroup: 4 query tiles sharing one key range
-constexpr int kRing = 6;            // z slots per wave (LDS ring)
+constexpr int kRing = 8;            // z slots per wave (LDS ring)
 constexpr int kAhead = kRing - 1;   // keys of z in flight ahead of the one being used
 constexpr int kKvDma = 8;           // DMA loads per wave per K/V tile (4 heads x K, V)
 
@@ -261,10 +272,11 @@ __device__ __forceinline__ void wait_key() {
 // with direct-to-LDS loads issued kAhead keys ahead; an invalid (masked or
 // out-of-range) key gets an out-of-range offset, so its load moves no data and
 // every load is unconditional. K/V tiles are loaded into LDS one tile ahead,
-// each wave fetching 4 heads; one barrier per tile.
+// each wave fetching 4 heads, into one LDS buffer; two barriers per tile (the
+// second, after the compute-only attention phase, frees the buffer).
 __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
-  __shared__ ZSlot zring[kWaves][kRing];  // 96 KB
-  __shared__ KvTile kv[2];                // 64 KB
+  __shared__ ZSlot zring[kWaves][kRing];  // 128 KB
+  __shared__ KvTile kv;                   // 32 KB
   const int tid = threadIdx.x, lane = tid & 63, n = lane & 15, g = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int64_t n_qt = a.nq_pad / kTileQ;
@@ -319,7 +331,7 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
   const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(a.vt), 0, (int)(kH * a.n_pad * kDp * 2), kRawBufferFlags);
   auto kv_dma = [&](int64_t t) {
-    const uint32_t base = lds_addr(&kv[t & 1]);
+    const uint32_t base = lds_addr(&kv);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int h = 4 * wave + i;
@@ -358,7 +370,7 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
         for (int st = 0; st < 4; ++st) zb[st] = zs.c[n][(4 * st + g) ^ n];
         f32x4 acc;
         float rstd;
-        pair_bias(zb, whi, wlo, a.eps, acc, rstd);
+        pair_bias(zb, whi, wlo, a.eps, n, acc, rstd);
 #pragma unroll
         for (int i = 0; i < 4; ++i) b[kk][i] = fmaf(acc[i], rstd, kShift);
       } else {
@@ -374,10 +386,9 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
         z_dma((t + 1) * 16 + (nk - 16), (bits_next >> (nk - 16)) & 1u, nslot);
     }
     // K/V tile t is complete in this wave (its loads precede the last key's);
-    // after the barrier, in every wave. Tile t-1's K/V buffer is then free.
+    // after the barrier, in every wave.
     barrier_lds();
-    if (t + 1 < t_end) kv_dma(t + 1);
-    const KvTile& cur = kv[t & 1];
+    const KvTile& cur = kv;
     transpose_bias(b);
 
 #pragma unroll
@@ -404,6 +415,9 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
       o[h][1] = mfma16(as_bf16x4(u32x2{vv[2], vv[3]}), p, o[h][1]);
       m[h] = mnew;
     }
+    // every wave is done with K/V tile t: load tile t+1 into the same buffer
+    barrier_lds();
+    if (t + 1 < t_end) kv_dma(t + 1);
     bits = bits_next;
   }
   wait_vm<0>();  // the last tile's look-ahead loads (no data) before exit
@@ -455,7 +469,7 @@ __global__ void __launch_bounds__(64) bias_kernel(FastBiasArgs a) {
     for (int s = 0; s < 4; ++s) zb[s] = __builtin_nontemporal_load(zrow + c * 16 + 4 * s);
     f32x4 acc;
     float rstd;
-    pair_bias(zb, whi, wlo, a.eps, acc, rstd);
+    pair_bias(zb, whi, wlo, a.eps, n, acc, rstd);
     if (row < a.n_rows) {
       float4 o;
       o.x = fmaf(acc[0], rstd, cst[0]);
