@@ -194,7 +194,18 @@ def main():
     synth.device_read(z.data_ptr(), read_bytes, sink.data_ptr(), sp)
     hip.record(e1, sp)
     read_gbps = read_bytes / (hip.elapsed_ms(e0, e1) * 1e-3) / 1e9
-    progress(f"streaming read of z: {read_gbps:.0f} GB/s")
+    # the attention kernel's own access pattern over the first stripe, no arithmetic
+    pattern_gbps = None
+    if wl.bf16 and cz == 128:
+        q0, nq = wl.stripes[0]
+        zp = z.data_ptr() + q0 * n * cz * wl.elem_bytes
+        synth.device_read_pattern(zp, n, nq, wl.n_key_blocks, sink.data_ptr(), sp)
+        hip.record(e0, sp)
+        synth.device_read_pattern(zp, n, nq, wl.n_key_blocks, sink.data_ptr(), sp)
+        hip.record(e1, sp)
+        pattern_gbps = nq * n * cz * wl.elem_bytes / (hip.elapsed_ms(e0, e1) * 1e-3) / 1e9
+    progress(f"streaming read of z: {read_gbps:.0f} GB/s; attention access pattern, no arithmetic: "
+             f"{pattern_gbps or 0:.0f} GB/s")
 
     progress(f"warmup {args.warmup} steps")
     for _ in range(args.warmup):
@@ -251,6 +262,7 @@ def main():
                      "kernel": "attn_kernel", "kernel_ms": round(avg_kernel_ms, 4),
                      "algorithmic_bytes_per_launch": bytes_per_launch[0]},
         "streaming_read_GBps": round(read_gbps, 1),
+        "pattern_read_GBps": None if pattern_gbps is None else round(pattern_gbps, 1),
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

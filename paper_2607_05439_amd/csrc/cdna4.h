@@ -109,6 +109,21 @@ __device__ __forceinline__ void dma_b128(__amdgpu_buffer_rsrc_t r, int voff, uin
       : "memory");
 }
 
+// The same with the non-temporal hint, for data read exactly once (the pair
+// tensor stream), so it does not displace reused data (K/V tiles) in the caches.
+__device__ __forceinline__ void dma_b128_stream(__amdgpu_buffer_rsrc_t r, int voff, uint32_t lds_base) {
+  uint32_t saved;
+  asm volatile(
+      "s_waitcnt lgkmcnt(0)\n\t"
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "buffer_load_dwordx4 %1, %2, 0 offen nt lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(voff), "s"(r), "s"(lds_base)
+      : "memory");
+}
+
 // Wait until at most N of this wave's vector-memory loads are outstanding.
 template <int N>
 __device__ __forceinline__ void wait_vm() {

@@ -264,7 +264,9 @@ def _dev() -> ctypes.CDLL:
         lib.synth_dev_normal.argtypes = [u64, u64, i64, i32, vp, vp]
         lib.synth_dev_copy.argtypes = [vp, vp, i64, vp]
         lib.synth_dev_read.argtypes = [vp, i64, vp, vp]
-        for f in (lib.synth_dev_z_rows, lib.synth_dev_normal, lib.synth_dev_copy, lib.synth_dev_read):
+        lib.synth_dev_read_pattern.argtypes = [vp, i64, i64, i32, vp, vp]
+        for f in (lib.synth_dev_z_rows, lib.synth_dev_normal, lib.synth_dev_copy, lib.synth_dev_read,
+                  lib.synth_dev_read_pattern):
             f.restype = ctypes.c_int
         _dev_lib = lib
     return _dev_lib
@@ -287,6 +289,13 @@ def normal_fill_device(k: int, start: int, count: int, bf16: bool, ptr: int, str
 def device_copy(src: int, dst: int, nbytes: int, stream: int) -> None:
     if _dev().synth_dev_copy(src, dst, nbytes, stream) != 0:
         raise RuntimeError("synth_dev_copy failed")
+
+
+def device_read_pattern(z: int, n_tok: int, n_rows: int, n_parts: int, sink: int, stream: int) -> None:
+    """Reads the 256-B pair vectors of z rows [0, n_rows) in the fused attention
+    kernel's order, with no arithmetic (the access pattern's bandwidth ceiling)."""
+    if _dev().synth_dev_read_pattern(z, n_tok, n_rows, n_parts, sink, stream) != 0:
+        raise RuntimeError("synth_dev_read_pattern failed")
 
 
 def device_read(src: int, nbytes: int, sink: int, stream: int) -> None:

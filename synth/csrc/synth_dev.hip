@@ -4,8 +4,9 @@
 // counter words, Irwin-Hall(12) normals that are exact fp32 numbers, bf16 by
 // round-to-nearest-even), so a value made here equals the host's bit for bit.
 // This library fills large device inputs (the pair tensor reaches 147 GB) and
-// holds none of the attention arithmetic. It also carries two calibration
-// kernels for the benchmark: a plain copy and a plain streaming read.
+// holds none of the attention arithmetic. It also carries calibration kernels
+// for the benchmark: a plain copy, a plain streaming read, and a read in the
+// fused attention kernel's access pattern.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -110,6 +111,31 @@ __global__ void __launch_bounds__(256) read_kernel(const uint4* __restrict__ src
   if (acc == 0x9E3779B9u) sink[0] = acc;  // practically never taken; keeps the loads
 }
 
+// Reads 256-byte pair vectors of rows [0, n_rows) in the fused attention
+// kernel's visiting order (a wave walks 16 rows key by key, 16 rows x 64 B per
+// load; workgroups of 4 waves; key ranges split into n_parts), with no
+// arithmetic, non-temporal like the kernel's stream: the memory system's
+// ceiling for that access pattern.
+__global__ void __launch_bounds__(256) read_pattern_kernel(const uint4* __restrict__ z, int64_t n_tok, int64_t n_rows,
+                                                           int n_parts, uint32_t* __restrict__ sink) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t r0 = ((int64_t)blockIdx.x * 4 + wave) * 16;
+  if (r0 + 16 > n_rows) return;  // whole 16-row tiles only
+  const int64_t q = n_tok / n_parts, rem = n_tok % n_parts, p = blockIdx.y;
+  const int64_t k0 = p * q + (p < rem ? p : rem), k1 = k0 + q + (p < rem ? 1 : 0);
+  const u32x4* base = reinterpret_cast<const u32x4*>(z) + r0 * n_tok * 16;
+  u32x4 acc = {0u, 0u, 0u, 0u};
+  for (int64_t j = k0; j < k1; ++j) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int idx = i * 64 + lane;  // row idx / 16 of the tile, 16-byte chunk idx % 16
+      acc ^= __builtin_nontemporal_load(base + ((int64_t)(idx >> 4) * n_tok + j) * 16 + (idx & 15));
+    }
+  }
+  if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9E3779B9u) sink[0] = 1;
+}
+
 int grid_for(int64_t items) {
   int64_t g = (items + 255) / 256;
   if (g > 256 * 64) g = 256 * 64;
@@ -144,6 +170,13 @@ int synth_dev_copy(const void* src, void* dst, int64_t bytes, void* stream) {
   if (bytes == 0) return 0;
   hipLaunchKernelGGL(copy_kernel, dim3(grid_for(bytes / 16)), dim3(256), 0, (hipStream_t)stream,
                      (const uint4*)src, (uint4*)dst, bytes / 16);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+int synth_dev_read_pattern(const void* z, int64_t n_tok, int64_t n_rows, int32_t n_parts, void* sink, void* stream) {
+  if (!z || !sink || n_tok <= 0 || n_rows <= 0 || n_parts < 1 || n_parts > n_tok) return -1;
+  hipLaunchKernelGGL(read_pattern_kernel, dim3((unsigned)((n_rows + 63) / 64), (unsigned)n_parts), dim3(256), 0,
+                     (hipStream_t)stream, (const uint4*)z, n_tok, n_rows, n_parts, (uint32_t*)sink);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
