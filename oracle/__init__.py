@@ -28,7 +28,10 @@ def _configure(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.oracle_merge.argtypes = [i32, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.oracle_attention.argtypes = [i64, i32, i32, i32, i32, vp, vp, i32, vp, i64, vp,
                                      vp, vp, vp, vp, vp, vp, vp, vp, f64, i32, vp, vp, vp, vp]
-    for f in (lib.oracle_bias, lib.oracle_attend, lib.oracle_merge, lib.oracle_attention):
+    lib.oracle_sparse_attention.argtypes = [i64, i32, i32, i32, i32, i32, vp, vp, i32, vp, vp, i64,
+                                            vp, vp, vp, vp, vp, vp, vp, vp, f64, i32, vp]
+    for f in (lib.oracle_bias, lib.oracle_attend, lib.oracle_merge, lib.oracle_attention,
+              lib.oracle_sparse_attention):
         f.restype = ctypes.c_int
     return lib
 
@@ -148,3 +151,30 @@ def attention(s: np.ndarray, z_rows: np.ndarray, rows: Sequence[int], mask: Opti
     if rc != 0:
         raise ValueError("oracle_attention rejected its arguments")
     return (out, parts) if return_parts else out
+
+
+def sparse_attention(a: np.ndarray, p_rows: np.ndarray, nbr: np.ndarray, rows: Sequence[int],
+                     w: Dict[str, Optional[np.ndarray]], n_heads: int, head_dim: int, eps: float = 1e-5,
+                     n_blocks: int = 1) -> np.ndarray:
+    """Sparse kNN pair-biased attention for query atoms ``rows``.
+
+    a: [L, c_atom] (fp32 or bf16 bits); p_rows: [len(rows), k, c_ap] gathered
+    pair slices (fp32 or bf16 bits); nbr: [len(rows), k] int32 neighbour atom
+    indices (-1 = empty slot); w: weights as for ``attention``.
+    """
+    a64 = decode(a) if a.dtype == np.uint16 else _f64(a)
+    n_atoms, c_atom = a64.shape
+    pb, dt = _zbuf(p_rows)
+    n_rows, k, c_ap = pb.shape
+    nb = np.ascontiguousarray(nbr, dtype=np.int32)
+    assert nb.shape == (n_rows, k) and len(rows) == n_rows
+    r = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+    ws = {k_: _f64(w.get(k_)) for k_ in ("w_q", "w_k", "w_v", "w_g", "w_b", "b_b", "ln_gamma", "ln_beta")}
+    out = np.empty((n_rows, n_heads * head_dim))
+    rc = _load().oracle_sparse_attention(
+        n_atoms, c_atom, c_ap, n_heads, head_dim, k, _p(a64), pb.ctypes.data, dt, nb.ctypes.data, _p(r), n_rows,
+        _p(ws["w_q"]), _p(ws["w_k"]), _p(ws["w_v"]), _p(ws["w_g"]), _p(ws["w_b"]), _p(ws["b_b"]),
+        _p(ws["ln_gamma"]), _p(ws["ln_beta"]), eps, n_blocks, _p(out))
+    if rc != 0:
+        raise ValueError("oracle_sparse_attention rejected its arguments")
+    return out

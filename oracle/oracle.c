@@ -326,3 +326,108 @@ int oracle_attention(int64_t n_tok, int c_s, int c_z, int n_heads, int d, const 
   free(gp);
   return 0;
 }
+
+/* ---------------------------------------------------------------------------
+ * Sparse (kNN) pair-biased atom attention.
+ *
+ * Paper, Methods, "RFDiffusion 3 preliminaries and notation": atom attention
+ * is sparse: each query atom attends to a budget of k neighbours, and the
+ * slice of the atom pair track P at those k indices is gathered and projected
+ * to the per-head bias. Appendix "Distributed kNN for sparse atom attention":
+ * at each ring step the indices are filtered to the visited column block, K, V
+ * and B are gathered there, and the logits are merged into the running
+ * softmax. Readings as for the token path (LayerNorm over the c_ap channels of
+ * one gathered pair, sigmoid gate); every neighbour slot is one key, and a slot
+ * whose index is not an atom (-1, or any value outside [0, L)) is empty.
+ *
+ *   q_i = W_q a_i, k_j = W_k a_j, v_j = W_v a_j, g_i = sigmoid(W_g a_i)
+ *   b[i,t,h] = sum_c W_b[h,c] LN(p[i,t,:])_c + b_b[h]   (p[i,t,:] = P[i, nbr[i,t], :])
+ *   l[h,i,t] = q_{i,h} . k_{nbr[i,t],h} / sqrt(d) + b[i,t,h]   (-inf for an empty slot)
+ *   (a query whose slots are all empty gives 0)
+ *   out[i, h*d+e] = g_i[h*d+e] * sum_t softmax_t(l[h,i,:]) v_{nbr[i,t],h,e}
+ *
+ * a [L, c_atom] fp64; p_rows [n_rows, k, c_ap] (fp32 or bf16 bits); nbr
+ * [n_rows, k] int32; rows[r] is the atom index of query r. n_blocks == 1: the
+ * plain softmax over all slots; n_blocks > 1: slots grouped by the chunk of
+ * [0, L) their neighbour index falls in, one partial per block, folded in
+ * increasing block order.
+ * ------------------------------------------------------------------------- */
+int oracle_sparse_attention(int64_t n_atoms, int c_atom, int c_ap, int n_heads, int d, int k, const double* a,
+                            const void* p_rows, int p_dtype, const int32_t* nbr, const int64_t* rows, int64_t n_rows,
+                            const double* w_q, const double* w_k, const double* w_v, const double* w_g,
+                            const double* w_b, const double* b_b, const double* gamma, const double* beta, double eps,
+                            int n_blocks, double* out) {
+  if (!a || !p_rows || !nbr || !rows || !w_q || !w_k || !w_v || !w_g || !w_b || !out) return -1;
+  if (n_atoms <= 0 || k <= 0 || n_blocks < 1 || n_blocks > n_atoms) return -1;
+  const int hd = n_heads * d;
+  double* kk = (double*)malloc(sizeof(double) * (size_t)(n_atoms * hd));
+  double* vv = (double*)malloc(sizeof(double) * (size_t)(n_atoms * hd));
+  oracle_linear(n_atoms, c_atom, hd, a, w_k, kk);
+  oracle_linear(n_atoms, c_atom, hd, a, w_v, vv);
+  const double scale = 1.0 / sqrt((double)d);
+#pragma omp parallel
+  {
+    double* ai = (double*)malloc(sizeof(double) * (size_t)c_atom);
+    double* q = (double*)malloc(sizeof(double) * (size_t)hd);
+    double* gp = (double*)malloc(sizeof(double) * (size_t)hd);
+    double* ln = (double*)malloc(sizeof(double) * (size_t)c_ap);
+    double* bias = (double*)malloc(sizeof(double) * (size_t)(k * n_heads));
+    double* logit = (double*)malloc(sizeof(double) * (size_t)k);
+    double* accb = (double*)malloc(sizeof(double) * (size_t)d);
+    double* run = (double*)malloc(sizeof(double) * (size_t)d);
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t r = 0; r < n_rows; ++r) {
+      const int64_t i = rows[r];
+      memcpy(ai, a + i * c_atom, sizeof(double) * (size_t)c_atom);
+      oracle_linear(1, c_atom, hd, ai, w_q, q);
+      oracle_linear(1, c_atom, hd, ai, w_g, gp);
+      for (int t = 0; t < k; ++t)
+        pair_bias(p_rows, p_dtype, (r * k + t) * (int64_t)c_ap, c_ap, n_heads, w_b, b_b, gamma, beta, eps, ln,
+                  bias + t * n_heads);
+      for (int h = 0; h < n_heads; ++h) {
+        double rm = -INFINITY, rl = 0.0;
+        for (int e = 0; e < d; ++e) run[e] = 0.0;
+        for (int blk = 0; blk < n_blocks; ++blk) {
+          int64_t bsize, bstart;
+          oracle_chunk(n_atoms, n_blocks, blk, &bsize, &bstart);
+          /* logits of the slots whose neighbour lies in this block */
+          double mx = -INFINITY;
+          for (int t = 0; t < k; ++t) {
+            const int32_t j = nbr[r * k + t];
+            logit[t] = -INFINITY;
+            if (j < 0 || j >= n_atoms || j < bstart || j >= bstart + bsize) continue;
+            double dot = 0.0;
+            for (int e = 0; e < d; ++e) dot += q[h * d + e] * kk[(int64_t)j * hd + h * d + e];
+            logit[t] = dot * scale + bias[t * n_heads + h];
+            if (logit[t] > mx) mx = logit[t];
+          }
+          if (mx == -INFINITY) continue; /* empty partial */
+          double lb = 0.0;
+          for (int e = 0; e < d; ++e) accb[e] = 0.0;
+          for (int t = 0; t < k; ++t) {
+            if (logit[t] == -INFINITY) continue;
+            const double w = exp(logit[t] - mx);
+            lb += w;
+            for (int e = 0; e < d; ++e) accb[e] += w * vv[(int64_t)nbr[r * k + t] * hd + h * d + e];
+          }
+          fold(d, &rm, &rl, run, mx, lb, accb);
+        }
+        for (int e = 0; e < d; ++e) {
+          const double o = rl > 0.0 ? run[e] / rl : 0.0;
+          out[r * hd + h * d + e] = sigmoid(gp[h * d + e]) * o;
+        }
+      }
+    }
+    free(ai);
+    free(q);
+    free(gp);
+    free(ln);
+    free(bias);
+    free(logit);
+    free(accb);
+    free(run);
+  }
+  free(kk);
+  free(vv);
+  return 0;
+}

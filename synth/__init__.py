@@ -35,6 +35,8 @@ _M2 = np.uint64(0x94D049BB133111EB)
 
 # Tensor ids: one independent stream each.
 T_S, T_Z, T_WQ, T_WK, T_WV, T_WG, T_WB, T_ZBASE, T_MASK, T_GAMMA, T_BETA, T_BB = range(1, 13)
+# atom path: single track A, pair track P, neighbour draws, ragged draws, weights
+(T_A, T_P, T_NBR, T_NBR_RAG, T_AWQ, T_AWK, T_AWV, T_AWG, T_AWB, T_AGAMMA, T_ABETA, T_ABB) = range(13, 25)
 
 
 # ----------------------------------------------------------------------------- numpy definition
@@ -122,6 +124,7 @@ def _host() -> ctypes.CDLL:
         lib.synth_normal_f32.argtypes = [u64, u64, i64, vp]
         lib.synth_normal_bf16.argtypes = [u64, u64, i64, vp]
         lib.synth_z_rows.argtypes = [u64, u64, i64, i64, i32, vp, i64, i32, vp]
+        lib.synth_neighbours.argtypes = [u64, u64, i64, i32, i32, i32, i32, i32, i64, i64, i32, vp]
         _host_lib = lib
     return _host_lib
 
@@ -246,6 +249,114 @@ def z_host(wl: Workload, rows: Sequence[int]) -> np.ndarray:
     """Rows of z[N, N, c_z] on the host, shape [len(rows), N, c_z]."""
     kz, kb = z_keys(wl)
     return z_rows(kz, kb, wl.z_period, wl.n_tok, wl.c_z, rows, wl.bf16)
+
+
+# ----------------------------------------------------------------------------- atom workloads
+@dataclasses.dataclass(frozen=True)
+class AtomWorkload:
+    """Sparse (kNN) pair-biased atom attention: L atoms with single track
+    A[L, c_atom] and pair track P[L, L, c_ap]; the query atoms
+    [q_row0, q_row0 + n_q) attend to k neighbour slots each."""
+    name: str
+    n_atoms: int
+    c_atom: int
+    c_ap: int
+    n_heads: int
+    head_dim: int
+    k: int
+    dtype: str                 # "f32" or "bf16": dtype of A and P
+    n_key_blocks: int
+    q_row0: int
+    n_q: int
+    per_res: int = 8           # atoms per residue
+    per_chain: int = 1600      # atoms per chain
+    win: int = 16              # residue window of the spatial draws
+    q_inter: int = 32          # inter-chain quota, max(32, k/4) at k = 128
+    ragged: bool = False
+    seed: int = 0
+    note: str = ""
+
+    @property
+    def bf16(self) -> bool:
+        return self.dtype == "bf16"
+
+    @property
+    def elem_bytes(self) -> int:
+        return 2 if self.bf16 else 4
+
+
+ATOM_WORKLOADS: Dict[str, AtomWorkload] = {
+    w.name: w
+    for w in [
+        AtomWorkload("atoms200_f32", 200, 128, 16, 4, 32, 128, "f32", 1, 0, 200, per_chain=50, ragged=True,
+                     note="4 chains of 50 atoms: budgets larger than the candidate pools leave empty slots"),
+        AtomWorkload("atoms5000_bf16", 5000, 128, 16, 4, 32, 128, "bf16", 1, 0, 5000, per_chain=1000,
+                     ragged=True, note="RFD3's 5000-atom training crop as 5 chains of 1000; full P = 800 MB"),
+        AtomWorkload("atoms96k_bf16", 96000, 128, 16, 4, 32, 128, "bf16", 4, 24000, 24000,
+                     note="60 chains x 1600 atoms (200 residues x 8); one 24000-row stripe of P "
+                          "(73.7 GB bf16) against 4 column blocks of 24000"),
+    ]
+}
+
+
+def neighbours(wl: AtomWorkload, row0: int, n_rows: int) -> np.ndarray:
+    """Neighbour lists nbr[n_rows, k] int32 of query atoms row0 .. row0+n_rows-1."""
+    out = np.empty((n_rows, wl.k), dtype=np.int32)
+    _host().synth_neighbours(key(wl.seed, T_NBR), key(wl.seed, T_NBR_RAG), wl.n_atoms, wl.per_res, wl.per_chain,
+                             wl.k, wl.win, wl.q_inter, row0, n_rows, int(wl.ragged), out.ctypes.data)
+    return out
+
+
+def atom_weights(wl: AtomWorkload, affine: bool = False) -> Dict[str, Optional[np.ndarray]]:
+    """fp32 weights [out, in] ~ N(0, 1/fan_in); ``affine`` also draws gamma, beta, b_b."""
+    hd = wl.n_heads * wl.head_dim
+    out: Dict[str, Optional[np.ndarray]] = {}
+    for name, tid, rows, fan in (("w_q", T_AWQ, hd, wl.c_atom), ("w_k", T_AWK, hd, wl.c_atom),
+                                 ("w_v", T_AWV, hd, wl.c_atom), ("w_g", T_AWG, hd, wl.c_atom),
+                                 ("w_b", T_AWB, wl.n_heads, wl.c_ap)):
+        scale = np.float32(1.0 / np.sqrt(fan))
+        out[name] = (normal(key(wl.seed, tid), 0, rows * fan) * scale).astype(np.float32).reshape(rows, fan)
+    if affine:
+        out["ln_gamma"] = (np.float32(1.0) + np.float32(0.25) * normal(key(wl.seed, T_AGAMMA), 0, wl.c_ap)
+                           ).astype(np.float32)
+        out["ln_beta"] = normal(key(wl.seed, T_ABETA), 0, wl.c_ap)
+        out["b_b"] = normal(key(wl.seed, T_ABB), 0, wl.n_heads)
+    else:
+        out["ln_gamma"] = out["ln_beta"] = out["b_b"] = None
+    return out
+
+
+def a_host(wl: AtomWorkload) -> np.ndarray:
+    """Atom single track A[L, c_atom]: bf16 bit patterns (uint16) or fp32."""
+    return normal(key(wl.seed, T_A), 0, wl.n_atoms * wl.c_atom, bf16=wl.bf16).reshape(wl.n_atoms, wl.c_atom)
+
+
+def p_gathered_host(wl: AtomWorkload, rows: Sequence[int], nbr: np.ndarray) -> np.ndarray:
+    """P[i, nbr[r, t], :] for i = rows[r] (zeros at empty slots), shape [len(rows), k, c_ap].
+
+    P[i, j, c] = normal(key_P, (i*L + j)*c_ap + c), the same element numbering
+    as the device generator of the pair tensor."""
+    rows = np.asarray(rows, dtype=np.int64)
+    nb = np.asarray(nbr, dtype=np.int64)
+    valid = (nb >= 0) & (nb < wl.n_atoms)
+    j = np.where(valid, nb, 0)
+    e = ((rows[:, None] * wl.n_atoms + j)[:, :, None] * wl.c_ap + np.arange(wl.c_ap)[None, None, :])
+    v = normal_np_at(key(wl.seed, T_P), e.astype(np.uint64).ravel()).reshape(e.shape)
+    v = np.where(valid[:, :, None], v, np.float32(0.0)).astype(np.float32)
+    return bf16_round(v) if wl.bf16 else v
+
+
+def p_rows_host(wl: AtomWorkload, rows: Sequence[int]) -> np.ndarray:
+    """Dense rows of P on the host, shape [len(rows), L, c_ap] (small L only)."""
+    return z_rows(key(wl.seed, T_P), 0, 0, wl.n_atoms, wl.c_ap, rows, wl.bf16)
+
+
+def p_fill_device(wl: AtomWorkload, ptr: int, row0: int, n_rows: int, stream: int) -> None:
+    """Write rows [row0, row0+n_rows) of P into device memory at ``ptr``."""
+    rc = _dev().synth_dev_z_rows(key(wl.seed, T_P), 0, 0, wl.n_atoms, wl.c_ap, row0, n_rows, int(wl.bf16), ptr,
+                                 stream)
+    if rc != 0:
+        raise RuntimeError(f"synth_dev_z_rows failed ({rc})")
 
 
 # ----------------------------------------------------------------------------- device twin

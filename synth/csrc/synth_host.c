@@ -99,3 +99,79 @@ void synth_z_rows(uint64_t key_z, uint64_t key_base, int64_t period, int64_t n_t
     }
   }
 }
+
+/* Neighbour lists for sparse atom attention, nbr[r, t] for query atoms
+ * i = row0 + r (r < n_rows), slots t < k; -1 marks an empty slot.
+ *
+ * Stand-in for the paper's kNN budget (query atom plus flanking residues in
+ * sequence, then spatial neighbours, with an inter-chain quota when there are
+ * more than three chains), made without coordinates:
+ *   atoms are grouped into residues of `per_res` atoms and chains of
+ *   `per_chain` atoms (the last chain may be shorter); atom i lies in chain
+ *   c = i / per_chain, at residue r = (i % per_chain) / per_res;
+ *   1. sequence-local: every atom of residues r-1, r, r+1 of the same chain,
+ *      in index order;
+ *   2. intra-chain: atoms drawn uniformly from residues r-win .. r+win of the
+ *      same chain, skipping repeats, until k - q_inter slots are filled;
+ *   3. inter-chain (only with more than three chains): q_inter atoms drawn
+ *      uniformly from residues r-win .. r+win of chains c+1, c-1 (cyclic, in
+ *      turn), skipping repeats;
+ *   draws use word(key, i*8192 + a), a the attempt number (attempts 0..4095
+ *   for step 2, 4096..8191 for step 3); unfilled slots stay -1.
+ *   ragged != 0: rows with word(key2, i) % 8 == 0 then empty their last
+ *   word(key2, i) / 8 % (k/2) slots (budgets not filled). */
+static int64_t nb_window(int64_t chain0, int64_t chain_len, int64_t per_res, int64_t r_lo, int64_t r_hi,
+                         int64_t* lo) {
+  int64_t a = chain0 + (r_lo < 0 ? 0 : r_lo) * per_res;
+  int64_t b = chain0 + (r_hi + 1) * per_res;
+  if (b > chain0 + chain_len) b = chain0 + chain_len;
+  *lo = a;
+  return b > a ? b - a : 0;
+}
+
+static int nb_has(const int32_t* row, int n, int32_t j) {
+  for (int t = 0; t < n; ++t)
+    if (row[t] == j) return 1;
+  return 0;
+}
+
+void synth_neighbours(uint64_t key, uint64_t key2, int64_t n_atoms, int32_t per_res, int32_t per_chain, int32_t k,
+                      int32_t win, int32_t q_inter, int64_t row0, int64_t n_rows, int32_t ragged, int32_t* out) {
+  const int64_t n_chains = (n_atoms + per_chain - 1) / per_chain;
+  const int32_t quota = n_chains > 3 ? (q_inter < k ? q_inter : k) : 0;
+#pragma omp parallel for schedule(static)
+  for (int64_t rr = 0; rr < n_rows; ++rr) {
+    const int64_t i = row0 + rr;
+    int32_t* row = out + rr * k;
+    for (int t = 0; t < k; ++t) row[t] = -1;
+    const int64_t c = i / per_chain, c0 = c * per_chain;
+    const int64_t clen = (c0 + per_chain <= n_atoms) ? per_chain : n_atoms - c0;
+    const int64_t r = (i - c0) / per_res;
+    int n = 0;
+    int64_t lo, cnt;
+    cnt = nb_window(c0, clen, per_res, r - 1, r + 1, &lo);
+    for (int64_t j = lo; j < lo + cnt && n < k; ++j) row[n++] = (int32_t)j;
+    cnt = nb_window(c0, clen, per_res, r - win, r + win, &lo);
+    for (uint64_t a = 0; a < 4096 && n < k - quota && cnt > 0; ++a) {
+      const int32_t j = (int32_t)(lo + (int64_t)(synth_word(key, (uint64_t)i * 8192 + a) % (uint64_t)cnt));
+      if (!nb_has(row, n, j)) row[n++] = j;
+    }
+    const int target = n + quota < k ? n + quota : k;
+    for (uint64_t a = 0; a < 4096 && n < target; ++a) {
+      const int64_t cc = (a & 1) ? (c + n_chains - 1) % n_chains : (c + 1) % n_chains;
+      const int64_t cc0 = cc * per_chain;
+      const int64_t cclen = (cc0 + per_chain <= n_atoms) ? per_chain : n_atoms - cc0;
+      cnt = nb_window(cc0, cclen, per_res, r - win, r + win, &lo);
+      if (cnt <= 0) continue;
+      const int32_t j = (int32_t)(lo + (int64_t)(synth_word(key, (uint64_t)i * 8192 + 4096 + a) % (uint64_t)cnt));
+      if (!nb_has(row, n, j)) row[n++] = j;
+    }
+    if (ragged) {
+      const uint64_t w = synth_word(key2, (uint64_t)i);
+      if (w % 8 == 0) {
+        const int drop = (int)((w / 8) % (uint64_t)(k / 2 > 0 ? k / 2 : 1));
+        for (int t = k - drop; t < k; ++t) row[t] = -1;
+      }
+    }
+  }
+}

@@ -14,6 +14,12 @@ library ``oracle._lib`` currently holds) disagrees with:
   equivariance, a masked key equals a deleted one);
 * brute force at 40 significant digits on tiny inputs (mpmath).
 
+The sparse (kNN) atom attention has its own pins: torch's SDPA over each
+query's gathered keys, the dense pipeline when every atom is a neighbour,
+closed forms (one neighbour atom in every slot, all slots empty), slot
+permutation, empty slots equal deleted ones, blocked equals unblocked, and
+brute force at 40 digits.
+
 ``tests/test_oracle_mutants.py`` plants plausible mistakes in copies of the
 oracle's C source and checks that every one of them fails at least one pin.
 """
@@ -396,6 +402,177 @@ def pin_bruteforce_mpmath():
                     num = mpmath.fsum(x * lin(Wv, S[j])[hh * d + e] for j, x in wts)
                     ref = gi[hh * d + e] * num / den
                     assert abs(float(ref) - got[i, hh * d + e]) <= 1e-13 * max(1.0, abs(float(ref))), (seed, i, hh, e)
+
+
+# ----------------------------------------------------------------------------- sparse kNN attention
+def _sparse_case(seed=0, L=11, c_atom=6, c_ap=5, h=2, d=3, k=7, n_rows=5, empty_frac=0.25, affine=True):
+    """Small random sparse case: A, gathered P slices, neighbour lists (repeats
+    allowed), query rows, weights."""
+    r = _rng(seed)
+    a = r.standard_normal((L, c_atom)).astype(np.float32)
+    rows = r.choice(L, n_rows, replace=False)
+    nbr = r.integers(0, L, (n_rows, k)).astype(np.int32)
+    nbr[r.random((n_rows, k)) < empty_frac] = -1
+    nbr[:, 0] = r.integers(0, L, n_rows)  # every query keeps a neighbour
+    p = r.standard_normal((n_rows, k, c_ap)).astype(np.float32)
+    w = {
+        "w_q": (r.standard_normal((h * d, c_atom)) / np.sqrt(c_atom)).astype(np.float32),
+        "w_k": (r.standard_normal((h * d, c_atom)) / np.sqrt(c_atom)).astype(np.float32),
+        "w_v": (r.standard_normal((h * d, c_atom)) / np.sqrt(c_atom)).astype(np.float32),
+        "w_g": (r.standard_normal((h * d, c_atom)) / np.sqrt(c_atom)).astype(np.float32),
+        "w_b": (r.standard_normal((h, c_ap)) / np.sqrt(c_ap)).astype(np.float32),
+        "ln_gamma": (1 + 0.3 * r.standard_normal(c_ap)).astype(np.float32) if affine else None,
+        "ln_beta": (0.5 * r.standard_normal(c_ap)).astype(np.float32) if affine else None,
+        "b_b": r.standard_normal(h).astype(np.float32) if affine else None,
+    }
+    return a, p, nbr, rows, w
+
+
+def _torch_sparse(a, p, nbr, rows, w, h, d, eps=1e-5):
+    """Per query: gather K, V at the neighbour indices, bias from torch's
+    layer_norm + linear on the gathered P slices, then torch's SDPA with -inf at
+    empty slots, then the gate (fp64, CPU)."""
+    t = lambda x: None if x is None else torch.from_numpy(np.asarray(x, dtype=np.float64))
+    A = t(a)
+    L = A.shape[0]
+    K = F.linear(A, t(w["w_k"])).view(L, h, d)
+    V = F.linear(A, t(w["w_v"])).view(L, h, d)
+    out = []
+    for r, i in enumerate(rows):
+        q = F.linear(A[i], t(w["w_q"])).view(h, 1, d)
+        g = torch.sigmoid(F.linear(A[i], t(w["w_g"])))
+        j = torch.from_numpy(np.asarray(nbr[r], dtype=np.int64))
+        valid = (j >= 0) & (j < L)
+        jj = torch.where(valid, j, torch.zeros_like(j))
+        P = t(p[r])
+        b = F.linear(F.layer_norm(P, (P.shape[-1],), t(w.get("ln_gamma")), t(w.get("ln_beta")), eps),
+                     t(w["w_b"]), t(w.get("b_b")))  # [k, h]
+        bias = b.t().masked_fill(~valid[None, :], float("-inf"))[:, None, :]  # [h, 1, k]
+        o = F.scaled_dot_product_attention(q, K[jj].transpose(0, 1).contiguous(), V[jj].transpose(0, 1).contiguous(),
+                                           attn_mask=bias)
+        out.append((g * o.reshape(h * d)).numpy())
+    return np.stack(out)
+
+
+def pin_sparse_sdpa_torch():
+    for seed, kw in ((40, {}), (41, dict(L=20, k=13, n_rows=8, h=3, d=2)), (42, dict(affine=False, empty_frac=0.6))):
+        a, p, nbr, rows, w = _sparse_case(seed, **kw)
+        h, d = w["w_b"].shape[0], w["w_q"].shape[0] // w["w_b"].shape[0]
+        got = oracle.sparse_attention(a, p, nbr, rows, w, h, d)
+        ref = _torch_sparse(a, p, nbr, rows, w, h, d)
+        assert _rel(got, ref) <= 1e-12, (seed, _rel(got, ref))
+
+
+def pin_sparse_full_neighbourhood_is_dense():
+    """Every atom a neighbour, slot t = atom t, P slices = rows of a pair
+    tensor: the token path's definition, composed from torch routines, with
+    masked keys as empty slots."""
+    s, z, w, mask = _case(43, n=10, c_s=5, c_z=6, h=2, d=3)
+    rows = np.array([0, 3, 9, 4])
+    nbr = np.tile(np.where(mask == 1, np.arange(10), -1).astype(np.int32), (len(rows), 1))
+    got = oracle.sparse_attention(s, z[rows], nbr, rows, w, 2, 3)
+    ref = _torch_pipeline(s, z, w, mask, 2, 3)[rows]
+    assert _rel(got, ref) <= 1e-12, _rel(got, ref)
+
+
+def pin_sparse_one_neighbour_atom():
+    """All slots on one atom j (different pair slices): out = g * v_j."""
+    a, p, nbr, rows, w = _sparse_case(44, affine=True, empty_frac=0.0)
+    jstar = np.array([3, 7, 0, 10, 5], dtype=np.int32)
+    nbr[:] = jstar[:, None]
+    nbr[1, 2:4] = -1
+    got = oracle.sparse_attention(a, p, nbr, rows, w, 2, 3)
+    A = a.astype(np.float64)
+    v = A[jstar] @ w["w_v"].astype(np.float64).T
+    g = 1.0 / (1.0 + np.exp(-(A[rows] @ w["w_g"].astype(np.float64).T)))
+    assert _rel(got, g * v) <= 1e-13, _rel(got, g * v)
+
+
+def pin_sparse_all_empty_is_zero():
+    a, p, nbr, rows, w = _sparse_case(45)
+    nbr[2, :] = -1
+    nbr[4, :] = 11  # == L: not an atom
+    got = oracle.sparse_attention(a, p, nbr, rows, w, 2, 3)
+    assert np.all(got[2] == 0.0) and np.all(got[4] == 0.0)
+    assert np.all(np.abs(got[0]) > 0.0)
+
+
+def pin_sparse_slot_permutation():
+    a, p, nbr, rows, w = _sparse_case(46, k=9)
+    base = oracle.sparse_attention(a, p, nbr, rows, w, 2, 3)
+    perm = _rng(47).permutation(9)
+    got = oracle.sparse_attention(a, p[:, perm], nbr[:, perm], rows, w, 2, 3)
+    assert _rel(got, base) <= 1e-13
+
+
+def pin_sparse_empty_equals_deleted():
+    a, p, nbr, rows, w = _sparse_case(48, k=8, empty_frac=0.0)
+    nb = nbr.copy()
+    nb[:, 5] = -1
+    nb[1, 2] = 1000  # out of range counts as empty too
+    got = oracle.sparse_attention(a, p, nb, rows, w, 2, 3)
+    keep = [t for t in range(8) if t != 5]
+    ref = np.empty_like(got)
+    for r in range(len(rows)):
+        kk = [t for t in keep if not (r == 1 and t == 2)]
+        ref[r] = oracle.sparse_attention(a, p[r:r + 1, kk], nbr[r:r + 1, kk], rows[r:r + 1], w, 2, 3)[0]
+    assert np.array_equal(got, ref) or _rel(got, ref) <= 1e-14
+
+
+def pin_sparse_blocked_equals_unblocked():
+    a, p, nbr, rows, w = _sparse_case(49, L=23, k=15, n_rows=9)
+    base = oracle.sparse_attention(a, p, nbr, rows, w, 2, 3)
+    for nb in (2, 3, 7, 23):
+        got = oracle.sparse_attention(a, p, nbr, rows, w, 2, 3, n_blocks=nb)
+        assert _rel(got, base) <= 1e-12, nb
+
+
+def pin_sparse_affine_constants_irrelevant():
+    a, p, nbr, rows, w = _sparse_case(50)
+    w0 = dict(w, ln_beta=None, b_b=None)
+    assert _rel(oracle.sparse_attention(a, p, nbr, rows, w, 2, 3),
+                oracle.sparse_attention(a, p, nbr, rows, w0, 2, 3)) <= 1e-13
+
+
+def pin_sparse_bruteforce_mpmath():
+    """The sparse definition at 40 digits on tiny inputs."""
+    mpmath.mp.dps = 40
+    for seed, kw in ((51, dict(L=6, c_atom=3, c_ap=4, h=2, d=2, k=4, n_rows=3)),
+                     (52, dict(L=5, c_atom=4, c_ap=3, h=1, d=3, k=5, n_rows=2))):
+        a, p, nbr, rows, w = _sparse_case(seed, **kw)
+        h, d = kw["h"], kw["d"]
+        got = oracle.sparse_attention(a, p, nbr, rows, w, h, d)
+        M = lambda x: [[mpmath.mpf(float(v)) for v in row] for row in np.atleast_2d(x)]
+        A, Wq, Wk, Wv, Wg, Wb = (M(x) for x in (a, w["w_q"], w["w_k"], w["w_v"], w["w_g"], w["w_b"]))
+        gam = [mpmath.mpf(float(x)) for x in w["ln_gamma"]]
+        bet = [mpmath.mpf(float(x)) for x in w["ln_beta"]]
+        bb = [mpmath.mpf(float(x)) for x in w["b_b"]]
+        eps = mpmath.mpf(1e-5)
+        c_ap = kw["c_ap"]
+        lin = lambda W, x: [mpmath.fsum(W[o][c] * x[c] for c in range(len(x))) for o in range(len(W))]
+        for r, i in enumerate(rows):
+            qi, gi = lin(Wq, A[i]), [1 / (1 + mpmath.exp(-t)) for t in lin(Wg, A[i])]
+            for hh in range(h):
+                logits = []
+                for t in range(kw["k"]):
+                    j = int(nbr[r, t])
+                    if j < 0:
+                        continue
+                    pp = [mpmath.mpf(float(x)) for x in p[r, t]]
+                    mu = mpmath.fsum(pp) / c_ap
+                    var = mpmath.fsum((x - mu) ** 2 for x in pp) / c_ap
+                    lnv = [gam[c] * (pp[c] - mu) / mpmath.sqrt(var + eps) + bet[c] for c in range(c_ap)]
+                    b = mpmath.fsum(Wb[hh][c] * lnv[c] for c in range(c_ap)) + bb[hh]
+                    kj = lin(Wk, A[j])
+                    dot = mpmath.fsum(qi[hh * d + e] * kj[hh * d + e] for e in range(d))
+                    logits.append((j, dot / mpmath.sqrt(d) + b))
+                mx = max(x for _, x in logits)
+                wts = [(j, mpmath.exp(x - mx)) for j, x in logits]
+                den = mpmath.fsum(x for _, x in wts)
+                for e in range(d):
+                    num = mpmath.fsum(x * lin(Wv, A[j])[hh * d + e] for j, x in wts)
+                    ref = gi[hh * d + e] * num / den
+                    assert abs(float(ref) - got[r, hh * d + e]) <= 1e-13 * max(1.0, abs(float(ref))), (seed, r, hh, e)
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -44,6 +44,18 @@ MUTANTS = [
     ("blocked partial not rescaled",
      "for (int e = 0; e < d; ++e) acc[e] = a * acc[e] + b * accb[e];",
      "for (int e = 0; e < d; ++e) acc[e] = acc[e] + accb[e];"),
+    ("sparse empty slot read as atom 0", "const int32_t j = nbr[r * k + t];",
+     "const int32_t j = nbr[r * k + t] < 0 ? 0 : nbr[r * k + t];"),
+    ("sparse pair slice of slot 0", "pair_bias(p_rows, p_dtype, (r * k + t) * (int64_t)c_ap,",
+     "pair_bias(p_rows, p_dtype, (r * k) * (int64_t)c_ap,"),
+    ("sparse value of the query atom", "accb[e] += w * vv[(int64_t)nbr[r * k + t] * hd + h * d + e];",
+     "accb[e] += w * vv[(int64_t)i * hd + h * d + e];"),
+    ("sparse block filter overlaps", "j < bstart || j >= bstart + bsize) continue;",
+     "j < bstart || j > bstart + bsize) continue;"),
+    ("sparse gate dropped", "out[r * hd + h * d + e] = sigmoid(gp[h * d + e]) * o;",
+     "out[r * hd + h * d + e] = o;"),
+    ("sparse query from key weights", "oracle_linear(1, c_atom, hd, ai, w_q, q);",
+     "oracle_linear(1, c_atom, hd, ai, w_k, q);"),
 ]
 
 RUNNER = r"""

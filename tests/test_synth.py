@@ -62,3 +62,51 @@ def test_weights_scale():
     assert abs(w["w_q"].std() * np.sqrt(384) - 1.0) < 0.02
     assert abs(w["w_b"].std() * np.sqrt(128) - 1.0) < 0.05
     assert not np.array_equal(w["w_q"], w["w_k"])
+
+
+def test_neighbour_lists_properties():
+    """The kNN stand-in: in range, no repeats, the sequence-local atoms first,
+    the inter-chain quota when there are more than three chains, deterministic."""
+    wl = synth.ATOM_WORKLOADS["atoms5000_bf16"]
+    nb = synth.neighbours(wl, 0, wl.n_atoms)
+    assert nb.shape == (wl.n_atoms, wl.k) and nb.dtype == np.int32
+    assert ((nb >= -1) & (nb < wl.n_atoms)).all()
+    for i in (0, 1, 998, 999, 1000, 2345, 4999):
+        row = nb[i][nb[i] >= 0]
+        assert len(row) == len(set(row.tolist()))
+        c0 = i // wl.per_chain * wl.per_chain
+        r = (i - c0) // wl.per_res
+        local = list(range(c0 + max(r - 1, 0) * wl.per_res, min(c0 + (r + 2) * wl.per_res, c0 + wl.per_chain)))
+        assert row[:len(local)].tolist() == local
+        if len(row) == wl.k:  # not one of the ragged rows
+            assert (row // wl.per_chain != i // wl.per_chain).sum() == wl.q_inter
+    assert np.array_equal(nb[100:200], synth.neighbours(wl, 100, 100))
+    # ragged rows: some budgets left partly empty, filled slots stay in front
+    valid = nb >= 0
+    assert (valid.sum(1) < wl.k).any() and (valid.sum(1) == wl.k).mean() > 0.8
+    assert all(not valid[i, t] or valid[i, :t].all() for i in range(0, 5000, 37) for t in range(wl.k))
+
+
+def test_neighbour_lists_small_pools():
+    """Fewer candidates than slots: every candidate once, the rest empty."""
+    wl = synth.ATOM_WORKLOADS["atoms200_f32"]
+    nb = synth.neighbours(wl, 0, wl.n_atoms)
+    for i in (0, 77, 199):
+        row = nb[i][nb[i] >= 0]
+        own = row[row // wl.per_chain == i // wl.per_chain]
+        assert sorted(own.tolist()) == list(range(i // 50 * 50, i // 50 * 50 + 50))
+        assert len(row) - len(own) == wl.q_inter
+
+
+def test_pair_slices_match_dense_rows():
+    wl = synth.ATOM_WORKLOADS["atoms200_f32"]
+    rows = [3, 150]
+    nb = synth.neighbours(wl, 0, wl.n_atoms)[rows]
+    got = synth.p_gathered_host(wl, rows, nb)
+    dense = synth.p_rows_host(wl, rows)
+    for r in range(2):
+        for t in range(wl.k):
+            if nb[r, t] >= 0:
+                assert np.array_equal(got[r, t], dense[r, nb[r, t]])
+            else:
+                assert not got[r, t].any()
