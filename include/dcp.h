@@ -143,10 +143,79 @@ int dcp_block_merge(int32_t n_parts, int64_t n_rows, int32_t n_heads, int32_t he
                     const float* l_parts, const float* acc_parts, float* m_out, float* l_out, float* acc_out,
                     const float* gate, void* out, int32_t out_dtype, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Sparse (kNN) pair-biased gated attention over atoms.
+ *
+ * Paper, Methods, "RFDiffusion 3 preliminaries and notation": atoms carry a
+ * single track A[L, c_atom] and a pair track P[L, L, c_ap]; atom attention is
+ * sparse, each query atom attending to a budget of k neighbours, and the slice
+ * of P at those neighbours is gathered and projected to the per-head bias.
+ * Appendix "Distributed kNN for sparse atom attention": per ring step the
+ * neighbour indices are filtered to the visited column block, K, V and the
+ * bias are gathered there, and the logits are merged into the running softmax.
+ * Readings as for the token path: b = Linear(LayerNorm(p)) over the c_ap
+ * channels of one gathered pair, output gated by sigmoid(W_g a_i).
+ *
+ * For query atoms i = q_row0 + r, r < n_q, and slots t < k with neighbour
+ * j_t = nbr[r, t] (a slot whose index is outside [0, L) is empty):
+ *   b[r,t,h] = sum_c W_b[h,c] LayerNorm(P[i, j_t, :])_c + b_b[h],
+ *   l[h,r,t] = (W_q a_i)_h . (W_k a_{j_t})_h / sqrt(d) + b[r,t,h]   (-inf if empty),
+ *   out[r, h*d+e] = sigmoid(W_g a_i)[h*d+e] * sum_t softmax_t(l[h,r,:]) (W_v a_{j_t})_{h,e};
+ *   a query whose slots are all empty gives 0. A neighbour listed twice is two keys.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  int64_t n_atoms;    /* L: rows of a, neighbour index range                     */
+  int32_t c_atom;     /* atom single-track channels                              */
+  int32_t c_ap;       /* atom pair channels                                      */
+  int32_t n_heads;    /* H                                                       */
+  int32_t head_dim;   /* d                                                       */
+  int32_t k;          /* neighbour slots per query atom                          */
+  int32_t act_dtype;  /* dcp_dtype of a and p                                    */
+  int32_t out_dtype;  /* dcp_dtype of out                                        */
+  int32_t p_gathered; /* 0: p holds dense rows of P; 1: p holds gathered slices  */
+  float ln_eps;       /* LayerNorm epsilon, >= 0                                 */
+} dcp_sparse_shape;
+
+/* Supported: H = 4, d = 32, c_ap = 16 (the paper's atom attention), k <= 256,
+ * L <= 4,000,000, c_atom <= 4096 (a multiple of 32 when act_dtype = BF16).
+ * Other shapes return DCP_ERR_UNSUPPORTED. */
+
+/* Workspace bytes for dcp_sparse_pair_bias_attention (written to *bytes). Host-only. */
+int dcp_sparse_workspace_size(const dcp_sparse_shape* shape, int64_t n_q, size_t* bytes);
+
+/* Sparse pair-biased gated attention of the query atoms [q_row0, q_row0 + n_q).
+ *   a           [L, c_atom] act_dtype, 16-byte aligned
+ *   p           p_gathered = 0: [n_q, L, c_ap], the stripe's rows of P, i.e.
+ *               &P[q_row0, 0, 0] of a contiguous P[L, L, c_ap];
+ *               p_gathered = 1: [n_q, k, c_ap], P[i, nbr[r, t], :] already
+ *               gathered (the paper's P_sparse; empty slots are not read);
+ *               act_dtype, 16-byte aligned
+ *   nbr         [n_q, k] int32 neighbour atom indices; -1 (or any index
+ *               outside [0, L)) marks an empty slot; 4-byte aligned
+ *   n_q         0 <= n_q, q_row0 >= 0, q_row0 + n_q <= L (n_q = 0 is a no-op)
+ *   n_key_blocks in [1, L]: the atoms are split into this many column blocks
+ *               by the paper's chunk rule, and each query's slots are
+ *               processed block by block in increasing order, folded into a
+ *               running softmax (the ring steps). Any value gives the same
+ *               result up to fp32 rounding.
+ *   out         [n_q, H*d] out_dtype, 16-byte aligned
+ *   workspace   at least dcp_sparse_workspace_size() bytes, 256-byte aligned
+ * Only w_q, w_k, w_v, w_g ([H*d, c_atom]), w_b ([H, c_ap]) and ln_gamma
+ * ([c_ap] or NULL) of `weights` are read: ln_beta and b_b add a per-head
+ * constant to every logit of a query and do not change the result. Softmax
+ * statistics, weights and accumulation are fp32; with BF16 activations the
+ * projected k and v are stored as bf16 and the projections run on the matrix
+ * cores (weights as a bf16 hi+lo pair). */
+int dcp_sparse_pair_bias_attention(const dcp_sparse_shape* shape, const dcp_weights* weights, const void* a,
+                                   const void* p, const int32_t* nbr, int64_t q_row0, int64_t n_q,
+                                   int32_t n_key_blocks, void* out, void* workspace, size_t workspace_bytes,
+                                   void* stream);
+
 /* Optional timing hook: when both are non-NULL hipEvent_t handles, the calling
- * thread's next dcp_pair_bias_attention calls record `start` just before and
- * `stop` just after the fused attention kernel, on that call's stream. Pass
- * NULL, NULL to clear. Host-only. */
+ * thread's next dcp_pair_bias_attention and dcp_sparse_pair_bias_attention
+ * calls record `start` just before and `stop` just after the attention kernel
+ * (after the projections), on that call's stream. Pass NULL, NULL to clear.
+ * Host-only. */
 int dcp_set_timing_events(void* start_event, void* stop_event);
 
 /* Message for the calling thread's last non-OK status ("" if none). */

@@ -3,7 +3,8 @@
 Every step of the computation runs in the library's HIP kernels; PyTorch is
 used for device memory and streams. The functions carry the C names
 (``dcp_pair_bias_attention``, ``dcp_bias_project``, ``dcp_block_merge``,
-``dcp_workspace_size``) and accept torch tensors (device pointers are taken
+``dcp_workspace_size``, ``dcp_sparse_pair_bias_attention``,
+``dcp_sparse_workspace_size``) and accept torch tensors (device pointers are taken
 from ``data_ptr()``) or plain integer addresses. Loading fails loudly when the
 library has not been built: there is no fallback.
 """
@@ -19,7 +20,8 @@ LIB_PATH = os.path.join(_HERE, "libdcp.so")
 DCP_F32, DCP_BF16 = 0, 1
 DCP_OK, DCP_ERR_INVALID_ARGUMENT, DCP_ERR_UNSUPPORTED, DCP_ERR_WORKSPACE, DCP_ERR_HIP = 0, -1, -2, -3, -4
 EXPORTS = ("dcp_workspace_size", "dcp_pair_bias_attention", "dcp_bias_project", "dcp_block_merge",
-           "dcp_set_timing_events", "dcp_last_error", "dcp_version")
+           "dcp_sparse_workspace_size", "dcp_sparse_pair_bias_attention", "dcp_set_timing_events",
+           "dcp_last_error", "dcp_version")
 
 
 class DcpError(RuntimeError):
@@ -38,6 +40,13 @@ class DcpWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("w_q", "w_k", "w_v", "w_g", "w_b", "b_b", "ln_gamma", "ln_beta")]
 
 
+class DcpSparseShape(ctypes.Structure):
+    _fields_ = [("n_atoms", ctypes.c_int64), ("c_atom", ctypes.c_int32), ("c_ap", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("k", ctypes.c_int32),
+                ("act_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32), ("p_gathered", ctypes.c_int32),
+                ("ln_eps", ctypes.c_float)]
+
+
 _lib: Optional[ctypes.CDLL] = None
 
 
@@ -53,9 +62,12 @@ def lib() -> ctypes.CDLL:
         L.dcp_pair_bias_attention.argtypes = [P(DcpShape), P(DcpWeights), vp, vp, vp, i64, i64, i32, vp, vp, sz, vp]
         L.dcp_bias_project.argtypes = [P(DcpShape), P(DcpWeights), vp, i64, i64, i64, vp, vp]
         L.dcp_block_merge.argtypes = [i32, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp]
+        L.dcp_sparse_workspace_size.argtypes = [P(DcpSparseShape), i64, P(sz)]
+        L.dcp_sparse_pair_bias_attention.argtypes = [P(DcpSparseShape), P(DcpWeights), vp, vp, vp, i64, i64, i32, vp,
+                                                     vp, sz, vp]
         L.dcp_set_timing_events.argtypes = [vp, vp]
         for f in (L.dcp_workspace_size, L.dcp_pair_bias_attention, L.dcp_bias_project, L.dcp_block_merge,
-                  L.dcp_set_timing_events):
+                  L.dcp_sparse_workspace_size, L.dcp_sparse_pair_bias_attention, L.dcp_set_timing_events):
             f.restype = ctypes.c_int
         L.dcp_last_error.restype = ctypes.c_char_p
         L.dcp_last_error.argtypes = []
@@ -126,6 +138,25 @@ def dcp_block_merge(n_parts: int, n_rows: int, n_heads: int, head_dim: int, m_pa
     _check(lib().dcp_block_merge(n_parts, n_rows, n_heads, head_dim, _ptr(m_parts), _ptr(l_parts), _ptr(acc_parts),
                                  _ptr(m_out), _ptr(l_out), _ptr(acc_out), _ptr(gate), _ptr(out), out_dtype,
                                  _stream(stream)))
+
+
+def make_sparse_shape(n_atoms: int, c_atom: int, c_ap: int, n_heads: int, head_dim: int, k: int, act_dtype: int,
+                      out_dtype: int, p_gathered: int = 0, ln_eps: float = 1e-5) -> DcpSparseShape:
+    return DcpSparseShape(n_atoms, c_atom, c_ap, n_heads, head_dim, k, act_dtype, out_dtype, p_gathered, ln_eps)
+
+
+def dcp_sparse_workspace_size(shape: DcpSparseShape, n_q: int) -> int:
+    out = ctypes.c_size_t()
+    _check(lib().dcp_sparse_workspace_size(ctypes.byref(shape), n_q, ctypes.byref(out)))
+    return out.value
+
+
+def dcp_sparse_pair_bias_attention(shape: DcpSparseShape, weights: DcpWeights, a: Ptr, p: Ptr, nbr: Ptr, q_row0: int,
+                                   n_q: int, n_key_blocks: int, out: Ptr, workspace: Ptr, workspace_bytes: int,
+                                   stream=None) -> None:
+    _check(lib().dcp_sparse_pair_bias_attention(ctypes.byref(shape), ctypes.byref(weights), _ptr(a), _ptr(p),
+                                                _ptr(nbr), q_row0, n_q, n_key_blocks, _ptr(out), _ptr(workspace),
+                                                workspace_bytes, _stream(stream)))
 
 
 def dcp_set_timing_events(start_event: Optional[int], stop_event: Optional[int]) -> None:

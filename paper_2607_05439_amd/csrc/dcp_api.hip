@@ -391,3 +391,161 @@ int dcp_block_merge(int32_t n_parts, int64_t n_rows, int32_t n_heads, int32_t he
 }
 
 }  // extern "C"
+
+// ----------------------------------------------------------------------------- sparse atom attention
+namespace {
+
+struct SparseLayout {
+  size_t off_q, off_g, off_k, off_v, total;
+};
+
+int check_sparse(const dcp_sparse_shape* sh, int64_t n_q) {
+  if (!sh) return fail(DCP_ERR_INVALID_ARGUMENT, "shape is NULL");
+  if (sh->n_atoms < 1) return fail(DCP_ERR_INVALID_ARGUMENT, "n_atoms must be >= 1 (got %lld)", (long long)sh->n_atoms);
+  if (sh->c_atom < 1 || sh->c_ap < 1 || sh->n_heads < 1 || sh->head_dim < 1 || sh->k < 1)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "c_atom, c_ap, n_heads, head_dim and k must be >= 1");
+  if ((sh->act_dtype != DCP_F32 && sh->act_dtype != DCP_BF16) || (sh->out_dtype != DCP_F32 && sh->out_dtype != DCP_BF16))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "act_dtype and out_dtype must be DCP_F32 or DCP_BF16");
+  if (sh->p_gathered != 0 && sh->p_gathered != 1) return fail(DCP_ERR_INVALID_ARGUMENT, "p_gathered must be 0 or 1");
+  if (!(sh->ln_eps >= 0.0f) || !isfinite(sh->ln_eps)) return fail(DCP_ERR_INVALID_ARGUMENT, "ln_eps must be finite and >= 0");
+  if (n_q < 0) return fail(DCP_ERR_INVALID_ARGUMENT, "n_q must be >= 0 (got %lld)", (long long)n_q);
+  if (n_q > sh->n_atoms) return fail(DCP_ERR_INVALID_ARGUMENT, "n_q exceeds n_atoms");
+  if (sh->n_heads != dcp::kSparseH || sh->head_dim != dcp::kSparseD || sh->c_ap != dcp::kSparseCap ||
+      sh->k > dcp::kSparseMaxK || sh->n_atoms > dcp::kSparseMaxAtoms || sh->c_atom > dcp::kMaxCs ||
+      (sh->act_dtype == DCP_BF16 && sh->c_atom % 32 != 0))
+    return fail(DCP_ERR_UNSUPPORTED,
+                "unsupported sparse shape (H %d, d %d, c_ap %d, k %d, L %lld, c_atom %d, dtype %d): needs H=4, d=32, "
+                "c_ap=16, k<=256, L<=4000000, c_atom<=4096 (a multiple of 32 for bf16)",
+                sh->n_heads, sh->head_dim, sh->c_ap, sh->k, (long long)sh->n_atoms, sh->c_atom, sh->act_dtype);
+  return DCP_OK;
+}
+
+void sparse_layout(const dcp_sparse_shape* sh, int64_t n_q, SparseLayout* L) {
+  const size_t hd = (size_t)dcp::kSparseH * dcp::kSparseD;
+  const size_t eb = sh->act_dtype == DCP_BF16 ? 2 : 4;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = round_up(off + bytes, 256);
+    return o;
+  };
+  L->off_q = take((size_t)n_q * hd * 4);
+  L->off_g = take((size_t)n_q * hd * 4);
+  L->off_k = take((size_t)sh->n_atoms * hd * eb);
+  L->off_v = take((size_t)sh->n_atoms * hd * eb);
+  L->total = off;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dcp_sparse_workspace_size(const dcp_sparse_shape* shape, int64_t n_q, size_t* bytes) {
+  if (!bytes) return fail(DCP_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  const int rc = check_sparse(shape, n_q);
+  if (rc) return rc;
+  if (n_q == 0) {
+    *bytes = 0;
+    return ok();
+  }
+  SparseLayout L;
+  sparse_layout(shape, n_q, &L);
+  *bytes = L.total;
+  return ok();
+}
+
+int dcp_sparse_pair_bias_attention(const dcp_sparse_shape* shape, const dcp_weights* w, const void* a, const void* p,
+                                   const int32_t* nbr, int64_t q_row0, int64_t n_q, int32_t n_key_blocks, void* out,
+                                   void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_sparse(shape, n_q);
+  if (rc) return rc;
+  if (q_row0 < 0 || q_row0 > shape->n_atoms - n_q)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "need 0 <= q_row0 and q_row0 + n_q <= n_atoms (q_row0 %lld, n_q %lld)",
+                (long long)q_row0, (long long)n_q);
+  if (n_key_blocks < 1 || n_key_blocks > shape->n_atoms)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "n_key_blocks must be in [1, n_atoms] (got %d)", n_key_blocks);
+  if (!w) return fail(DCP_ERR_INVALID_ARGUMENT, "weights is NULL");
+  if (!w->w_q || !w->w_k || !w->w_v || !w->w_g || !w->w_b)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "w_q, w_k, w_v, w_g and w_b are required");
+  if (!a || !p || !nbr || !out) return fail(DCP_ERR_INVALID_ARGUMENT, "a, p, nbr and out are required");
+  if (n_q == 0) return ok();
+  if (!aligned(a, 16) || !aligned(p, 16) || !aligned(out, 16) || !aligned(nbr, 4))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "a, p and out must be 16-byte aligned, nbr 4-byte aligned");
+  const bool bf16 = shape->act_dtype == DCP_BF16;
+  if (bf16 && (!aligned(w->w_q, 16) || !aligned(w->w_k, 16) || !aligned(w->w_v, 16) || !aligned(w->w_g, 16)))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "w_q, w_k, w_v and w_g must be 16-byte aligned");
+  SparseLayout L;
+  sparse_layout(shape, n_q, &L);
+  if (!workspace || !aligned(workspace, 256))
+    return fail(DCP_ERR_WORKSPACE, "workspace must be a 256-byte aligned device pointer");
+  if (workspace_bytes < L.total)
+    return fail(DCP_ERR_WORKSPACE, "workspace too small: %zu bytes given, %zu needed", workspace_bytes, L.total);
+
+  char* ws = static_cast<char*>(workspace);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  if (bf16) {
+    dcp::SparseProjArgs pa{};
+    pa.a = static_cast<const uint16_t*>(a);
+    pa.w_q = w->w_q;
+    pa.w_k = w->w_k;
+    pa.w_v = w->w_v;
+    pa.w_g = w->w_g;
+    pa.n_atoms = shape->n_atoms;
+    pa.q_row0 = q_row0;
+    pa.n_q = n_q;
+    pa.c_atom = shape->c_atom;
+    pa.q = reinterpret_cast<float*>(ws + L.off_q);
+    pa.g = reinterpret_cast<float*>(ws + L.off_g);
+    pa.k = reinterpret_cast<uint16_t*>(ws + L.off_k);
+    pa.v = reinterpret_cast<uint16_t*>(ws + L.off_v);
+    e = dcp::launch_sparse_proj(pa, st);
+  } else {
+    dcp::GenProjArgs pa{};
+    pa.s = a;
+    pa.s_bf16 = 0;
+    pa.w_q = w->w_q;
+    pa.w_k = w->w_k;
+    pa.w_v = w->w_v;
+    pa.w_g = w->w_g;
+    pa.n_tok = shape->n_atoms;
+    pa.q_row0 = q_row0;
+    pa.n_q = n_q;
+    pa.c_s = shape->c_atom;
+    pa.hd = dcp::kSparseH * dcp::kSparseD;
+    pa.q = reinterpret_cast<float*>(ws + L.off_q);
+    pa.k = reinterpret_cast<float*>(ws + L.off_k);
+    pa.v = reinterpret_cast<float*>(ws + L.off_v);
+    pa.g = reinterpret_cast<float*>(ws + L.off_g);
+    e = dcp::launch_gen_proj(pa, st);
+  }
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "projection launch failed: %s", hipGetErrorString(e));
+
+  dcp::SparseAttnArgs aa{};
+  aa.p = p;
+  aa.nbr = nbr;
+  aa.w_b = w->w_b;
+  aa.gamma = w->ln_gamma;
+  aa.q = reinterpret_cast<const float*>(ws + L.off_q);
+  aa.g = reinterpret_cast<const float*>(ws + L.off_g);
+  aa.k = ws + L.off_k;
+  aa.v = ws + L.off_v;
+  aa.n_atoms = shape->n_atoms;
+  aa.n_q = n_q;
+  aa.p_row_elems = (shape->p_gathered ? (int64_t)shape->k : shape->n_atoms) * shape->c_ap;
+  aa.k_slots = shape->k;
+  aa.n_kb = n_key_blocks;
+  aa.p_gathered = shape->p_gathered;
+  aa.out_bf16 = shape->out_dtype == DCP_BF16;
+  aa.eps = shape->ln_eps;
+  aa.out = out;
+  if (g_ev_start && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_start), st)) != hipSuccess)
+    return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
+  if ((e = dcp::launch_sparse_attn(aa, bf16, st)) != hipSuccess)
+    return fail(DCP_ERR_HIP, "sparse attention launch failed: %s", hipGetErrorString(e));
+  if (g_ev_stop && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_stop), st)) != hipSuccess)
+    return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"

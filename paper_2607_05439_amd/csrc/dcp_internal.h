@@ -122,6 +122,38 @@ struct MergeArgs {
   int32_t log2_units;  // 1: m is in base-2 units with integer differences
 };
 
+// Sparse (kNN) atom attention: the paper's atom-attention shape (4 heads of
+// 32, 16 pair channels), up to 256 neighbour slots per query.
+constexpr int kSparseH = 4;
+constexpr int kSparseD = 32;
+constexpr int kSparseCap = 16;
+constexpr int kSparseMaxK = 256;
+// Neighbour indices are packed with their slot number into 32 bits (24 + 8),
+// and an fp32 K or V array of this many atoms stays below 2^31 bytes.
+constexpr int64_t kSparseMaxAtoms = 4000000;
+
+struct SparseProjArgs {
+  const uint16_t* a;  // [L, c_atom] bf16
+  const float *w_q, *w_k, *w_v, *w_g;
+  int64_t n_atoms, q_row0, n_q;
+  int32_t c_atom;
+  float *q, *g;       // [n_q][128] fp32 (g after the sigmoid)
+  uint16_t *k, *v;    // [L][128] bf16
+};
+
+struct SparseAttnArgs {
+  const void* p;          // pair rows of the query stripe (dense [n_q][L][16] or gathered [n_q][k][16])
+  const int32_t* nbr;     // [n_q][k]
+  const float *w_b, *gamma;
+  const float *q, *g;     // [n_q][128] fp32
+  const void *k, *v;      // [L][128] in the activation dtype
+  int64_t n_atoms, n_q;
+  int64_t p_row_elems;    // elements per query row of p
+  int32_t k_slots, n_kb, p_gathered, out_bf16;
+  float eps;
+  void* out;              // [n_q][128]
+};
+
 hipError_t launch_fast_proj(const FastProjArgs& a, hipStream_t st);
 hipError_t launch_fast_attn(const FastAttnArgs& a, hipStream_t st);
 hipError_t launch_fast_bias(const FastBiasArgs& a, hipStream_t st);
@@ -129,5 +161,7 @@ hipError_t launch_gen_proj(const GenProjArgs& a, hipStream_t st);
 hipError_t launch_gen_attn(const GenAttnArgs& a, hipStream_t st);
 hipError_t launch_gen_bias(const GenBiasArgs& a, hipStream_t st);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t st);
+hipError_t launch_sparse_proj(const SparseProjArgs& a, hipStream_t st);
+hipError_t launch_sparse_attn(const SparseAttnArgs& a, bool bf16, hipStream_t st);
 
 }  // namespace dcp

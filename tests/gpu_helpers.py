@@ -132,3 +132,95 @@ def sample_rows(n_tok: int, stripes, n_kb: int, n_random: int, mask: Optional[np
     r = np.random.default_rng(seed)
     rows.update(int(x) for x in r.choice(n_tok, size=min(n_random, n_tok), replace=False))
     return sorted(rows)
+
+
+# ----------------------------------------------------------------------------- sparse atom attention
+def atom_workload(name: str, **kw) -> synth.AtomWorkload:
+    wl = synth.ATOM_WORKLOADS[name]
+    return dataclasses.replace(wl, **kw) if kw else wl
+
+
+class AtomDevice:
+    """Device-resident inputs of one atom workload: A, the query stripe's rows
+    of P (dense), and the neighbour lists."""
+
+    def __init__(self, wl: synth.AtomWorkload, affine: bool = False):
+        import torch
+        self.torch = torch
+        self.wl = wl
+        self.dev = torch.device("cuda:0")
+        self.w_host = synth.atom_weights(wl, affine=affine)
+        self.a_host = synth.a_host(wl)
+        self.a = self._to_dev(self.a_host)
+        self.w = {k: (None if v is None else torch.from_numpy(np.ascontiguousarray(v)).to(self.dev))
+                  for k, v in self.w_host.items()}
+        self.nbr_host = synth.neighbours(wl, wl.q_row0, wl.n_q)
+        self.nbr = torch.from_numpy(self.nbr_host).to(self.dev)
+        dt = torch.bfloat16 if wl.bf16 else torch.float32
+        self.p = torch.empty((wl.n_q, wl.n_atoms, wl.c_ap), dtype=dt, device=self.dev)
+        synth.p_fill_device(wl, self.p.data_ptr(), wl.q_row0, wl.n_q, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+
+    def _to_dev(self, a: np.ndarray):
+        torch = self.torch
+        if a.dtype == np.uint16:
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(self.dev)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(self.dev)
+
+    def shape(self, out_dtype: int = DCP_F32, p_gathered: int = 0, k: Optional[int] = None, eps: float = 1e-5):
+        import paper_2607_05439_amd as dcp
+        wl = self.wl
+        return dcp.make_sparse_shape(wl.n_atoms, wl.c_atom, wl.c_ap, wl.n_heads, wl.head_dim, k or wl.k,
+                                     DCP_BF16 if wl.bf16 else DCP_F32, out_dtype, p_gathered, eps)
+
+    def weights(self, drop_affine: bool = False):
+        import paper_2607_05439_amd as dcp
+        w = self.w
+        if drop_affine:
+            return dcp.make_weights(w["w_q"], w["w_k"], w["w_v"], w["w_g"], w["w_b"], None, w["ln_gamma"], None)
+        return dcp.make_weights(w["w_q"], w["w_k"], w["w_v"], w["w_g"], w["w_b"], w["b_b"], w["ln_gamma"],
+                                w["ln_beta"])
+
+    def attention(self, n_kb: int, out_dtype: int = DCP_F32, row0: int = 0, n_q: Optional[int] = None, nbr=None,
+                  p=None, p_gathered: int = 0, workspace=None):
+        """dcp_sparse_pair_bias_attention for stripe rows [row0, row0 + n_q)
+        (query atoms q_row0 + row0 ...); returns the output as a device tensor."""
+        import paper_2607_05439_amd as dcp
+        torch = self.torch
+        wl = self.wl
+        n_q = wl.n_q - row0 if n_q is None else n_q
+        nb = self.nbr if nbr is None else nbr
+        k = nb.shape[1]
+        shape = self.shape(out_dtype, p_gathered, k)
+        out = torch.empty((max(n_q, 1), wl.n_heads * wl.head_dim),
+                          dtype=torch.float32 if out_dtype == DCP_F32 else torch.bfloat16, device=self.dev)
+        nbytes = dcp.dcp_sparse_workspace_size(shape, n_q)
+        ws = workspace if workspace is not None else torch.empty(max(nbytes, 256), dtype=torch.uint8,
+                                                                 device=self.dev)
+        pt = self.p if p is None else p
+        p_ptr = pt.data_ptr() + row0 * pt.shape[1] * pt.shape[2] * pt.element_size()
+        nbr_ptr = nb.data_ptr() + row0 * k * 4
+        dcp.dcp_sparse_pair_bias_attention(shape, self.weights(), self.a, p_ptr, nbr_ptr, wl.q_row0 + row0, n_q, n_kb,
+                                           out, ws, ws.numel(), None)
+        return out
+
+    def gathered_p(self, nbr: Optional[np.ndarray] = None):
+        """P_sparse [n_q, k, c_ap] on the device, from the host generator."""
+        nb = self.nbr_host if nbr is None else nbr
+        rows = self.wl.q_row0 + np.arange(self.wl.n_q)
+        return self._to_dev(synth.p_gathered_host(self.wl, rows, nb))
+
+    def oracle_rows(self, local_rows: Sequence[int], n_blocks: int = 1, nbr: Optional[np.ndarray] = None,
+                    drop_affine: bool = False) -> np.ndarray:
+        """fp64 oracle for stripe rows ``local_rows`` on the generator's host copy
+        of the same inputs."""
+        local_rows = np.asarray(local_rows, dtype=np.int64)
+        nb = (self.nbr_host if nbr is None else nbr)[local_rows]
+        atoms = self.wl.q_row0 + local_rows
+        p = synth.p_gathered_host(self.wl, atoms, nb)
+        w = dict(self.w_host)
+        if drop_affine:
+            w["b_b"] = None
+            w["ln_beta"] = None
+        return oracle.sparse_attention(self.a_host, p, nb, atoms, w, self.wl.n_heads, self.wl.head_dim,
+                                       n_blocks=n_blocks)

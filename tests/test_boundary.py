@@ -139,3 +139,70 @@ def test_binding_raises():
     with pytest.raises(dcp.DcpError) as e:
         dcp.dcp_workspace_size(shape(n_heads=0), 10, 1)
     assert e.value.code == dcp.DCP_ERR_INVALID_ARGUMENT
+
+
+# ----------------------------------------------------------------------------- sparse atom attention
+def sparse_shape(**kw):
+    base = dict(n_atoms=96000, c_atom=128, c_ap=16, n_heads=4, head_dim=32, k=128, act_dtype=dcp.DCP_BF16,
+                out_dtype=dcp.DCP_F32, p_gathered=0, ln_eps=1e-5)
+    base.update(kw)
+    return dcp.make_sparse_shape(**base)
+
+
+def sparse(sh, w=None, a=FAKE, p=FAKE, nbr=FAKE, q_row0=0, n_q=24000, n_kb=4, out=FAKE, ws=FAKE, ws_bytes=1 << 40):
+    return dcp.lib().dcp_sparse_pair_bias_attention(ctypes.byref(sh), ctypes.byref(w or weights()), a, p, nbr, q_row0,
+                                                    n_q, n_kb, out, ws, ws_bytes, None)
+
+
+def test_sparse_workspace_sizes():
+    # q, g fp32 for 24000 queries + K, V bf16 for 96000 atoms
+    got = dcp.dcp_sparse_workspace_size(sparse_shape(), 24000)
+    assert got >= 2 * 24000 * 128 * 4 + 2 * 96000 * 128 * 2
+    assert got < 1.01 * (2 * 24000 * 128 * 4 + 2 * 96000 * 128 * 2) + 4096
+    f32 = dcp.dcp_sparse_workspace_size(sparse_shape(act_dtype=dcp.DCP_F32), 24000)
+    assert f32 > got
+    assert dcp.dcp_sparse_workspace_size(sparse_shape(), 0) == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n_atoms=0), dcp.DCP_ERR_INVALID_ARGUMENT),
+    (dict(k=0), dcp.DCP_ERR_INVALID_ARGUMENT),
+    (dict(act_dtype=3), dcp.DCP_ERR_INVALID_ARGUMENT),
+    (dict(p_gathered=2), dcp.DCP_ERR_INVALID_ARGUMENT),
+    (dict(ln_eps=float("inf")), dcp.DCP_ERR_INVALID_ARGUMENT),
+    (dict(n_heads=8), dcp.DCP_ERR_UNSUPPORTED),
+    (dict(head_dim=16), dcp.DCP_ERR_UNSUPPORTED),
+    (dict(c_ap=32), dcp.DCP_ERR_UNSUPPORTED),
+    (dict(k=257), dcp.DCP_ERR_UNSUPPORTED),
+    (dict(n_atoms=5_000_000), dcp.DCP_ERR_UNSUPPORTED),
+    (dict(c_atom=100), dcp.DCP_ERR_UNSUPPORTED),  # bf16 needs a multiple of 32
+])
+def test_sparse_bad_shapes(kw, code):
+    sh = sparse_shape(**kw)
+    assert sparse(sh) == code
+    assert len(dcp.dcp_last_error()) > 0
+    out = ctypes.c_size_t()
+    assert dcp.lib().dcp_sparse_workspace_size(ctypes.byref(sh), 100, ctypes.byref(out)) == code
+
+
+def test_sparse_bad_arguments():
+    E, W = dcp.DCP_ERR_INVALID_ARGUMENT, dcp.DCP_ERR_WORKSPACE
+    sh = sparse_shape()
+    assert sparse(sh, q_row0=-1) == E
+    assert sparse(sh, q_row0=80000) == E      # 80000 + 24000 > 96000
+    assert sparse(sh, n_q=-1) == E
+    assert sparse(sh, n_kb=0) == E
+    assert sparse(sh, n_kb=96001) == E
+    assert sparse(sh, a=None) == E
+    assert sparse(sh, p=None) == E
+    assert sparse(sh, nbr=None) == E
+    assert sparse(sh, out=None) == E
+    assert sparse(sh, a=FAKE + 8) == E        # misaligned
+    assert sparse(sh, nbr=FAKE + 2) == E
+    assert sparse(sh, w=dcp.make_weights(FAKE, FAKE, FAKE, FAKE, None)) == E
+    assert sparse(sh, ws=None) == W
+    assert sparse(sh, ws=FAKE + 16) == W
+    assert sparse(sh, ws_bytes=1000) == W
+    # an f32 call accepts any c_atom and unaligned weights
+    assert sparse(sparse_shape(act_dtype=dcp.DCP_F32, c_atom=100), ws_bytes=1000) == W
+    assert sparse(sh, n_q=0, ws=None) == dcp.DCP_OK  # no-op
