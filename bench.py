@@ -7,6 +7,11 @@ workload, with all inputs already resident in HBM. Default workload: the
 whole-assembly case, N = 24000 tokens (60 x 400), bf16 z[N, N, 128] = 147 GB,
 16 heads of width 24, 6 key blocks, last 480 tokens masked.
 
+With an atom workload (--workload atoms96k_bf16) it measures the sparse kNN
+pair-biased atom attention instead: one step = one layer call (atom
+projections, then the sparse attention over all key blocks) for the query
+stripe.
+
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
 import argparse
@@ -23,6 +28,8 @@ sys.path.insert(0, ROOT)
 METRIC = "ms/layer + achieved HBM GB/s (% peak) for pair-biased attention at N tokens"
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, published
 KERNEL_SOURCES = ("paper_2607_05439_amd/csrc/fast.hip", "paper_2607_05439_amd/csrc/cdna4.h")
+SPARSE_SOURCES = ("paper_2607_05439_amd/csrc/sparse.hip", "paper_2607_05439_amd/csrc/cdna4.h")
+SPARSE_METRIC = "ms/layer + gathered GB/s for sparse kNN pair-biased atom attention"
 
 
 def progress(msg):
@@ -57,15 +64,15 @@ class Hip:
         self.lib.hipEventDestroy(ev)
 
 
-def kernel_source_sha():
+def kernel_source_sha(sources=KERNEL_SOURCES):
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in sources:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def stored_traffic(workload):
+def stored_traffic(workload, sources=KERNEL_SOURCES):
     """HBM bytes per launch from committed rocprofv3 counters, if they were
     taken on the current kernel source; else None."""
     path = os.path.join(ROOT, "profiles", f"traffic_attn_{workload}.json")
@@ -73,7 +80,7 @@ def stored_traffic(workload):
         return None
     with open(path) as f:
         t = json.load(f)
-    if t.get("kernel_source_sha") != kernel_source_sha():
+    if t.get("kernel_source_sha") != kernel_source_sha(sources):
         return None
     return t.get("hbm_bytes_per_launch")
 
@@ -111,6 +118,171 @@ def cpu_baseline(wl, s_host, w_host, mask, seconds):
     return {"t_layer_s": t_layer, "rows": len(rows), "t_run_s": t_run, "threads": threads, "t_fixed_s": t_fixed}
 
 
+def sparse_cpu_baseline(wl, a_host, w_host, nbr_host, seconds):
+    """The fp64 oracle on a bounded sample of query atoms, extrapolated to the
+    stripe (fixed K/V projection of all atoms + n_q x per-row)."""
+    import numpy as np
+    import oracle
+    import synth
+    threads = ctypes.CDLL("libgomp.so.1").omp_get_max_threads()
+    a64 = oracle.decode(a_host) if a_host.dtype == np.uint16 else a_host.astype(np.float64)
+    t0 = time.perf_counter()
+    oracle.linear(a64, w_host["w_k"])
+    oracle.linear(a64, w_host["w_v"])
+    t_fixed = time.perf_counter() - t0
+    n = min(wl.n_q, 64 * threads)
+    rows = np.arange(n) * (wl.n_q // n)
+    p = synth.p_gathered_host(wl, wl.q_row0 + rows, nbr_host[rows])
+    t0 = time.perf_counter()
+    oracle.sparse_attention(a_host, p, nbr_host[rows], wl.q_row0 + rows, w_host, wl.n_heads, wl.head_dim,
+                            n_blocks=wl.n_key_blocks)
+    t_small = time.perf_counter() - t0
+    per_row = max((t_small - t_fixed) / n, 1e-9)
+    n_rows = int(min(wl.n_q, max(n, (seconds - t_small) / per_row)))
+    rng = np.random.default_rng(1)
+    rows = np.sort(rng.choice(wl.n_q, size=n_rows, replace=False))
+    p = synth.p_gathered_host(wl, wl.q_row0 + rows, nbr_host[rows])
+    t0 = time.perf_counter()
+    oracle.sparse_attention(a_host, p, nbr_host[rows], wl.q_row0 + rows, w_host, wl.n_heads, wl.head_dim,
+                            n_blocks=wl.n_key_blocks)
+    t_run = time.perf_counter() - t0
+    per_row = max((t_run - t_fixed) / n_rows, 1e-12)
+    return {"t_layer_s": t_fixed + per_row * wl.n_q, "rows": n_rows, "t_run_s": t_run, "threads": threads,
+            "t_fixed_s": t_fixed}
+
+
+def sparse_main(args, wl):
+    import numpy as np
+    import torch
+    import paper_2607_05439_amd as dcp
+    import synth
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    L, eb, hd = wl.n_atoms, wl.elem_bytes, wl.n_heads * wl.head_dim
+    progress(f"workload {wl.name}: L={L} atoms, query rows {wl.q_row0}..{wl.q_row0 + wl.n_q - 1}, k={wl.k}, "
+             f"n_kb={wl.n_key_blocks}, P rows {wl.n_q * L * wl.c_ap * eb / 1e9:.1f} GB")
+
+    def to_dev(x):
+        if x.dtype == np.uint16:
+            return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+
+    a_host = synth.a_host(wl)
+    w_host = synth.atom_weights(wl)
+    nbr_host = synth.neighbours(wl, wl.q_row0, wl.n_q)
+    a = to_dev(a_host)
+    w = {k: (None if v is None else torch.from_numpy(v).to(dev)) for k, v in w_host.items()}
+    nbr = torch.from_numpy(nbr_host).to(dev)
+    p = torch.empty((wl.n_q, L, wl.c_ap), dtype=torch.bfloat16 if wl.bf16 else torch.float32, device=dev)
+    synth.p_fill_device(wl, p.data_ptr(), wl.q_row0, wl.n_q, sp)
+    out_dtype = dcp.DCP_BF16 if wl.bf16 else dcp.DCP_F32
+    shape = dcp.make_sparse_shape(L, wl.c_atom, wl.c_ap, wl.n_heads, wl.head_dim, wl.k,
+                                  dcp.DCP_BF16 if wl.bf16 else dcp.DCP_F32, out_dtype, 0, 1e-5)
+    weights = dcp.make_weights(w["w_q"], w["w_k"], w["w_v"], w["w_g"], w["w_b"])
+    ws_bytes = dcp.dcp_sparse_workspace_size(shape, wl.n_q)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    out = torch.empty((wl.n_q, hd), dtype=torch.bfloat16 if wl.bf16 else torch.float32, device=dev)
+    valid = (nbr_host >= 0) & (nbr_host < L)
+    n_slots = int(valid.sum())
+    n_ref = int(np.unique(nbr_host[valid]).size)
+    # bytes the kernel moves per valid slot: the pair slice, the K row and the V row
+    gathered = n_slots * (wl.c_ap * eb + 2 * hd * eb)
+    # bytes that must come from HBM at least once: pair slices, neighbour lists,
+    # K/V rows of the referenced atoms, q and g, the output
+    compulsory = (n_slots * wl.c_ap * eb + nbr_host.size * 4 + n_ref * 2 * hd * eb + wl.n_q * hd * 4 * 2
+                  + wl.n_q * hd * (2 if wl.bf16 else 4))
+    torch.cuda.synchronize()
+    hip = Hip()
+
+    def step(evs=None):
+        if evs is not None:
+            dcp.dcp_set_timing_events(*evs)
+        dcp.dcp_sparse_pair_bias_attention(shape, weights, a, p, nbr, wl.q_row0, wl.n_q, wl.n_key_blocks, out, ws,
+                                           ws_bytes, sp)
+        if evs is not None:
+            dcp.dcp_set_timing_events(None, None)
+
+    # ceiling of the K/V gather pattern (same neighbour lists, no arithmetic)
+    kbuf = torch.zeros((L, hd), dtype=torch.bfloat16 if wl.bf16 else torch.float32, device=dev)
+    vbuf = torch.zeros_like(kbuf)
+    sink = torch.zeros(4, dtype=torch.int32, device=dev)
+    e0, e1 = hip.event(), hip.event()
+    synth.device_gather_pattern(kbuf.data_ptr(), vbuf.data_ptr(), L, nbr.data_ptr(), wl.n_q, wl.k, sink.data_ptr(), sp)
+    hip.record(e0, sp)
+    synth.device_gather_pattern(kbuf.data_ptr(), vbuf.data_ptr(), L, nbr.data_ptr(), wl.n_q, wl.k, sink.data_ptr(), sp)
+    hip.record(e1, sp)
+    pattern_ms = hip.elapsed_ms(e0, e1)
+    pattern_gbps = n_slots * 2 * hd * eb / (pattern_ms * 1e-3) / 1e9
+    del kbuf, vbuf
+    progress(f"K/V gather pattern, no arithmetic: {pattern_ms * 1e3:.1f} us, {pattern_gbps:.0f} GB/s")
+
+    progress(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    kernel_evs = [(hip.event(), hip.event()) for _ in range(args.steps)]
+    progress(f"timing {args.steps} steps")
+    t_start, t_stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for k in range(args.steps):
+        step(kernel_evs[k])
+    t_stop.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t_start.elapsed_time(t_stop) / args.steps
+    k_ms = [hip.elapsed_ms(x, y) for (x, y) in kernel_evs]
+    avg_kernel_ms = sum(k_ms) / len(k_ms)
+    achieved = compulsory / (avg_kernel_ms * 1e-3) / 1e9
+    gathered_gbps = gathered / (avg_kernel_ms * 1e-3) / 1e9
+    kv_gbps = n_slots * 2 * hd * eb / (avg_kernel_ms * 1e-3) / 1e9
+    value = gathered / (ms_per_step * 1e-3) / 1e9
+    progress(f"{ms_per_step * 1e3:.1f} us/layer, sparse attention kernel {avg_kernel_ms * 1e3:.1f} us/launch: "
+             f"{gathered_gbps:.0f} GB/s gathered, K/V {kv_gbps:.0f} GB/s ({kv_gbps / pattern_gbps:.1%} of the "
+             f"pattern ceiling), compulsory HBM {achieved:.0f} GB/s")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        progress(f"cpu baseline: oracle on sampled query atoms (~{args.cpu_seconds:.0f} s)")
+        cb = sparse_cpu_baseline(wl, a_host, w_host, nbr_host, args.cpu_seconds)
+        cpu = {"value": round(gathered / cb["t_layer_s"] / 1e9, 6), "unit": "GB/s", "cores": cb["threads"],
+               "kind": "oracle",
+               "sample": f"{cb['rows']} of {wl.n_q} query atoms in {cb['t_run_s']:.1f} s (fp64, includes the k/v "
+                         f"projection of all {L} atoms, {cb['t_fixed_s']:.1f} s); extrapolated layer time "
+                         f"{cb['t_layer_s']:.2f} s",
+               "ms_per_layer_extrapolated": round(cb["t_layer_s"] * 1e3, 1)}
+
+    line = {
+        "metric": SPARSE_METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.bf16 else "f32",
+        "data": "synthetic (seeded; kNN-budget neighbour lists stand in for RFD3 atom neighbourhoods)",
+        "config": {"workload": wl.name, "n_atoms": L, "q_row0": wl.q_row0, "n_q": wl.n_q, "k": wl.k,
+                   "valid_slots": n_slots, "c_atom": wl.c_atom, "c_ap": wl.c_ap, "n_heads": wl.n_heads,
+                   "head_dim": wl.head_dim, "n_key_blocks": wl.n_key_blocks,
+                   "gathered_bytes_per_step": gathered, "compulsory_bytes_per_step": compulsory},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBPS, 4),
+                     "traffic": stored_traffic(wl.name, SPARSE_SOURCES),
+                     "kernel": "sparse_attn_kernel", "kernel_ms": round(avg_kernel_ms, 5),
+                     "algorithmic_bytes_per_launch": compulsory},
+        "gather": {"gathered_GBps": round(gathered_gbps, 1), "kv_GBps": round(kv_gbps, 1),
+                   "kv_pattern_ceiling_GBps": round(pattern_gbps, 1),
+                   "frac_of_pattern": round(kv_gbps / pattern_gbps, 4)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -133,6 +305,8 @@ def main():
     import paper_2607_05439_amd as dcp
     import synth
 
+    if args.workload in synth.ATOM_WORKLOADS:
+        return sparse_main(args, synth.ATOM_WORKLOADS[args.workload])
     wl = synth.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()

@@ -42,13 +42,20 @@ constexpr int kH = kSparseH, kD = kSparseD, kHD = kSparseH * kSparseD, kCap = kS
 constexpr int kWaves = 4;  // waves (query atoms) per workgroup
 constexpr float kLog2e = 1.44269504088896340736f;
 constexpr uint32_t kNt = 2;  // cache-policy bit of a buffer load: non-temporal
+// bf16 path: logits in base-2 units are offset by this constant (through the
+// bias), so every logit of moderate size lies in [128, 256), on one fp32 grid
+// (2^-16). With integer running maxima the subtraction logit - max is then
+// exact, and the bf16-rounded softmax weights do not depend on how the slots
+// are split into key blocks (rescaling is by exact powers of two).
+constexpr float kShift = 192.0f;
 
 // ----------------------------------------------------------------------------- projections
 constexpr int kProjTiles = 4;  // 16-atom tiles per wave (share the weight operands)
 
-// grid (groups of 4 tiles of 16 atoms, head h, projection {q, k, v, g}); one
-// wave each. Weight rows of head h are the A operand (rows e = 16 et + n), the
-// atoms the B operand: the accumulator holds outputs 16 et + 4g + i of atom n.
+// Any c_atom (a multiple of 32). grid (groups of 4 tiles of 16 atoms, head h,
+// projection {q, k, v, g}); one wave each. Weight rows of head h are the A
+// operand (rows e = 16 et + n), the atoms the B operand: the accumulator holds
+// outputs 16 et + 4g + i of atom n.
 __global__ void __launch_bounds__(64) atom_proj_kernel(SparseProjArgs a) {
   const int lane = threadIdx.x, n = lane & 15, g = lane >> 4;
   const int h = blockIdx.y, which = blockIdx.z;  // 0 q, 1 k, 2 v, 3 g
@@ -115,6 +122,105 @@ __global__ void __launch_bounds__(64) atom_proj_kernel(SparseProjArgs a) {
           v.w = 1.0f / (1.0f + __expf(-acc[u][et][3]));
         }
         *reinterpret_cast<float4*>((which == 0 ? a.q : a.g) + row * kHD + o) = v;
+      }
+    }
+  }
+}
+
+// c_atom = 128 (the paper's atom width). blockIdx.y picks the projection
+// (0 q, 1 k, 2 v, 3 g; q and g over the query rows, k and v over all atoms).
+// Its weight matrix is converted once per workgroup into matrix-core A
+// operands in LDS (bf16 hi + lo, 64 KB, so two workgroups share a CU); each
+// wave then takes 4 tiles of 16 atoms at a time, holds their B operands in
+// registers, and runs all 128 outputs against them.
+constexpr int kP128Ks = 4;  // 32-channel k-steps
+struct ProjOperands {
+  u32x4 w[8][kP128Ks][2][64];  // [output tile][k-step][hi, lo][lane]
+};
+
+__global__ void __launch_bounds__(256, 2) atom_proj128_kernel(SparseProjArgs a) {
+  __shared__ ProjOperands ops;
+  const int which = blockIdx.y;
+  const bool query = which == 0 || which == 3;
+  const int64_t rows = query ? a.n_q : a.n_atoms;
+  const int64_t base = query ? a.q_row0 : 0;
+  const int64_t n_groups = (rows + 63) / 64;
+  if ((int64_t)blockIdx.x * 4 >= n_groups) return;  // whole workgroup, before any barrier
+  const float* wsrc = which == 0 ? a.w_q : which == 1 ? a.w_k : which == 2 ? a.w_v : a.w_g;
+  constexpr int kEntries = 8 * kP128Ks * 64;  // 8 per thread, 4 at a time with their loads in flight
+  for (int i0 = threadIdx.x; i0 < kEntries; i0 += 4 * 256) {
+    float4 x[4][2];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int idx = i0 + 256 * v;
+      const int ln = idx & 63, ks = (idx >> 6) % kP128Ks, ot = (idx >> 6) / kP128Ks;
+      const float4* wp = reinterpret_cast<const float4*>(wsrc + (16 * ot + (ln & 15)) * kHD + 32 * ks + 8 * (ln >> 4));
+      x[v][0] = wp[0];
+      x[v][1] = wp[1];
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int idx = i0 + 256 * v;
+      const int ln = idx & 63, ks = (idx >> 6) % kP128Ks, ot = (idx >> 6) / kP128Ks;
+      const float xs[8] = {x[v][0].x, x[v][0].y, x[v][0].z, x[v][0].w, x[v][1].x, x[v][1].y, x[v][1].z, x[v][1].w};
+      bf16x8 hi, lo;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        hi[i] = (__bf16)xs[i];
+        lo[i] = (__bf16)(xs[i] - (float)hi[i]);
+      }
+      ops.w[ot][ks][0][ln] = __builtin_bit_cast(u32x4, hi);
+      ops.w[ot][ks][1][ln] = __builtin_bit_cast(u32x4, lo);
+    }
+  }
+  __syncthreads();
+
+  const int lane = threadIdx.x & 63, n = lane & 15, g = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  for (int64_t grp = (int64_t)blockIdx.x * 4 + wave; grp < n_groups; grp += (int64_t)gridDim.x * 4) {
+    u32x4 av[4][kP128Ks];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t row = min(grp * 64 + 16 * u + n, rows - 1);  // rows past the end are not stored
+      const u32x4* ap = reinterpret_cast<const u32x4*>(a.a + (base + row) * kHD + 8 * g);
+#pragma unroll
+      for (int ks = 0; ks < kP128Ks; ++ks) av[u][ks] = ap[4 * ks];
+    }
+#pragma unroll 2
+    for (int ot = 0; ot < 8; ++ot) {
+      f32x4 acc[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < kP128Ks; ++ks) {
+        const bf16x8 hi = as_bf16x8(ops.w[ot][ks][0][lane]);
+        const bf16x8 lo = as_bf16x8(ops.w[ot][ks][1][lane]);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          acc[u] = mfma32(hi, as_bf16x8(av[u][ks]), acc[u]);
+          acc[u] = mfma32(lo, as_bf16x8(av[u][ks]), acc[u]);
+        }
+      }
+      const int o = 16 * ot + 4 * g;  // outputs o .. o+3 of the atom row
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int64_t row = grp * 64 + 16 * u + n;
+        if (row >= rows) continue;
+        if (which == 1 || which == 2) {
+          bf16x4 v;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] = (__bf16)acc[u][i];
+          *reinterpret_cast<u32x2*>((which == 1 ? a.k : a.v) + row * kHD + o) = __builtin_bit_cast(u32x2, v);
+        } else if (which == 0) {
+          *reinterpret_cast<float4*>(a.q + row * kHD + o) = make_float4(acc[u][0], acc[u][1], acc[u][2], acc[u][3]);
+        } else {
+          float4 v;
+          v.x = 1.0f / (1.0f + __expf(-acc[u][0]));
+          v.y = 1.0f / (1.0f + __expf(-acc[u][1]));
+          v.z = 1.0f / (1.0f + __expf(-acc[u][2]));
+          v.w = 1.0f / (1.0f + __expf(-acc[u][3]));
+          *reinterpret_cast<float4*>(a.g + row * kHD + o) = v;
+        }
       }
     }
   }
@@ -191,6 +297,42 @@ __device__ __forceinline__ int block_of(uint32_t j, uint32_t q, uint32_t rem) {
 }
 
 // ----------------------------------------------------------------------------- attention
+// Bias operands of the 16x16x16 matrix-core form (bf16 path): row h < 4 holds
+// W''[h, c] = log2(e) W_b[h, c] gamma_c, centred over c (then sum_c W''[h,c] p_c
+// = sum_c W''[h,c] (p_c - mean p)), split into bf16 hi + lo; row 4 holds ones
+// in hi (the row sum of the pair vector); other rows are zero. Lane L: row
+// L % 16, channels 4g .. 4g+3 with g = L / 16.
+__device__ __forceinline__ void bias_operands(const float* __restrict__ w_b, const float* __restrict__ gamma, int lane,
+                                              bf16x4& hi, bf16x4& lo) {
+  const int n = lane & 15, g = lane >> 4;
+  float w[4], rs = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int ch = 4 * g + i;
+    w[i] = n < kH ? w_b[n * kCap + ch] * (gamma ? gamma[ch] : 1.0f) * kLog2e : 0.0f;
+    rs += w[i];
+  }
+  const float mean = sum4(rs) * (1.0f / kCap);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float cw = w[i] - mean;
+    const __bf16 x = (__bf16)cw;
+    hi[i] = n < kH ? x : (n == kH ? (__bf16)1.0f : (__bf16)0.0f);
+    lo[i] = n < kH ? (__bf16)(cw - (float)x) : (__bf16)0.0f;
+  }
+}
+
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+  bf16x2 v;
+  v[0] = (__bf16)a;
+  v[1] = (__bf16)b;
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(a), as_bf16x2(b), c, false);
+}
+
 template <bool kBf16, int KMAX>
 __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs a) {
   constexpr int EB = kBf16 ? 2 : 4;  // bytes per element of P, K and V
@@ -199,10 +341,14 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
   constexpr int NPI = 64 / LPN;      // rows per load instruction (4 | 2)
   constexpr int LPH = kD / EPL;      // lanes per head (4 | 8)
   constexpr int KS = KMAX / 64;      // slots per lane in slot order
-  constexpr int CPL = kCap / 4;      // pair channels per lane in the bias phase
-  constexpr int kUnroll = 8;
-  __shared__ uint32_t s_list[kWaves][KMAX];  // (atom << 8) | slot, compacted
-  __shared__ float s_lg[kWaves][KMAX][kH];   // bias, then logits (base-2 units)
+  constexpr int kUnroll = 4;         // K (and V) loads per lane per batch
+  constexpr int kBatch = NPI * kUnroll;  // slots per batch (32 | 16)
+  constexpr int kPad = 32;           // list length granularity
+  constexpr int kPasses = KMAX / 16; // bias passes of 16 slots
+  static_assert(kPad % 16 == 0 && kPad % kBatch == 0 && KMAX % kPad == 0, "list padding");
+  __shared__ uint32_t s_kv[kWaves][KMAX];  // byte offset of the K/V row, or out of range (padding)
+  __shared__ uint32_t s_p[kWaves][KMAX];   // byte offset of the pair vector in this query's P row
+  __shared__ __attribute__((aligned(16))) float s_b[kWaves][KMAX][kH];  // bias (base-2 units), -inf for padding
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -214,11 +360,13 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
   const int64_t r = lwg * kWaves + wave;
   if (r >= a.n_q) return;
 
-  const int c = lane % LPN;  // 16-byte chunk of a K/V row held by this lane
-  const int hl = c / LPH;    // its head
+  const int c = lane % LPN;    // 16-byte chunk of a K/V row held by this lane
+  const int grp = lane / LPN;  // which of the NPI rows of a load
+  const int hl = c / LPH;      // head of the chunk
+  // q slice, scaled into base-2 logit units (log2(e) / sqrt(32))
   float qv[EPL];
   {
-    const float qs = kLog2e * 0.17677669529663688110f;  // log2(e) / sqrt(32)
+    const float qs = kLog2e * 0.17677669529663688110f;
     const float4* qp = reinterpret_cast<const float4*>(a.q + r * kHD + c * EPL);
 #pragma unroll
     for (int e4 = 0; e4 < EPL / 4; ++e4) {
@@ -229,28 +377,41 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
       qv[4 * e4 + 3] = t.w * qs;
     }
   }
-  // bias weights for this lane's 4 pair channels: log2(e) W_b[h, ch] gamma[ch]
-  const int cq = lane & 3;
-  float wb[kH][CPL];
+  uint32_t qhi[4], qlo[4];  // bf16 path: q as a bf16 hi + lo pair, packed by element pairs
+  if constexpr (kBf16) {
 #pragma unroll
-  for (int h = 0; h < kH; ++h)
-#pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-      const int ch = CPL * cq + i;
-      wb[h][i] = a.w_b[h * kCap + ch] * (a.gamma ? a.gamma[ch] : 1.0f) * kLog2e;
+    for (int w = 0; w < 4; ++w) {
+      qhi[w] = pack_bf16(qv[2 * w], qv[2 * w + 1]);
+      const bf16x2 h = as_bf16x2(qhi[w]);
+      qlo[w] = pack_bf16(qv[2 * w] - (float)h[0], qv[2 * w + 1] - (float)h[1]);
     }
+  }
+  bf16x4 whi, wlo;       // bf16 path: bias operands
+  float wb[kH][4] = {};  // fp32 path: log2(e) W_b[h, ch] gamma[ch] for this lane's 4 channels
+  if constexpr (kBf16) {
+    bias_operands(a.w_b, a.gamma, lane, whi, wlo);
+  } else {
+#pragma unroll
+    for (int h = 0; h < kH; ++h)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int ch = 4 * (lane & 3) + i;
+        wb[h][i] = a.w_b[h * kCap + ch] * (a.gamma ? a.gamma[ch] : 1.0f) * kLog2e;
+      }
+  }
 
   // neighbour slots in slot order: lane holds slots 64u + lane
   const uint32_t bq = (uint32_t)(a.n_atoms / a.n_kb), brem = (uint32_t)(a.n_atoms % a.n_kb);
-  int32_t jn[KS];
+  uint32_t kvo[KS], po[KS];
   int blk[KS];
 #pragma unroll
   for (int u = 0; u < KS; ++u) {
     const int t = 64 * u + lane;
     const int32_t j = t < a.k_slots ? a.nbr[r * a.k_slots + t] : -1;
     const bool valid = j >= 0 && (int64_t)j < a.n_atoms;
-    jn[u] = j;
     blk[u] = valid ? block_of((uint32_t)j, bq, brem) : INT32_MAX;
+    kvo[u] = (uint32_t)j * (uint32_t)(kHD * EB);
+    po[u] = (a.p_gathered ? (uint32_t)t : (uint32_t)j) * (uint32_t)(kCap * EB);
   }
 
   const __amdgpu_buffer_rsrc_t pres = __builtin_amdgcn_make_buffer_rsrc(
@@ -261,20 +422,91 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
       __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.k), 0, kv_bytes, kRawBufferFlags);
   const __amdgpu_buffer_rsrc_t vres =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(a.v), 0, kv_bytes, kRawBufferFlags);
-  uint32_t* list = s_list[wave];
-  float(*lgs)[kH] = s_lg[wave];
+  uint32_t* lkv = s_kv[wave];
+  uint32_t* lp = s_p[wave];
+  float(*lb)[kH] = s_b[wave];
 
-  float m_run = -INFINITY, l_run = 0.0f;  // head hl; l_run over this lane's rows only
+  // running softmax state of head hl: integer maximum m (base-2 units), and
+  // this lane's share of l and acc (summed over the NPI row groups at the end)
+  float m_run = -INFINITY, l_run = 0.0f;
   float acc[EPL];
 #pragma unroll
   for (int e = 0; e < EPL; ++e) acc[e] = 0.0f;
+
+  // one register buffer of K/V rows per batch; the next batch's loads are
+  // issued as soon as this batch's registers are free (more buffers cost
+  // occupancy, which hides the gather latency better)
+  u32x4 kw[1][kUnroll], vw[1][kUnroll];
+  auto issue_batch = [&](int buf, int b0) {
+    int off[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) off[u] = (int)(lkv[b0 + NPI * u + grp] + 16u * c);
+    // K first: the logits can start while V is still arriving
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) kw[buf][u] = __builtin_amdgcn_raw_buffer_load_b128(kres, off[u], 0, 0);
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) vw[buf][u] = __builtin_amdgcn_raw_buffer_load_b128(vres, off[u], 0, 0);
+  };
+  // one batch: logits, online softmax (integer maxima, exact power-of-two
+  // rescaling), weighted V
+  auto compute_batch = [&](int buf, int b0) {
+    float lg[kUnroll];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      float dot = 0.0f;
+      if constexpr (kBf16) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          dot = dot2(qhi[w], kw[buf][u][w], dot);
+          dot = dot2(qlo[w], kw[buf][u][w], dot);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) dot = fmaf(qv[e], __uint_as_float(kw[buf][u][e]), dot);
+      }
+      lg[u] = group_sum<LPH>(dot) + lb[b0 + NPI * u + grp][hl];
+      mx = fmaxf(mx, lg[u]);
+    }
+    mx = across_max<NPI>(mx);
+    const float m_new = fmaxf(m_run, ceilf(mx));
+    if (m_new != m_run) {  // lane-varying (per head); only a rescale of the state
+      const float sr = m_run == -INFINITY ? 0.0f : ldexpf(1.0f, (int)(m_run - m_new));
+      l_run *= sr;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[e] *= sr;
+      m_run = m_new;
+    }
+    const float m_use = m_run == -INFINITY ? 0.0f : m_run;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const float p = __builtin_amdgcn_exp2f(lg[u] - m_use);
+      if constexpr (kBf16) {
+        // the weight as bf16 pairs (p, 0) and (0, p): one dot2 per element (no
+        // constant operands in the dot2: an inline constant is not read as a
+        // packed bf16 pair)
+        const uint32_t plo = pack_bf16(p, 0.0f), phi = plo << 16;
+        l_run += __uint_as_float(phi);  // bf16(p) as fp32: the weight the numerator uses
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          acc[2 * w] = dot2(plo, vw[buf][u][w], acc[2 * w]);
+          acc[2 * w + 1] = dot2(phi, vw[buf][u][w], acc[2 * w + 1]);
+        }
+      } else {
+        l_run += p;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[e] = fmaf(p, __uint_as_float(vw[buf][u][e]), acc[e]);
+      }
+    }
+  };
 
   int b = INT32_MAX;
 #pragma unroll
   for (int u = 0; u < KS; ++u) b = min(b, blk[u]);
   b = __builtin_amdgcn_readfirstlane(wave_min(b));
   while (b != INT32_MAX) {
-    // 1. compact the slots of block b
+    // 1. compact the slots of block b; pad the list to a multiple of kPad with
+    //    out-of-range offsets (those loads move no data)
     int count = 0;
 #pragma unroll
     for (int u = 0; u < KS; ++u) {
@@ -282,109 +514,111 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
       const uint64_t mask = __ballot(sel);
       const int pos = count + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-      if (sel) list[pos] = ((uint32_t)jn[u] << 8) | (uint32_t)(64 * u + lane);
+      if (sel) {
+        lkv[pos] = kvo[u];
+        lp[pos] = po[u];
+      }
       count += __popcll(mask);
     }
-    wave_lds_sync();
-
-    // 2. bias of each listed slot: 4 lanes per slot, 16 slots per pass
-    for (int p0 = 0; p0 < count; p0 += 16) {
-      const int pos = p0 + (lane >> 2);
-      const bool ok = pos < count;
-      const uint32_t ent = list[ok ? pos : 0];
-      const uint32_t idx = a.p_gathered ? (ent & 255u) : (ent >> 8);
-      const int voff = ok ? (int)(idx * (uint32_t)(kCap * EB) + (uint32_t)(cq * CPL * EB)) : kOutOfRange;
-      float x[CPL];
-      if constexpr (kBf16) {
-        const u32x2 w = __builtin_amdgcn_raw_buffer_load_b64(pres, voff, 0, kNt);
-        x[0] = __uint_as_float(w[0] << 16);
-        x[1] = __uint_as_float(w[0] & 0xFFFF0000u);
-        x[2] = __uint_as_float(w[1] << 16);
-        x[3] = __uint_as_float(w[1] & 0xFFFF0000u);
-      } else {
-        const u32x4 w = __builtin_amdgcn_raw_buffer_load_b128(pres, voff, 0, kNt);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) x[i] = __uint_as_float(w[i]);
-      }
-      const float mu = group_sum<4>((x[0] + x[1]) + (x[2] + x[3])) * (1.0f / kCap);
-      float dv[CPL], ss = 0.0f;
-#pragma unroll
-      for (int i = 0; i < CPL; ++i) {
-        dv[i] = x[i] - mu;
-        ss = fmaf(dv[i], dv[i], ss);
-      }
-      const float rstd = __builtin_amdgcn_rsqf(group_sum<4>(ss) * (1.0f / kCap) + a.eps);
-      float hp[kH];
-#pragma unroll
-      for (int h = 0; h < kH; ++h) {
-        float t = 0.0f;
-#pragma unroll
-        for (int i = 0; i < CPL; ++i) t = fmaf(wb[h][i], dv[i], t);
-        hp[h] = group_sum<4>(t);
-      }
-      const float mine = cq == 0 ? hp[0] : cq == 1 ? hp[1] : cq == 2 ? hp[2] : hp[3];
-      if (ok) lgs[pos][cq] = rstd * mine;
+    const int count_pad = (count + kPad - 1) / kPad * kPad;
+    if (lane < count_pad - count) {
+      lkv[count + lane] = (uint32_t)kOutOfRange;
+      lp[count + lane] = (uint32_t)kOutOfRange;
     }
     wave_lds_sync();
 
-    // 3. logits: K rows, NPI per load instruction, lane chunk c
-    const int n_ins = (count + NPI - 1) / NPI;
-    float mx = -INFINITY;
-    for (int i0 = 0; i0 < n_ins; i0 += kUnroll) {
-      u32x4 kw[kUnroll];
+    // 2. every pair-vector load of the list, then the first K/V batch, so the
+    //    bias work below overlaps the K/V latency
+    if constexpr (kBf16) {
+      // 16 slots per pass on the matrix cores: lane (n, g) holds channels
+      // 4g..4g+3 of slot n; W''.p gives the heads (rows 0..3) and the row sum
+      // (row 4); the diagonal of the Gram tile p.p^T the sums of squares.
+      const int n = lane & 15, g = lane >> 4;
+      u32x2 pw[kPasses];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int pos = NPI * (i0 + u) + lane / LPN;
-        const bool ok = pos < count;
-        const uint32_t j = list[ok ? pos : 0] >> 8;
-        kw[u] = __builtin_amdgcn_raw_buffer_load_b128(kres, ok ? (int)(j * (uint32_t)(kHD * EB) + 16u * c) : kOutOfRange,
-                                                      0, 0);
+      for (int ps = 0; ps < kPasses; ++ps) {
+        const int off = 16 * ps < count_pad ? (int)(lp[16 * ps + n] + 8u * g) : kOutOfRange;
+        pw[ps] = __builtin_amdgcn_raw_buffer_load_b64(pres, off, 0, kNt);
       }
+      issue_batch(0, 0);
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int pos = NPI * (i0 + u) + lane / LPN;
-        const bool ok = pos < count;
-        float dot = 0.0f;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) dot = fmaf(qv[e], chunk_elem<kBf16>(kw[u], e), dot);
-        dot = group_sum<LPH>(dot);
-        if (ok) {
-          const float lg = dot + lgs[pos][hl];
-          if ((lane % LPH) == 0) lgs[pos][hl] = lg;
-          mx = fmaxf(mx, lg);
+      for (int ps = 0; ps < kPasses; ++ps) {
+        if (16 * ps >= count_pad) break;
+        const int pos = 16 * ps + n;
+        const bf16x4 pv = as_bf16x4(pw[ps]);
+        const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+        f32x4 hb = mfma16(whi, pv, zero);
+        hb = mfma16(wlo, pv, hb);
+        const f32x4 gram = mfma16(pv, pv, zero);
+        // diagonal entry of column n: row n sits in lane group n/4, register n%4
+        const float t0 = (n & 1) ? gram[1] : gram[0];
+        const float t1 = (n & 1) ? gram[3] : gram[2];
+        float d = (n & 2) ? t1 : t0;
+        const int tg = n >> 2;
+        float x0 = d, x1 = d;
+        swap32(x0, x1);
+        d = (tg & 2) ? x1 : x0;
+        x0 = d;
+        x1 = d;
+        swap16(x0, x1);
+        const float s2 = (tg & 1) ? x1 : x0;
+        // row sum: row 4 is register 0 of lane group 1; bring it to group 0
+        float y0 = hb[0], y1 = hb[0];
+        swap16(y0, y1);
+        const float mu = y1 * (1.0f / kCap);
+        const float var = fmaxf(s2 * (1.0f / kCap) - mu * mu, 0.0f);
+        const float rstd = __builtin_amdgcn_rsqf(var + a.eps);
+        if (g == 0) {
+          const bool ok = pos < count;
+          *reinterpret_cast<float4*>(lb[pos]) =
+              ok ? make_float4(fmaf(rstd, hb[0], kShift), fmaf(rstd, hb[1], kShift), fmaf(rstd, hb[2], kShift),
+                               fmaf(rstd, hb[3], kShift))
+                 : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
         }
       }
-    }
-    mx = across_max<NPI>(mx);
-    const float mb = ceilf(mx);  // integer block maximum (or -inf)
-    const float m_new = fmaxf(m_run, mb);
-    const float sr = m_run == -INFINITY ? 0.0f : ldexpf(1.0f, (int)(m_run - m_new));
-    l_run *= sr;
+    } else {
+      // 4 lanes per slot, 16 slots per pass; quad reductions
+      const int cq = lane & 3;
+      u32x4 pw[kPasses];
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) acc[e] *= sr;
-    m_run = m_new;
+      for (int ps = 0; ps < kPasses; ++ps) {
+        const int off = 16 * ps < count_pad ? (int)(lp[16 * ps + (lane >> 2)] + 16u * cq) : kOutOfRange;
+        pw[ps] = __builtin_amdgcn_raw_buffer_load_b128(pres, off, 0, kNt);
+      }
+      issue_batch(0, 0);
+#pragma unroll
+      for (int ps = 0; ps < kPasses; ++ps) {
+        if (16 * ps >= count_pad) break;
+        const int pos = 16 * ps + (lane >> 2);
+        float x[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) x[i] = __uint_as_float(pw[ps][i]);
+        const float mu = group_sum<4>((x[0] + x[1]) + (x[2] + x[3])) * (1.0f / kCap);
+        float dv[4], ss = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          dv[i] = x[i] - mu;
+          ss = fmaf(dv[i], dv[i], ss);
+        }
+        const float rstd = __builtin_amdgcn_rsqf(group_sum<4>(ss) * (1.0f / kCap) + a.eps);
+        float hp[kH];
+#pragma unroll
+        for (int h = 0; h < kH; ++h) {
+          float t = 0.0f;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) t = fmaf(wb[h][i], dv[i], t);
+          hp[h] = group_sum<4>(t);
+        }
+        const float mine = cq == 0 ? hp[0] : cq == 1 ? hp[1] : cq == 2 ? hp[2] : hp[3];
+        lb[pos][cq] = pos < count ? rstd * mine : -INFINITY;
+      }
+    }
     wave_lds_sync();
 
-    // 4. values: V rows, weights exp2(logit - m)
-    for (int i0 = 0; i0 < n_ins; i0 += kUnroll) {
-      u32x4 vw[kUnroll];
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int pos = NPI * (i0 + u) + lane / LPN;
-        const bool ok = pos < count;
-        const uint32_t j = list[ok ? pos : 0] >> 8;
-        vw[u] = __builtin_amdgcn_raw_buffer_load_b128(vres, ok ? (int)(j * (uint32_t)(kHD * EB) + 16u * c) : kOutOfRange,
-                                                      0, 0);
-      }
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int pos = NPI * (i0 + u) + lane / LPN;
-        const bool ok = pos < count && m_new != -INFINITY;
-        const float p = ok ? __builtin_amdgcn_exp2f(lgs[pos < count ? pos : 0][hl] - m_new) : 0.0f;
-        l_run += p;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[e] = fmaf(p, chunk_elem<kBf16>(vw[u], e), acc[e]);
-      }
+    // 3. batches of K/V rows
+    for (int b0 = 0; b0 < count_pad; b0 += kBatch) {
+      compute_batch(0, b0);
+      if (b0 + kBatch < count_pad) issue_batch(0, b0 + kBatch);
     }
 
     // next block present among the neighbours
@@ -435,6 +669,12 @@ hipError_t launch_attn(const SparseAttnArgs& a, hipStream_t st) {
 
 hipError_t launch_sparse_proj(const SparseProjArgs& a, hipStream_t st) {
   const int64_t rows = a.n_atoms > a.n_q ? a.n_atoms : a.n_q;
+  if (a.c_atom == kHD) {
+    int64_t wgs = ((rows + 63) / 64 + 3) / 4;
+    if (wgs > 128) wgs = 128;  // 4 x 128 workgroups, two per CU (64 KB of LDS each); waves loop over atom groups
+    hipLaunchKernelGGL(atom_proj128_kernel, dim3((unsigned)wgs, 4), dim3(256), 0, st, a);
+    return hipGetLastError();
+  }
   const int64_t groups = ((rows + 15) / 16 + kProjTiles - 1) / kProjTiles;
   hipLaunchKernelGGL(atom_proj_kernel, dim3((unsigned)groups, kH, 4), dim3(64), 0, st, a);
   return hipGetLastError();

@@ -376,8 +376,9 @@ def _dev() -> ctypes.CDLL:
         lib.synth_dev_copy.argtypes = [vp, vp, i64, vp]
         lib.synth_dev_read.argtypes = [vp, i64, vp, vp]
         lib.synth_dev_read_pattern.argtypes = [vp, i64, i64, i32, vp, vp]
+        lib.synth_dev_gather_pattern.argtypes = [vp, vp, i64, vp, i64, i32, vp, vp]
         for f in (lib.synth_dev_z_rows, lib.synth_dev_normal, lib.synth_dev_copy, lib.synth_dev_read,
-                  lib.synth_dev_read_pattern):
+                  lib.synth_dev_read_pattern, lib.synth_dev_gather_pattern):
             f.restype = ctypes.c_int
         _dev_lib = lib
     return _dev_lib
@@ -407,6 +408,14 @@ def device_read_pattern(z: int, n_tok: int, n_rows: int, n_parts: int, sink: int
     kernel's order, with no arithmetic (the access pattern's bandwidth ceiling)."""
     if _dev().synth_dev_read_pattern(z, n_tok, n_rows, n_parts, sink, stream) != 0:
         raise RuntimeError("synth_dev_read_pattern failed")
+
+
+def device_gather_pattern(k: int, v: int, n_atoms: int, nbr: int, n_q: int, n_slots: int, sink: int,
+                          stream: int) -> None:
+    """Gathers the 256-byte K and V rows of every listed neighbour in the sparse
+    attention's pattern, with no arithmetic (that pattern's ceiling)."""
+    if _dev().synth_dev_gather_pattern(k, v, n_atoms, nbr, n_q, n_slots, sink, stream) != 0:
+        raise RuntimeError("synth_dev_gather_pattern failed")
 
 
 def device_read(src: int, nbytes: int, sink: int, stream: int) -> None:

@@ -5,8 +5,9 @@
 // round-to-nearest-even), so a value made here equals the host's bit for bit.
 // This library fills large device inputs (the pair tensor reaches 147 GB) and
 // holds none of the attention arithmetic. It also carries calibration kernels
-// for the benchmark: a plain copy, a plain streaming read, and a read in the
-// fused attention kernel's access pattern.
+// for the benchmark: a plain copy, a plain streaming read, a read in the
+// fused attention kernel's access pattern, and the sparse attention's K/V
+// gather pattern.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -136,6 +137,35 @@ __global__ void __launch_bounds__(256) read_pattern_kernel(const uint4* __restri
   if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9E3779B9u) sink[0] = 1;
 }
 
+// Gathers the K and V rows (256 bytes each) of every listed neighbour as the
+// sparse atom attention does (one wave per query row, 16 lanes per row, 16
+// bytes per lane, 4 rows per load, 8 loads of K and 8 of V in flight), with no
+// arithmetic: the ceiling of that access pattern. An empty slot (index outside
+// [0, n_atoms)) reads row 0 instead.
+__global__ void __launch_bounds__(256) gather_pattern_kernel(const uint4* __restrict__ k, const uint4* __restrict__ v,
+                                                             int64_t n_atoms, const int32_t* __restrict__ nbr,
+                                                             int64_t n_q, int32_t n_slots, uint32_t* __restrict__ sink) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= n_q) return;
+  u32x4 acc = {0u, 0u, 0u, 0u};
+  for (int t0 = 0; t0 < n_slots; t0 += 32) {
+    u32x4 x[16];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int t = t0 + 4 * u + (lane >> 4);
+      const int32_t j = t < n_slots ? nbr[r * n_slots + t] : -1;
+      const int64_t jj = (j >= 0 && j < n_atoms) ? j : 0;
+      x[2 * u] = *reinterpret_cast<const u32x4*>(k + jj * 16 + (lane & 15));
+      x[2 * u + 1] = *reinterpret_cast<const u32x4*>(v + jj * 16 + (lane & 15));
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u) acc ^= x[u];
+  }
+  if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9E3779B9u) sink[0] = 1;
+}
+
 int grid_for(int64_t items) {
   int64_t g = (items + 255) / 256;
   if (g > 256 * 64) g = 256 * 64;
@@ -177,6 +207,15 @@ int synth_dev_read_pattern(const void* z, int64_t n_tok, int64_t n_rows, int32_t
   if (!z || !sink || n_tok <= 0 || n_rows <= 0 || n_parts < 1 || n_parts > n_tok) return -1;
   hipLaunchKernelGGL(read_pattern_kernel, dim3((unsigned)((n_rows + 63) / 64), (unsigned)n_parts), dim3(256), 0,
                      (hipStream_t)stream, (const uint4*)z, n_tok, n_rows, n_parts, (uint32_t*)sink);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+int synth_dev_gather_pattern(const void* k, const void* v, int64_t n_atoms, const int32_t* nbr, int64_t n_q,
+                             int32_t n_slots, void* sink, void* stream) {
+  if (!k || !v || !nbr || !sink || n_atoms <= 0 || n_q < 0 || n_slots <= 0) return -1;
+  if (n_q == 0) return 0;
+  hipLaunchKernelGGL(gather_pattern_kernel, dim3((unsigned)((n_q + 3) / 4)), dim3(256), 0, (hipStream_t)stream,
+                     (const uint4*)k, (const uint4*)v, n_atoms, nbr, n_q, n_slots, (uint32_t*)sink);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
