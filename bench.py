@@ -204,6 +204,13 @@ def sparse_main(args, wl):
         if evs is not None:
             dcp.dcp_set_timing_events(None, None)
 
+    # calibration (outside the timed region): a plain copy of known size for
+    # counter scaling
+    cal = min(args.calibrate_bytes, p.numel() * p.element_size() // 2 // 16 * 16)
+    scratch = torch.empty(cal, dtype=torch.uint8, device=dev)
+    synth.device_copy(p.data_ptr(), scratch.data_ptr(), cal, sp)
+    torch.cuda.synchronize()
+    del scratch
     # ceiling of the K/V gather pattern (same neighbour lists, no arithmetic)
     kbuf = torch.zeros((L, hd), dtype=torch.bfloat16 if wl.bf16 else torch.float32, device=dev)
     vbuf = torch.zeros_like(kbuf)
