@@ -30,6 +30,9 @@ PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, published
 KERNEL_SOURCES = ("paper_2607_05439_amd/csrc/fast.hip", "paper_2607_05439_amd/csrc/cdna4.h")
 SPARSE_SOURCES = ("paper_2607_05439_amd/csrc/sparse.hip", "paper_2607_05439_amd/csrc/cdna4.h")
 SPARSE_METRIC = "ms/layer + gathered GB/s for sparse kNN pair-biased atom attention"
+KNN_SOURCES = ("paper_2607_05439_amd/csrc/knn.hip",)
+KNN_METRIC = "ms per kNN search + candidate pairs/s for the chunked k-nearest-neighbour top-k"
+PEAK_FP32_TFLOPS = 157.3  # MI355X fp32 vector, published
 
 
 def progress(msg):
@@ -290,6 +293,101 @@ def sparse_main(args, wl):
     print(json.dumps(line), flush=True)
 
 
+def knn_main(args, wl):
+    import numpy as np
+    import torch
+    import paper_2607_05439_amd as dcp
+    import oracle
+    import synth
+
+    dev = torch.device("cuda:0")
+    sp = torch.cuda.current_stream().cuda_stream
+    L, k, n_q = wl.n_atoms, wl.k, wl.n_q
+    progress(f"workload {wl.name}: L={L} atoms, query atoms {wl.q_row0}..{wl.q_row0 + n_q - 1}, k={k}")
+    x_host = synth.coords(wl)
+    x = torch.from_numpy(x_host).to(dev)
+    xq = x[wl.q_row0:wl.q_row0 + n_q]
+    idx = torch.empty((n_q, k), dtype=torch.int32, device=dev)
+    d2 = torch.empty((n_q, k), dtype=torch.float32, device=dev)
+    pairs = n_q * L
+    hip = Hip()
+
+    def step(evs=None):
+        if evs is not None:
+            dcp.dcp_set_timing_events(*evs)
+        dcp.dcp_knn_topk(xq, n_q, x, L, 0, wl.q_row0, None, None, 0, k, idx, d2, sp)
+        if evs is not None:
+            dcp.dcp_set_timing_events(None, None)
+
+    # calibration for counter scaling: a plain copy of known size
+    cal = 1 << 28
+    src = torch.empty(cal, dtype=torch.uint8, device=dev)
+    dst = torch.empty(cal, dtype=torch.uint8, device=dev)
+    synth.device_copy(src.data_ptr(), dst.data_ptr(), cal, sp)
+    torch.cuda.synchronize()
+    del src, dst
+    progress(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(hip.event(), hip.event()) for _ in range(args.steps)]
+    t_start, t_stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    progress(f"timing {args.steps} steps")
+    t_start.record()
+    for i in range(args.steps):
+        step(evs[i])
+    t_stop.record()
+    torch.cuda.synchronize()
+    ms_per_step = t_start.elapsed_time(t_stop) / args.steps
+    kms = sum(hip.elapsed_ms(a, b) for a, b in evs) / len(evs)
+    flops = 8.0 * pairs  # 3 subtractions, 3 products, 2 sums per candidate pair
+    achieved = flops / (kms * 1e-3) / 1e12
+    value = pairs / (ms_per_step * 1e-3) / 1e9
+    progress(f"{ms_per_step:.3f} ms per search, kernel {kms:.3f} ms: {pairs / (kms * 1e-3) / 1e9:.1f} Gpair/s, "
+             f"{achieved:.1f} TFLOP/s of distance arithmetic")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        progress(f"cpu baseline: oracle on sampled query atoms (~{args.cpu_seconds:.0f} s)")
+        threads = ctypes.CDLL("libgomp.so.1").omp_get_max_threads()
+        rows = np.arange(0, n_q, max(1, n_q // (4 * threads)))
+        t0 = time.perf_counter()
+        oracle.knn(x_host[wl.q_row0 + rows], x_host, k)
+        per_row = (time.perf_counter() - t0) / len(rows)
+        n_rows = int(min(n_q, max(len(rows), args.cpu_seconds / per_row)))
+        rows = np.sort(np.random.default_rng(1).choice(n_q, n_rows, replace=False))
+        t0 = time.perf_counter()
+        oracle.knn(x_host[wl.q_row0 + rows], x_host, k)
+        t_run = time.perf_counter() - t0
+        t_full = t_run / n_rows * n_q
+        cpu = {"value": round(pairs / t_full / 1e9, 6), "unit": "Gpair/s", "cores": threads, "kind": "oracle",
+               "sample": f"{n_rows} of {n_q} query atoms in {t_run:.1f} s (brute force + sort per row); "
+                         f"extrapolated search time {t_full:.1f} s",
+               "ms_per_search_extrapolated": round(t_full * 1e3, 1)}
+    line = {
+        "metric": KNN_METRIC,
+        "value": round(value, 2),
+        "unit": "Gpair/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded chains of residues placed on a sphere; stands in for RFD3 assembly coordinates)",
+        "config": {"workload": wl.name, "n_atoms": L, "q_row0": wl.q_row0, "n_q": n_q, "k": k,
+                   "candidate_pairs": pairs},
+        "roofline": {"bound": "alu", "achieved": round(achieved, 2), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_FP32_TFLOPS, 4),
+                     "traffic": stored_traffic(wl.name, KNN_SOURCES), "kernel": "knn_kernel",
+                     "kernel_ms": round(kms, 4), "algorithmic_flops_per_launch": flops},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -314,6 +412,8 @@ def main():
 
     if args.workload in synth.ATOM_WORKLOADS:
         return sparse_main(args, synth.ATOM_WORKLOADS[args.workload])
+    if args.workload in synth.KNN_WORKLOADS:
+        return knn_main(args, synth.KNN_WORKLOADS[args.workload])
     wl = synth.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()

@@ -211,10 +211,52 @@ int dcp_sparse_pair_bias_attention(const dcp_sparse_shape* shape, const dcp_weig
                                    int32_t n_key_blocks, void* out, void* workspace, size_t workspace_bytes,
                                    void* stream);
 
+/* ---------------------------------------------------------------------------
+ * k nearest neighbours of atoms (Appendix "Distributed kNN for sparse atom
+ * attention": each query atom keeps the k closest atoms; distances are taken
+ * block by block, never as a whole [L, L] matrix, and the running top-k of each
+ * query is merged with every block's candidates, the ring top-k combine;
+ * Methods, "Atom-level kNN attention budget": k = 128, intra- and inter-chain
+ * budgets).
+ *
+ * Order: squared Euclidean distance computed in fp32 as
+ * ((dx*dx) + (dy*dy)) + (dz*dz), dx = x_q - x_c, every operation rounded to
+ * fp32; ties go to the smaller candidate index. The result is therefore exact
+ * and deterministic: it does not depend on blocking or on the visiting order.
+ * NaN coordinates give an unspecified order.
+ * ------------------------------------------------------------------------- */
+
+/* The k nearest candidates of each query.
+ *   x_q        [n_q, 3] fp32 query coordinates
+ *   x_c        [n_c, 3] fp32 candidate coordinates (may be NULL when n_c = 0);
+ *              candidate j has the global index c_index0 + j
+ *              (c_index0 + n_c <= INT32_MAX)
+ *   q_self0    when the queries are themselves candidates, the position in x_c
+ *              of query 0 (then query r is candidate q_self0 + r); else -1.
+ *              Only the visiting order depends on it, never the result.
+ *   group_q, group_c  [n_q], [n_c] int32 group ids (chains), used when
+ *              group_mode = 1 (same group only) or 2 (other groups only);
+ *              may be NULL with group_mode = 0 (every candidate admissible)
+ *   k          1 <= k <= 256
+ *   idx_out    [n_q, k] int32 global indices, nearest first; -1 past the
+ *              number of admissible candidates
+ *   d2_out     [n_q, k] fp32 squared distances (+inf past the end), or NULL
+ * Device pointers, 4-byte aligned. No workspace. n_q = 0 is a no-op. */
+int dcp_knn_topk(const float* x_q, int64_t n_q, const float* x_c, int64_t n_c, int64_t c_index0, int64_t q_self0,
+                 const int32_t* group_q, const int32_t* group_c, int32_t group_mode, int32_t k, int32_t* idx_out,
+                 float* d2_out, void* stream);
+
+/* The ring top-k combine: per row, the k smallest entries of the union of two
+ * lists sorted as dcp_knn_topk returns them ([n_rows, k] each; index -1 =
+ * empty). Equal entries in both lists are both kept (a's first). Outputs must
+ * not overlap the inputs. */
+int dcp_topk_merge(int64_t n_rows, int32_t k, const int32_t* idx_a, const float* d2_a, const int32_t* idx_b,
+                   const float* d2_b, int32_t* idx_out, float* d2_out, void* stream);
+
 /* Optional timing hook: when both are non-NULL hipEvent_t handles, the calling
- * thread's next dcp_pair_bias_attention and dcp_sparse_pair_bias_attention
- * calls record `start` just before and `stop` just after the attention kernel
- * (after the projections), on that call's stream. Pass NULL, NULL to clear.
+ * thread's next dcp_pair_bias_attention, dcp_sparse_pair_bias_attention and
+ * dcp_knn_topk calls record `start` just before and `stop` just after the
+ * attention (or kNN) kernel, after any projections, on that call's stream. Pass NULL, NULL to clear.
  * Host-only. */
 int dcp_set_timing_events(void* start_event, void* stop_event);
 

@@ -30,8 +30,11 @@ def _configure(lib: ctypes.CDLL) -> ctypes.CDLL:
                                      vp, vp, vp, vp, vp, vp, vp, vp, f64, i32, vp, vp, vp, vp]
     lib.oracle_sparse_attention.argtypes = [i64, i32, i32, i32, i32, i32, vp, vp, i32, vp, vp, i64,
                                             vp, vp, vp, vp, vp, vp, vp, vp, f64, i32, vp]
+    lib.oracle_knn.argtypes = [vp, i64, vp, i64, i64, vp, vp, i32, i32, vp, vp]
+    lib.oracle_topk_merge.argtypes = [i64, i32, vp, vp, vp, vp, vp, vp]
+    lib.oracle_knn_blocked.argtypes = [vp, i64, vp, i64, vp, vp, i32, i32, i32, vp, vp]
     for f in (lib.oracle_bias, lib.oracle_attend, lib.oracle_merge, lib.oracle_attention,
-              lib.oracle_sparse_attention):
+              lib.oracle_sparse_attention, lib.oracle_knn, lib.oracle_topk_merge, lib.oracle_knn_blocked):
         f.restype = ctypes.c_int
     return lib
 
@@ -178,3 +181,47 @@ def sparse_attention(a: np.ndarray, p_rows: np.ndarray, nbr: np.ndarray, rows: S
     if rc != 0:
         raise ValueError("oracle_sparse_attention rejected its arguments")
     return out
+
+
+def _f32c(a):
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _i32c(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.int32)
+
+
+def knn(x_q: np.ndarray, x_c: np.ndarray, k: int, c_index0: int = 0, group_q=None, group_c=None, group_mode: int = 0,
+        n_blocks: int = 1) -> Tuple[np.ndarray, np.ndarray]:
+    """k nearest candidates of each query: (idx [n_q, k] int32, d2 [n_q, k] fp32),
+    sorted by (d2, index); n_blocks > 1 uses the blocked ring form (c_index0 = 0)."""
+    xq, xc = _f32c(x_q), _f32c(x_c)
+    gq, gc = _i32c(group_q), _i32c(group_c)
+    n_q, n_c = xq.shape[0], xc.shape[0]
+    idx = np.empty((n_q, k), dtype=np.int32)
+    d2 = np.empty((n_q, k), dtype=np.float32)
+    gp = lambda a: None if a is None else a.ctypes.data
+    if n_blocks == 1:
+        rc = _load().oracle_knn(xq.ctypes.data, n_q, xc.ctypes.data, n_c, c_index0, gp(gq), gp(gc), group_mode, k,
+                                idx.ctypes.data, d2.ctypes.data)
+    else:
+        assert c_index0 == 0
+        rc = _load().oracle_knn_blocked(xq.ctypes.data, n_q, xc.ctypes.data, n_c, gp(gq), gp(gc), group_mode, k,
+                                        n_blocks, idx.ctypes.data, d2.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle_knn rejected its arguments")
+    return idx, d2
+
+
+def topk_merge(idx_a, d2_a, idx_b, d2_b) -> Tuple[np.ndarray, np.ndarray]:
+    """The ring top-k combine of two sorted candidate lists [n, k]."""
+    ia, ib = _i32c(idx_a), _i32c(idx_b)
+    da, db = _f32c(d2_a), _f32c(d2_b)
+    n, k = ia.shape
+    io = np.empty((n, k), dtype=np.int32)
+    do = np.empty((n, k), dtype=np.float32)
+    rc = _load().oracle_topk_merge(n, k, ia.ctypes.data, da.ctypes.data, ib.ctypes.data, db.ctypes.data,
+                                   io.ctypes.data, do.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle_topk_merge rejected its arguments")
+    return io, do

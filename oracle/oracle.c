@@ -431,3 +431,126 @@ int oracle_sparse_attention(int64_t n_atoms, int c_atom, int c_ap, int n_heads, 
   free(vv);
   return 0;
 }
+
+/* ---------------------------------------------------------------------------
+ * k nearest neighbours of atoms (Appendix "Distributed kNN for sparse atom
+ * attention"; Methods, "Atom-level kNN attention budget"): for every query
+ * atom, the k candidate atoms closest in Euclidean distance, never forming the
+ * whole [L, L] distance matrix: the candidates are visited in blocks, each
+ * block's top-k is taken, and the running top-k is merged with it (the ring
+ * top-k combine).
+ *
+ * Readings: the order is by squared distance, computed in fp32 as
+ * ((dx*dx) + (dy*dy)) + (dz*dz) with dx = x_q - x_c and every operation
+ * rounded to fp32, ties broken by the smaller candidate index; a query's own
+ * atom (distance 0) counts. group_mode 1 admits only candidates of the query's
+ * group, 2 only candidates of other groups (the paper's intra- and
+ * inter-chain budgets); 0 admits all. Fewer than k admissible candidates
+ * leave index -1 and d2 +inf at the end of the list.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  float d2;
+  int64_t j;
+} knn_key;
+
+static int knn_less(knn_key a, knn_key b) { return a.d2 < b.d2 || (a.d2 == b.d2 && a.j < b.j); }
+
+static int knn_cmp(const void* pa, const void* pb) {
+  const knn_key a = *(const knn_key*)pa, b = *(const knn_key*)pb;
+  return knn_less(a, b) ? -1 : (knn_less(b, a) ? 1 : 0);
+}
+
+static float knn_d2(const float* a, const float* b) {
+  const float dx = a[0] - b[0], dy = a[1] - b[1], dz = a[2] - b[2];
+  const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
+  const float s = xx + yy;
+  return s + zz;
+}
+
+/* Top-k of each query against candidates [0, n_c) (global index c_index0 + j). */
+int oracle_knn(const float* x_q, int64_t n_q, const float* x_c, int64_t n_c, int64_t c_index0, const int32_t* group_q,
+               const int32_t* group_c, int group_mode, int k, int32_t* idx_out, float* d2_out) {
+  if (!x_q || !x_c || !idx_out || k < 1 || n_c < 0 || n_q < 0) return -1;
+  if (group_mode != 0 && (!group_q || !group_c)) return -1;
+#pragma omp parallel
+  {
+    knn_key* keys = (knn_key*)malloc(sizeof(knn_key) * (size_t)(n_c > 0 ? n_c : 1));
+#pragma omp for schedule(dynamic, 4)
+    for (int64_t r = 0; r < n_q; ++r) {
+      int64_t n = 0;
+      for (int64_t j = 0; j < n_c; ++j) {
+        if (group_mode == 1 && group_c[j] != group_q[r]) continue;
+        if (group_mode == 2 && group_c[j] == group_q[r]) continue;
+        keys[n].d2 = knn_d2(x_q + 3 * r, x_c + 3 * j);
+        keys[n].j = c_index0 + j;
+        ++n;
+      }
+      qsort(keys, (size_t)n, sizeof(knn_key), knn_cmp);
+      for (int t = 0; t < k; ++t) {
+        idx_out[r * k + t] = t < n ? (int32_t)keys[t].j : -1;
+        if (d2_out) d2_out[r * k + t] = t < n ? keys[t].d2 : INFINITY;
+      }
+    }
+    free(keys);
+  }
+  return 0;
+}
+
+/* The ring top-k combine: per row, the k smallest entries of the union of two
+ * sorted candidate lists (index -1 entries are empty and sort last). */
+int oracle_topk_merge(int64_t n_rows, int k, const int32_t* idx_a, const float* d2_a, const int32_t* idx_b,
+                      const float* d2_b, int32_t* idx_out, float* d2_out) {
+  if (!idx_a || !d2_a || !idx_b || !d2_b || !idx_out || !d2_out || k < 1) return -1;
+  for (int64_t r = 0; r < n_rows; ++r) {
+    knn_key* u = (knn_key*)malloc(sizeof(knn_key) * (size_t)(2 * k));
+    int n = 0;
+    for (int t = 0; t < k; ++t) {
+      if (idx_a[r * k + t] >= 0) {
+        u[n].d2 = d2_a[r * k + t];
+        u[n].j = idx_a[r * k + t];
+        ++n;
+      }
+      if (idx_b[r * k + t] >= 0) {
+        u[n].d2 = d2_b[r * k + t];
+        u[n].j = idx_b[r * k + t];
+        ++n;
+      }
+    }
+    qsort(u, (size_t)n, sizeof(knn_key), knn_cmp);
+    for (int t = 0; t < k; ++t) {
+      idx_out[r * k + t] = t < n ? (int32_t)u[t].j : -1;
+      d2_out[r * k + t] = t < n ? u[t].d2 : INFINITY;
+    }
+    free(u);
+  }
+  return 0;
+}
+
+/* Blocked form (self-tests): candidates split into n_blocks by the chunk rule,
+ * each block's top-k taken, merged into the running top-k in block order. */
+int oracle_knn_blocked(const float* x_q, int64_t n_q, const float* x_c, int64_t n_c, const int32_t* group_q,
+                       const int32_t* group_c, int group_mode, int k, int n_blocks, int32_t* idx_out, float* d2_out) {
+  if (n_blocks < 1 || n_blocks > n_c) return -1;
+  const size_t cells = (size_t)(n_q * k);
+  int32_t* bi = (int32_t*)malloc(sizeof(int32_t) * cells);
+  float* bd = (float*)malloc(sizeof(float) * cells);
+  int32_t* ri = (int32_t*)malloc(sizeof(int32_t) * cells);
+  float* rd = (float*)malloc(sizeof(float) * cells);
+  for (size_t c = 0; c < cells; ++c) {
+    ri[c] = -1;
+    rd[c] = INFINITY;
+  }
+  for (int b = 0; b < n_blocks; ++b) {
+    int64_t size, start;
+    oracle_chunk(n_c, n_blocks, b, &size, &start);
+    oracle_knn(x_q, n_q, x_c + 3 * start, size, start, group_q, group_c ? group_c + start : NULL, group_mode, k, bi, bd);
+    oracle_topk_merge(n_q, k, ri, rd, bi, bd, idx_out, d2_out);
+    memcpy(ri, idx_out, sizeof(int32_t) * cells);
+    memcpy(rd, d2_out, sizeof(float) * cells);
+  }
+  free(bi);
+  free(bd);
+  free(ri);
+  free(rd);
+  return 0;
+}

@@ -548,4 +548,67 @@ int dcp_sparse_pair_bias_attention(const dcp_sparse_shape* shape, const dcp_weig
   return ok();
 }
 
+// ----------------------------------------------------------------------------- k nearest neighbours
+int dcp_knn_topk(const float* x_q, int64_t n_q, const float* x_c, int64_t n_c, int64_t c_index0, int64_t q_self0,
+                 const int32_t* group_q, const int32_t* group_c, int32_t group_mode, int32_t k, int32_t* idx_out,
+                 float* d2_out, void* stream) {
+  if (n_q < 0 || n_c < 0) return fail(DCP_ERR_INVALID_ARGUMENT, "n_q and n_c must be >= 0");
+  if (k < 1) return fail(DCP_ERR_INVALID_ARGUMENT, "k must be >= 1 (got %d)", k);
+  if (k > dcp::kKnnMaxK) return fail(DCP_ERR_UNSUPPORTED, "k must be <= %d (got %d)", dcp::kKnnMaxK, k);
+  if (c_index0 < 0 || c_index0 + n_c > (int64_t)INT32_MAX)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "candidate indices c_index0 .. c_index0 + n_c must fit in int32");
+  if (group_mode < 0 || group_mode > 2) return fail(DCP_ERR_INVALID_ARGUMENT, "group_mode must be 0, 1 or 2");
+  if (group_mode != 0 && (!group_q || !group_c))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "group_q and group_c are required when group_mode != 0");
+  if (n_q == 0) return ok();
+  if (!x_q || (!x_c && n_c > 0) || !idx_out)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "x_q, x_c (when n_c > 0) and idx_out are required");
+  if (!aligned(x_q, 4) || !aligned(x_c, 4) || !aligned(idx_out, 4) || (d2_out && !aligned(d2_out, 4)))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "x_q, x_c, idx_out and d2_out must be 4-byte aligned");
+  if (n_q == 0) return ok();
+  dcp::KnnArgs a{};
+  a.x_q = x_q;
+  a.x_c = x_c;
+  a.group_q = group_q;
+  a.group_c = group_c;
+  a.n_q = n_q;
+  a.n_c = n_c;
+  a.c_index0 = c_index0;
+  a.q_self0 = q_self0 >= 0 && q_self0 < n_c ? q_self0 : -1;
+  a.k = k;
+  a.group_mode = group_mode;
+  a.idx_out = idx_out;
+  a.d2_out = d2_out;
+  hipError_t e;
+  if (g_ev_start && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_start), static_cast<hipStream_t>(stream))) != hipSuccess)
+    return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
+  if ((e = dcp::launch_knn(a, static_cast<hipStream_t>(stream))) != hipSuccess)
+    return fail(DCP_ERR_HIP, "knn launch failed: %s", hipGetErrorString(e));
+  if (g_ev_stop && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_stop), static_cast<hipStream_t>(stream))) != hipSuccess)
+    return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int dcp_topk_merge(int64_t n_rows, int32_t k, const int32_t* idx_a, const float* d2_a, const int32_t* idx_b,
+                   const float* d2_b, int32_t* idx_out, float* d2_out, void* stream) {
+  if (n_rows < 0) return fail(DCP_ERR_INVALID_ARGUMENT, "n_rows must be >= 0");
+  if (k < 1) return fail(DCP_ERR_INVALID_ARGUMENT, "k must be >= 1 (got %d)", k);
+  if (k > dcp::kKnnMaxK) return fail(DCP_ERR_UNSUPPORTED, "k must be <= %d (got %d)", dcp::kKnnMaxK, k);
+  if (!idx_a || !d2_a || !idx_b || !d2_b || !idx_out || !d2_out)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "all six lists are required");
+  if (n_rows == 0) return ok();
+  dcp::TopkMergeArgs a{};
+  a.n_rows = n_rows;
+  a.k = k;
+  a.idx_a = idx_a;
+  a.idx_b = idx_b;
+  a.d2_a = d2_a;
+  a.d2_b = d2_b;
+  a.idx_out = idx_out;
+  a.d2_out = d2_out;
+  const hipError_t e = dcp::launch_topk_merge(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "top-k merge launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 }  // extern "C"

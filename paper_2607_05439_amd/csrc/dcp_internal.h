@@ -154,6 +154,28 @@ struct SparseAttnArgs {
   void* out;              // [n_q][128]
 };
 
+// k nearest neighbours: up to 256 per query; candidate indices fit in int32.
+constexpr int kKnnMaxK = 256;
+
+struct KnnArgs {
+  const float* x_q;       // [n_q][3]
+  const float* x_c;       // [n_c][3]
+  const int32_t *group_q, *group_c;
+  int64_t n_q, n_c, c_index0, q_self0;
+  int32_t k, group_mode;
+  int32_t* idx_out;       // [n_q][k]
+  float* d2_out;          // [n_q][k] or null
+};
+
+struct TopkMergeArgs {
+  int64_t n_rows;
+  int32_t k;
+  const int32_t *idx_a, *idx_b;
+  const float *d2_a, *d2_b;
+  int32_t* idx_out;
+  float* d2_out;
+};
+
 hipError_t launch_fast_proj(const FastProjArgs& a, hipStream_t st);
 hipError_t launch_fast_attn(const FastAttnArgs& a, hipStream_t st);
 hipError_t launch_fast_bias(const FastBiasArgs& a, hipStream_t st);
@@ -163,5 +185,7 @@ hipError_t launch_gen_bias(const GenBiasArgs& a, hipStream_t st);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t st);
 hipError_t launch_sparse_proj(const SparseProjArgs& a, hipStream_t st);
 hipError_t launch_sparse_attn(const SparseAttnArgs& a, bool bf16, hipStream_t st);
+hipError_t launch_knn(const KnnArgs& a, hipStream_t st);
+hipError_t launch_topk_merge(const TopkMergeArgs& a, hipStream_t st);
 
 }  // namespace dcp

@@ -37,6 +37,7 @@ _M2 = np.uint64(0x94D049BB133111EB)
 T_S, T_Z, T_WQ, T_WK, T_WV, T_WG, T_WB, T_ZBASE, T_MASK, T_GAMMA, T_BETA, T_BB = range(1, 13)
 # atom path: single track A, pair track P, neighbour draws, ragged draws, weights
 (T_A, T_P, T_NBR, T_NBR_RAG, T_AWQ, T_AWK, T_AWV, T_AWG, T_AWB, T_AGAMMA, T_ABETA, T_ABB) = range(13, 25)
+T_XYZ = 25  # atom coordinates
 
 
 # ----------------------------------------------------------------------------- numpy definition
@@ -125,6 +126,7 @@ def _host() -> ctypes.CDLL:
         lib.synth_normal_bf16.argtypes = [u64, u64, i64, vp]
         lib.synth_z_rows.argtypes = [u64, u64, i64, i64, i32, vp, i64, i32, vp]
         lib.synth_neighbours.argtypes = [u64, u64, i64, i32, i32, i32, i32, i32, i64, i64, i32, vp]
+        lib.synth_coords.argtypes = [u64, i64, i32, i32, vp]
         _host_lib = lib
     return _host_lib
 
@@ -357,6 +359,50 @@ def p_fill_device(wl: AtomWorkload, ptr: int, row0: int, n_rows: int, stream: in
                                  stream)
     if rc != 0:
         raise RuntimeError(f"synth_dev_z_rows failed ({rc})")
+
+
+# ----------------------------------------------------------------------------- kNN workloads
+@dataclasses.dataclass(frozen=True)
+class KnnWorkload:
+    """k nearest neighbours of the query atoms [q_row0, q_row0 + n_q) among all
+    L atoms of a synthetic assembly (chains of residues of atoms)."""
+    name: str
+    n_atoms: int
+    k: int
+    q_row0: int
+    n_q: int
+    n_col_blocks: int       # candidate blocks visited in ring order
+    per_res: int = 8
+    per_chain: int = 1600
+    seed: int = 0
+    note: str = ""
+
+    @property
+    def n_chains(self) -> int:
+        return (self.n_atoms + self.per_chain - 1) // self.per_chain
+
+
+KNN_WORKLOADS: Dict[str, KnnWorkload] = {
+    w.name: w
+    for w in [
+        KnnWorkload("knn300", 300, 128, 0, 300, 1, per_chain=50,
+                    note="6 chains of 50 atoms: every query sees every atom"),
+        KnnWorkload("knn5000", 5000, 128, 0, 5000, 3, per_chain=1000, note="RFD3's 5000-atom crop, 5 chains"),
+        KnnWorkload("knn96k", 96000, 128, 24000, 24000, 4,
+                    note="60 chains x 1600 atoms; a 24000-atom query stripe against 4 candidate blocks of 24000"),
+    ]
+}
+
+
+def coords(wl: KnnWorkload) -> np.ndarray:
+    """Atom coordinates [L, 3] fp32 of the workload's assembly."""
+    out = np.empty((wl.n_atoms, 3), dtype=np.float32)
+    _host().synth_coords(key(wl.seed, T_XYZ), wl.n_atoms, wl.per_res, wl.per_chain, out.ctypes.data)
+    return out
+
+
+def chain_ids(wl: KnnWorkload) -> np.ndarray:
+    return (np.arange(wl.n_atoms) // wl.per_chain).astype(np.int32)
 
 
 # ----------------------------------------------------------------------------- device twin

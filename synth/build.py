@@ -10,7 +10,7 @@ HIP_FLAGS = ["-O3", "--offload-arch=gfx950", "-fPIC", "-shared", "-ffp-contract=
 def build_host() -> str:
     out = os.path.join(HERE, "libsynth_host.so")
     subprocess.check_call(["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-fPIC", "-shared",
-                           os.path.join(HERE, "csrc", "synth_host.c"), "-o", out + ".tmp"])
+                           os.path.join(HERE, "csrc", "synth_host.c"), "-lm", "-o", out + ".tmp"])
     os.replace(out + ".tmp", out)
     return out
 

@@ -19,6 +19,8 @@
  *                 evaluated as two separately rounded fp32 operations.
  */
 #include <stdint.h>
+#include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #define SM_G 0x9E3779B97F4A7C15ULL
@@ -173,5 +175,53 @@ void synth_neighbours(uint64_t key, uint64_t key2, int64_t n_atoms, int32_t per_
         for (int t = k - drop; t < k; ++t) row[t] = -1;
       }
     }
+  }
+}
+
+/* Atom coordinates of a synthetic assembly, out[L, 3] fp32 (Angstrom).
+ * Chains of `per_chain` atoms (residues of `per_res` atoms) are random walks:
+ * residue r sits 3.8 A from residue r-1 along the direction of a normal vector;
+ * each chain is centred on its mean and moved to point c of a Fibonacci sphere
+ * of radius 12 * sqrt(n_chains) A (neighbouring chains touch); atoms scatter
+ * around their residue with N(0, 1.5 A) per axis. Normals: direction noise normal(key, (c * n_res + r) * 3 + axis),
+ * atom offsets normal(key, 2^40 + 3 * atom + axis). Computed in fp64, stored
+ * rounded to fp32. */
+void synth_coords(uint64_t key, int64_t n_atoms, int32_t per_res, int32_t per_chain, float* out) {
+  const int64_t n_chains = (n_atoms + per_chain - 1) / per_chain;
+  const int64_t n_res = (per_chain + per_res - 1) / per_res;
+  const double radius = 12.0 * sqrt((double)n_chains);
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t c = 0; c < n_chains; ++c) {
+    double* res = (double*)malloc(sizeof(double) * (size_t)(3 * n_res));
+    double dir[3], p[3] = {0.0, 0.0, 0.0}, mean[3] = {0.0, 0.0, 0.0};
+    for (int64_t r = 0; r < n_res; ++r) {
+      double nd[3], nn = 0.0;
+      for (int a = 0; a < 3; ++a) {
+        nd[a] = (double)sm_normal(key, (uint64_t)((c * n_res + r) * 3 + a));
+        nn += nd[a] * nd[a];
+      }
+      nn = sqrt(nn);
+      for (int a = 0; a < 3; ++a) {
+        dir[a] = nd[a] / nn;
+        if (r > 0) p[a] += 3.8 * dir[a];
+        res[3 * r + a] = p[a];
+        mean[a] += p[a];
+      }
+    }
+    /* Fibonacci sphere point c of n_chains */
+    const double golden = 2.39996322972865332; /* pi (3 - sqrt 5) */
+    const double y = n_chains > 1 ? 1.0 - 2.0 * ((double)c + 0.5) / (double)n_chains : 0.0;
+    const double rr = sqrt(1.0 - y * y), th = golden * (double)c;
+    const double centre[3] = {radius * rr * cos(th), radius * y, radius * rr * sin(th)};
+    for (int64_t t = 0; t < per_chain; ++t) {
+      const int64_t atom = c * per_chain + t;
+      if (atom >= n_atoms) break;
+      const int64_t r = t / per_res;
+      for (int a = 0; a < 3; ++a) {
+        const double off = 1.5 * (double)sm_normal(key, (1ULL << 40) + (uint64_t)(3 * atom + a));
+        out[3 * atom + a] = (float)(res[3 * r + a] - mean[a] / (double)n_res + centre[a] + off);
+      }
+    }
+    free(res);
   }
 }

@@ -14,6 +14,11 @@ library ``oracle._lib`` currently holds) disagrees with:
   equivariance, a masked key equals a deleted one);
 * brute force at 40 significant digits on tiny inputs (mpmath).
 
+The k-nearest-neighbour search is pinned to a hand-worked golden file (atoms
+on a line), numpy brute force in fp32 with lexicographic (d2, index) order,
+integer-lattice ties, the blocked ring merge, merge properties, group modes,
+short lists and relabelling.
+
 The sparse (kNN) atom attention has its own pins: torch's SDPA over each
 query's gathered keys, the dense pipeline when every atom is a neighbour,
 closed forms (one neighbour atom in every slot, all slots empty), slot
@@ -573,6 +578,111 @@ def pin_sparse_bruteforce_mpmath():
                     num = mpmath.fsum(x * lin(Wv, A[j])[hh * d + e] for j, x in wts)
                     ref = gi[hh * d + e] * num / den
                     assert abs(float(ref) - got[r, hh * d + e]) <= 1e-13 * max(1.0, abs(float(ref))), (seed, r, hh, e)
+
+
+# ----------------------------------------------------------------------------- k nearest neighbours
+def _knn_numpy(x_q, x_c, k, keep=None):
+    """Brute force: squared distances in fp32 numpy arithmetic (each operation
+    rounded), candidates sorted by (d2, index)."""
+    out_i = np.full((len(x_q), k), -1, dtype=np.int32)
+    out_d = np.full((len(x_q), k), np.inf, dtype=np.float32)
+    for r, q in enumerate(np.asarray(x_q, dtype=np.float32)):
+        d = np.asarray(x_c, dtype=np.float32) - q[None, :]
+        d2 = (d[:, 0] * d[:, 0] + d[:, 1] * d[:, 1]) + d[:, 2] * d[:, 2]
+        j = np.arange(len(x_c))
+        if keep is not None:
+            m = keep(r)
+            d2, j = d2[m], j[m]
+        order = np.lexsort((j, d2))[:k]
+        out_i[r, :len(order)] = j[order]
+        out_d[r, :len(order)] = d2[order]
+    return out_i, out_d
+
+
+def _coords(seed, n, scale=10.0):
+    return (_rng(seed).standard_normal((n, 3)) * scale).astype(np.float32)
+
+
+def pin_knn_golden_line():
+    with open(os.path.join(GOLDEN, "knn_line.txt")) as f:
+        for line in f:
+            if not line.strip() or line.startswith("#"):
+                continue
+            pos, q, k, want = (part.split() for part in line.split("|"))
+            x = np.zeros((len(pos), 3), dtype=np.float32)
+            x[:, 0] = [float(p) for p in pos]
+            q, k = int(q[0]), int(k[0])
+            idx, d2 = oracle.knn(x[q:q + 1], x, k)
+            assert idx[0].tolist() == [int(w) for w in want], (line, idx[0])
+            for t, w in enumerate(int(w) for w in want):
+                assert d2[0, t] == ((x[w, 0] - x[q, 0]) ** 2 if w >= 0 else np.inf)
+
+
+def pin_knn_numpy_bruteforce():
+    for seed, n, k in ((60, 300, 16), (61, 1000, 128), (62, 40, 64)):
+        x = _coords(seed, n)
+        q = np.arange(0, n, 7)
+        idx, d2 = oracle.knn(x[q], x, k)
+        ri, rd = _knn_numpy(x[q], x, k)
+        assert np.array_equal(idx, ri) and np.array_equal(d2, rd), seed
+
+
+def pin_knn_ties_by_index():
+    """Many equal distances (integer lattice): ties go to the smaller index."""
+    g = np.stack(np.meshgrid(np.arange(4), np.arange(4), np.arange(4), indexing="ij"), -1).reshape(-1, 3)
+    x = g.astype(np.float32)
+    perm = _rng(63).permutation(len(x))
+    x = x[perm]
+    idx, d2 = oracle.knn(x, x, 20)
+    ri, rd = _knn_numpy(x, x, 20)
+    assert np.array_equal(idx, ri) and np.array_equal(d2, rd)
+
+
+def pin_knn_blocked_ring_merge():
+    x = _coords(64, 500)
+    q = np.arange(3, 500, 11)
+    base = oracle.knn(x[q], x, 32)
+    for nb in (2, 3, 7, 64):
+        got = oracle.knn(x[q], x, 32, n_blocks=nb)
+        assert np.array_equal(got[0], base[0]) and np.array_equal(got[1], base[1]), nb
+
+
+def pin_knn_merge_properties():
+    x = _coords(65, 200)
+    q = x[:9]
+    a = oracle.knn(q, x[:80], 24, c_index0=0)
+    b = oracle.knn(q, x[80:], 24, c_index0=80)
+    m = oracle.topk_merge(*a, *b)
+    full = _knn_numpy(q, x, 24)
+    assert np.array_equal(m[0], full[0]) and np.array_equal(m[1], full[1])
+    m2 = oracle.topk_merge(*b, *a)
+    assert np.array_equal(m2[0], m[0])
+    empty = (np.full_like(a[0], -1), np.full_like(a[1], np.inf))
+    e = oracle.topk_merge(*a, *empty)
+    assert np.array_equal(e[0], a[0]) and np.array_equal(e[1], a[1])
+
+
+def pin_knn_groups():
+    x = _coords(66, 400)
+    grp = (np.arange(400) // 50).astype(np.int32)
+    q = np.arange(5, 400, 13)
+    for mode, keep in ((1, lambda r: grp == grp[q[r]]), (2, lambda r: grp != grp[q[r]])):
+        idx, d2 = oracle.knn(x[q], x, 30, group_q=grp[q], group_c=grp, group_mode=mode)
+        ri, rd = _knn_numpy(x[q], x, 30, keep=keep)
+        assert np.array_equal(idx, ri) and np.array_equal(d2, rd), mode
+
+
+def pin_knn_short_lists_and_permutation():
+    x = _coords(67, 12)
+    idx, d2 = oracle.knn(x, x, 20)
+    assert (idx[:, 12:] == -1).all() and np.isinf(d2[:, 12:]).all()
+    assert sorted(idx[0, :12].tolist()) == list(range(12)) and idx[0, 0] == 0
+    # relabelling the candidates relabels the answer (no ties in random data)
+    y = _coords(68, 300)
+    perm = _rng(69).permutation(300)
+    a = oracle.knn(y[:10], y, 25)[0]
+    b = oracle.knn(y[:10], y[perm], 25)[0]
+    assert np.array_equal(perm[b], a)
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -206,3 +206,36 @@ def test_sparse_bad_arguments():
     # an f32 call accepts any c_atom and unaligned weights
     assert sparse(sparse_shape(act_dtype=dcp.DCP_F32, c_atom=100), ws_bytes=1000) == W
     assert sparse(sh, n_q=0, ws=None) == dcp.DCP_OK  # no-op
+
+
+# ----------------------------------------------------------------------------- k nearest neighbours
+def knn(x_q=FAKE, n_q=100, x_c=FAKE, n_c=1000, c0=0, self0=-1, gq=None, gc=None, mode=0, k=128, idx=FAKE, d2=FAKE):
+    return dcp.lib().dcp_knn_topk(x_q, n_q, x_c, n_c, c0, self0, gq, gc, mode, k, idx, d2, None)
+
+
+def test_knn_bad_arguments():
+    E, U = dcp.DCP_ERR_INVALID_ARGUMENT, dcp.DCP_ERR_UNSUPPORTED
+    assert knn(k=0) == E
+    assert knn(k=257) == U
+    assert knn(n_q=-1) == E
+    assert knn(n_c=-1) == E
+    assert knn(c0=-1) == E
+    assert knn(c0=2**31 - 100, n_c=1000) == E     # indices past int32
+    assert knn(mode=3) == E
+    assert knn(mode=1) == E                        # groups required
+    assert knn(x_q=None) == E
+    assert knn(x_c=None) == E
+    assert knn(idx=None) == E
+    assert knn(x_q=FAKE + 2) == E                  # misaligned
+    assert knn(n_q=0) == dcp.DCP_OK                # no-op
+    assert len(dcp.dcp_last_error()) == 0
+
+
+def test_topk_merge_bad_arguments():
+    E = dcp.DCP_ERR_INVALID_ARGUMENT
+    L = dcp.lib()
+    assert L.dcp_topk_merge(10, 0, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == E
+    assert L.dcp_topk_merge(10, 300, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == dcp.DCP_ERR_UNSUPPORTED
+    assert L.dcp_topk_merge(-1, 8, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == E
+    assert L.dcp_topk_merge(10, 8, FAKE, None, FAKE, FAKE, FAKE, FAKE, None) == E
+    assert L.dcp_topk_merge(0, 8, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == dcp.DCP_OK

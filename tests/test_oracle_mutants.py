@@ -56,6 +56,14 @@ MUTANTS = [
      "out[r * hd + h * d + e] = o;"),
     ("sparse query from key weights", "oracle_linear(1, c_atom, hd, ai, w_q, q);",
      "oracle_linear(1, c_atom, hd, ai, w_k, q);"),
+    ("knn ties by larger index", "return a.d2 < b.d2 || (a.d2 == b.d2 && a.j < b.j);",
+     "return a.d2 < b.d2 || (a.d2 == b.d2 && a.j > b.j);"),
+    ("knn distance summed in another order", "const float s = xx + yy;\n  return s + zz;",
+     "const float s = yy + zz;\n  return xx + s;"),
+    ("knn group mode inverted", "if (group_mode == 1 && group_c[j] != group_q[r]) continue;",
+     "if (group_mode == 1 && group_c[j] == group_q[r]) continue;"),
+    ("knn merge drops the second list", "      if (idx_b[r * k + t] >= 0) {", "      if (0) {"),
+    ("knn block offset lost", "keys[n].j = c_index0 + j;", "keys[n].j = j;"),
 ]
 
 RUNNER = r"""
