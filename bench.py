@@ -378,7 +378,7 @@ def knn_main(args, wl):
         "dtype": "f32",
         "data": "synthetic (seeded chains of residues placed on a sphere; stands in for RFD3 assembly coordinates)",
         "config": {"workload": wl.name, "n_atoms": L, "q_row0": wl.q_row0, "n_q": n_q, "k": k,
-                   "candidate_pairs": pairs},
+                   "candidate_pairs": pairs, "calibration_bytes": cal},
         "roofline": {"bound": "alu", "achieved": round(achieved, 2), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_FP32_TFLOPS, 4),
                      "traffic": stored_traffic(wl.name, KNN_SOURCES), "kernel": "knn_kernel",

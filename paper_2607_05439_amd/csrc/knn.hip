@@ -134,23 +134,24 @@ __global__ void __launch_bounds__(64 * kKnnWaves) knn_kernel(KnnArgs a) {
     }
     __syncthreads();
     if (!active) continue;
-    for (int s = 0; s < n_here; s += 64) {
+    // 64 candidates per step, no branch on the tile tail: lanes past n_here
+    // read stale LDS (inside the tile) and are masked out of `take`
+    auto step = [&](int s) {
       const int i = s + lane;
-      bool take = false;
-      uint64_t key = kNoKey;
-      if (i < n_here) {
+      float d2;
+      {
         // the distance is part of the definition: each operation rounded, in
         // this order, never fused into multiply-adds
 #pragma clang fp contract(off)
         const float dx = qx - s_x[i], dy = qy - s_y[i], dz = qz - s_z[i];
-        const float d2 = (dx * dx + dy * dy) + dz * dz;
-        key = ((uint64_t)__float_as_uint(d2) << 32) | (uint32_t)(a.c_index0 + c0 + i);
-        take = key < tau;
-        if constexpr (MODE == 1) take = take && s_g[i] == qg;
-        if constexpr (MODE == 2) take = take && s_g[i] != qg;
+        d2 = (dx * dx + dy * dy) + dz * dz;
       }
+      const uint64_t key = ((uint64_t)__float_as_uint(d2) << 32) | (uint32_t)(a.c_index0 + c0 + i);
+      bool take = key < tau && i < n_here;
+      if constexpr (MODE == 1) take = take && s_g[i] == qg;
+      if constexpr (MODE == 2) take = take && s_g[i] != qg;
       const uint64_t mask = __ballot(take);
-      if (mask == 0) continue;
+      if (mask == 0) return;
       const int n_new = __popcll(mask);
       if (bcount + n_new > 64) flush();
       const int pos = bcount + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
@@ -158,6 +159,10 @@ __global__ void __launch_bounds__(64 * kKnnWaves) knn_kernel(KnnArgs a) {
       if (take) buf[pos] = key;
       wave_lds_sync();
       bcount += n_new;
+    };
+    for (int s = 0; s < n_here; s += 128) {
+      step(s);
+      if (s + 64 < n_here) step(s + 64);
     }
   }
   if (!active) return;
