@@ -31,10 +31,12 @@ def _configure(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.oracle_sparse_attention.argtypes = [i64, i32, i32, i32, i32, i32, vp, vp, i32, vp, vp, i64,
                                             vp, vp, vp, vp, vp, vp, vp, vp, f64, i32, vp]
     lib.oracle_knn.argtypes = [vp, i64, vp, i64, i64, vp, vp, i32, i32, vp, vp]
+    lib.oracle_transition.argtypes = [i64, i32, i32, vp, i32, vp, vp, vp, vp, vp, f64, vp]
     lib.oracle_topk_merge.argtypes = [i64, i32, vp, vp, vp, vp, vp, vp]
     lib.oracle_knn_blocked.argtypes = [vp, i64, vp, i64, vp, vp, i32, i32, i32, vp, vp]
     for f in (lib.oracle_bias, lib.oracle_attend, lib.oracle_merge, lib.oracle_attention,
-              lib.oracle_sparse_attention, lib.oracle_knn, lib.oracle_topk_merge, lib.oracle_knn_blocked):
+              lib.oracle_sparse_attention, lib.oracle_knn, lib.oracle_topk_merge, lib.oracle_knn_blocked,
+              lib.oracle_transition):
         f.restype = ctypes.c_int
     return lib
 
@@ -225,3 +227,18 @@ def topk_merge(idx_a, d2_a, idx_b, d2_b) -> Tuple[np.ndarray, np.ndarray]:
     if rc != 0:
         raise ValueError("oracle_topk_merge rejected its arguments")
     return io, do
+
+
+def transition(z: np.ndarray, w1: np.ndarray, w2: np.ndarray, w3: np.ndarray, gamma=None, beta=None,
+               eps: float = 1e-5) -> np.ndarray:
+    """z + W3 (SiLU(W1 LN(z)) * W2 LN(z)) per pair; z [..., c_z] fp32 or bf16 bits; fp64 result."""
+    zb, dt = _zbuf(z)
+    c_z = zb.shape[-1]
+    n = zb.size // c_z
+    hidden = np.asarray(w1).shape[0]
+    out = np.empty(zb.shape, dtype=np.float64)
+    keep = [_f64(a) for a in (w1, w2, w3, gamma, beta)]  # alive until the call returns
+    rc = _load().oracle_transition(n, c_z, hidden, zb.ctypes.data, dt, *[_p(a) for a in keep], eps, _p(out))
+    if rc != 0:
+        raise ValueError("oracle_transition rejected its arguments")
+    return out

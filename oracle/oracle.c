@@ -554,3 +554,55 @@ int oracle_knn_blocked(const float* x_q, int64_t n_q, const float* x_c, int64_t 
   free(rd);
   return 0;
 }
+
+/* ---------------------------------------------------------------------------
+ * Pair transition (Appendix "Manual SwiGLU decomposition", Eq. for
+ * Transition(Z) and Alg. alg:swiglu-decomp): the SwiGLU feed-forward update of
+ * the pair track with its residual,
+ *   N = LayerNorm(z),  A = W1 N,  B = W2 N,  T = W3 (SiLU(A) * B),  z <- z + T,
+ * SiLU(a) = a / (1 + exp(-a)), W1, W2: c_z -> hidden, W3: hidden -> c_z
+ * (nn.Linear layout [out, in], no bias), evaluated per pair; the LayerNorm
+ * is the one read for the attention bias (biased variance, eps inside the
+ * square root, affine gamma and beta; NULL = 1 and 0).
+ * z: [n_pairs, c_z] fp32 (dtype 0) or bf16 (1); out: [n_pairs, c_z] fp64.
+ * ------------------------------------------------------------------------- */
+int oracle_transition(int64_t n_pairs, int c_z, int hidden, const void* z, int dtype, const double* w1, const double* w2,
+                      const double* w3, const double* gamma, const double* beta, double eps, double* out) {
+  if (!z || !w1 || !w2 || !w3 || !out || c_z <= 0 || hidden <= 0) return -1;
+#pragma omp parallel
+  {
+    double* x = (double*)malloc(sizeof(double) * (size_t)c_z);
+    double* n = (double*)malloc(sizeof(double) * (size_t)c_z);
+    double* h = (double*)malloc(sizeof(double) * (size_t)hidden);
+#pragma omp for schedule(static)
+    for (int64_t p = 0; p < n_pairs; ++p) {
+      double mu = 0.0, var = 0.0;
+      for (int c = 0; c < c_z; ++c) {
+        x[c] = load_elem(z, dtype, p * c_z + c);
+        mu += x[c];
+      }
+      mu /= c_z;
+      for (int c = 0; c < c_z; ++c) var += (x[c] - mu) * (x[c] - mu);
+      var /= c_z;
+      const double inv = 1.0 / sqrt(var + eps);
+      for (int c = 0; c < c_z; ++c) n[c] = (gamma ? gamma[c] : 1.0) * ((x[c] - mu) * inv) + (beta ? beta[c] : 0.0);
+      for (int u = 0; u < hidden; ++u) {
+        double a = 0.0, b = 0.0;
+        for (int c = 0; c < c_z; ++c) {
+          a += w1[(int64_t)u * c_z + c] * n[c];
+          b += w2[(int64_t)u * c_z + c] * n[c];
+        }
+        h[u] = a / (1.0 + exp(-a)) * b;
+      }
+      for (int c = 0; c < c_z; ++c) {
+        double t = 0.0;
+        for (int u = 0; u < hidden; ++u) t += w3[(int64_t)c * hidden + u] * h[u];
+        out[p * c_z + c] = x[c] + t;
+      }
+    }
+    free(x);
+    free(n);
+    free(h);
+  }
+  return 0;
+}

@@ -19,6 +19,10 @@ on a line), numpy brute force in fp32 with lexicographic (d2, index) order,
 integer-lattice ties, the blocked ring merge, merge properties, group modes,
 short lists and relabelling.
 
+The pair transition is pinned to its torch composition (layer_norm, linear,
+silu), zero-branch and scaling closed forms, the LayerNorm shift, and brute
+force at 40 digits.
+
 The sparse (kNN) atom attention has its own pins: torch's SDPA over each
 query's gathered keys, the dense pipeline when every atom is a neighbour,
 closed forms (one neighbour atom in every slot, all slots empty), slot
@@ -683,6 +687,90 @@ def pin_knn_short_lists_and_permutation():
     a = oracle.knn(y[:10], y, 25)[0]
     b = oracle.knn(y[:10], y[perm], 25)[0]
     assert np.array_equal(perm[b], a)
+
+
+# ----------------------------------------------------------------------------- pair transition
+def _transition_case(seed=0, n=7, c_z=6, hidden=10, affine=True):
+    r = _rng(seed)
+    z = (0.5 + r.standard_normal((n, c_z))).astype(np.float32)
+    w = {
+        "w1": (r.standard_normal((hidden, c_z)) / np.sqrt(c_z)).astype(np.float32),
+        "w2": (r.standard_normal((hidden, c_z)) / np.sqrt(c_z)).astype(np.float32),
+        "w3": (r.standard_normal((c_z, hidden)) / np.sqrt(hidden)).astype(np.float32),
+        "gamma": (1 + 0.3 * r.standard_normal(c_z)).astype(np.float32) if affine else None,
+        "beta": (0.4 * r.standard_normal(c_z)).astype(np.float32) if affine else None,
+    }
+    return z, w
+
+
+def pin_transition_torch():
+    """The update composed from torch's layer_norm, linear and silu (fp64)."""
+    for seed, kw in ((70, {}), (71, dict(n=20, c_z=16, hidden=64)), (72, dict(affine=False))):
+        z, w = _transition_case(seed, **kw)
+        got = oracle.transition(z, w["w1"], w["w2"], w["w3"], w["gamma"], w["beta"])
+        t = lambda a: None if a is None else torch.from_numpy(np.asarray(a, dtype=np.float64))
+        Z = t(z)
+        N = F.layer_norm(Z, (Z.shape[-1],), t(w["gamma"]), t(w["beta"]), 1e-5)
+        ref = (Z + F.linear(F.silu(F.linear(N, t(w["w1"]))) * F.linear(N, t(w["w2"])), t(w["w3"]))).numpy()
+        assert _rel(got, ref) <= 1e-13, seed
+
+
+def pin_transition_zero_branches():
+    """W1 = 0 (SiLU(0) = 0), W2 = 0 or W3 = 0: the update is the identity."""
+    z, w = _transition_case(73)
+    for name in ("w1", "w2", "w3"):
+        ww = dict(w)
+        ww[name] = np.zeros_like(w[name])
+        got = oracle.transition(z, ww["w1"], ww["w2"], ww["w3"], ww["gamma"], ww["beta"])
+        assert np.array_equal(got, z.astype(np.float64)), name
+
+
+def pin_transition_silu_branch_and_scaling():
+    """SiLU sits on the W1 branch (swapping W1 and W2 changes the result), and
+    T is linear in W3 and in W2 (scaling either by 2 doubles T)."""
+    z, w = _transition_case(74)
+    base = oracle.transition(z, w["w1"], w["w2"], w["w3"], w["gamma"], w["beta"]) - z
+    swapped = oracle.transition(z, w["w2"], w["w1"], w["w3"], w["gamma"], w["beta"]) - z
+    assert _rel(swapped, base) > 1e-3
+    for name in ("w2", "w3"):
+        ww = dict(w)
+        ww[name] = 2 * w[name]
+        got = oracle.transition(z, ww["w1"], ww["w2"], ww["w3"], ww["gamma"], ww["beta"]) - z
+        assert _rel(got, 2 * base) <= 1e-13, name
+
+
+def pin_transition_layernorm_shift():
+    """LN(z + c) = LN(z): adding a constant to every channel of a pair adds
+    exactly that constant to the output."""
+    z, w = _transition_case(75, affine=True)
+    z = (np.round(z * 64) / 64).astype(np.float32)  # on a grid where z + 3 is exact in fp32
+    a = oracle.transition(z, w["w1"], w["w2"], w["w3"], w["gamma"], w["beta"])
+    b = oracle.transition(z + np.float32(3.0), w["w1"], w["w2"], w["w3"], w["gamma"], w["beta"])
+    assert np.max(np.abs((b - 3.0) - a)) <= 1e-9
+
+
+def pin_transition_bruteforce_mpmath():
+    mpmath.mp.dps = 40
+    z, w = _transition_case(76, n=3, c_z=4, hidden=5)
+    got = oracle.transition(z, w["w1"], w["w2"], w["w3"], w["gamma"], w["beta"])
+    M = lambda a: [[mpmath.mpf(float(x)) for x in row] for row in np.atleast_2d(a)]
+    W1, W2, W3 = M(w["w1"]), M(w["w2"]), M(w["w3"])
+    gam = [mpmath.mpf(float(x)) for x in w["gamma"]]
+    bet = [mpmath.mpf(float(x)) for x in w["beta"]]
+    eps = mpmath.mpf(1e-5)
+    for p in range(3):
+        x = [mpmath.mpf(float(v)) for v in z[p]]
+        mu = mpmath.fsum(x) / 4
+        var = mpmath.fsum((v - mu) ** 2 for v in x) / 4
+        nn = [gam[c] * (x[c] - mu) / mpmath.sqrt(var + eps) + bet[c] for c in range(4)]
+        h = []
+        for u in range(5):
+            a = mpmath.fsum(W1[u][c] * nn[c] for c in range(4))
+            b = mpmath.fsum(W2[u][c] * nn[c] for c in range(4))
+            h.append(a / (1 + mpmath.exp(-a)) * b)
+        for c in range(4):
+            ref = x[c] + mpmath.fsum(W3[c][u] * h[u] for u in range(5))
+            assert abs(float(ref) - got[p, c]) <= 1e-13 * max(1.0, abs(float(ref))), (p, c)
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -64,6 +64,12 @@ MUTANTS = [
      "if (group_mode == 1 && group_c[j] == group_q[r]) continue;"),
     ("knn merge drops the second list", "      if (idx_b[r * k + t] >= 0) {", "      if (0) {"),
     ("knn block offset lost", "keys[n].j = c_index0 + j;", "keys[n].j = j;"),
+    ("transition silu without the input", "h[u] = a / (1.0 + exp(-a)) * b;", "h[u] = 1.0 / (1.0 + exp(-a)) * b;"),
+    ("transition gate on the other branch", "h[u] = a / (1.0 + exp(-a)) * b;", "h[u] = b / (1.0 + exp(-b)) * a;"),
+    ("transition residual dropped", "out[p * c_z + c] = x[c] + t;", "out[p * c_z + c] = t;"),
+    ("transition beta dropped", "((x[c] - mu) * inv) + (beta ? beta[c] : 0.0);", "((x[c] - mu) * inv);"),
+    ("transition w3 transposed", "t += w3[(int64_t)c * hidden + u] * h[u];",
+     "t += w3[(int64_t)(u % c_z) * hidden + (c % hidden)] * h[u];"),
 ]
 
 RUNNER = r"""
