@@ -33,6 +33,9 @@ SPARSE_METRIC = "ms/layer + gathered GB/s for sparse kNN pair-biased atom attent
 KNN_SOURCES = ("paper_2607_05439_amd/csrc/knn.hip",)
 KNN_METRIC = "ms per kNN search + candidate pairs/s for the chunked k-nearest-neighbour top-k"
 PEAK_FP32_TFLOPS = 157.3  # MI355X fp32 vector, published
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 matrix cores, published
+TRANS_SOURCES = ("paper_2607_05439_amd/csrc/transition.hip", "paper_2607_05439_amd/csrc/cdna4.h")
+TRANS_METRIC = "ms per pair transition (LayerNorm + SwiGLU + residual) + matrix-core TFLOP/s"
 
 
 def progress(msg):
@@ -388,6 +391,105 @@ def knn_main(args, wl):
     print(json.dumps(line), flush=True)
 
 
+def transition_main(args, name):
+    import numpy as np
+    import torch
+    import paper_2607_05439_amd as dcp
+    import oracle
+    import synth
+
+    wl, hidden = synth.transition_workload(name)
+    dev = torch.device("cuda:0")
+    sp = torch.cuda.current_stream().cuda_stream
+    n, c_z = wl.n_tok, wl.c_z
+    n_pairs = n * n
+    progress(f"workload {name}: z[{n}, {n}, {c_z}] {wl.dtype} in place ({n_pairs * c_z * wl.elem_bytes / 1e9:.1f} GB), "
+             f"hidden {hidden}")
+    dtype = dcp.DCP_BF16 if wl.bf16 else dcp.DCP_F32
+    z = torch.empty((n, n, c_z), dtype=torch.bfloat16 if wl.bf16 else torch.float32, device=dev)
+    synth.z_fill_device(wl, z.data_ptr(), 0, n, sp)
+    w_host = synth.transition_weights(wl, hidden)
+    w = {k: (None if v is None else torch.from_numpy(v).to(dev)) for k, v in w_host.items()}
+    ws_bytes = dcp.dcp_transition_workspace_size(c_z, hidden, dtype)
+    ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+    hip = Hip()
+
+    def step(evs=None):
+        if evs is not None:
+            dcp.dcp_set_timing_events(*evs)
+        dcp.dcp_pair_transition(n_pairs, c_z, hidden, dtype, 1e-5, w["w1"], w["w2"], w["w3"], w["gamma"], w["beta"],
+                                z, z, ws, ws.numel(), sp)
+        if evs is not None:
+            dcp.dcp_set_timing_events(None, None)
+
+    cal = min(args.calibrate_bytes, z.numel() * z.element_size() // 2 // 16 * 16)
+    scratch = torch.empty(cal, dtype=torch.uint8, device=dev)
+    synth.device_copy(z.data_ptr(), scratch.data_ptr(), cal, sp)
+    torch.cuda.synchronize()
+    del scratch
+    progress(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(hip.event(), hip.event()) for _ in range(args.steps)]
+    t_start, t_stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    progress(f"timing {args.steps} steps")
+    t_start.record()
+    for i in range(args.steps):
+        step(evs[i])
+    t_stop.record()
+    torch.cuda.synchronize()
+    ms_per_step = t_start.elapsed_time(t_stop) / args.steps
+    kms = sum(hip.elapsed_ms(a, b) for a, b in evs) / len(evs)
+    flops = 6.0 * c_z * hidden * n_pairs  # W1, W2 (2 c_z hidden each) and W3 (2 hidden c_z) per pair
+    hbm = 2.0 * n_pairs * c_z * wl.elem_bytes  # z read once, written once
+    achieved = flops / (kms * 1e-3) / 1e12
+    progress(f"{ms_per_step:.2f} ms per transition (weights + kernel {kms:.2f} ms): {achieved:.0f} TFLOP/s "
+             f"({achieved / PEAK_BF16_TFLOPS:.1%} of dense bf16), z stream {hbm / (kms * 1e-3) / 1e9:.0f} GB/s")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        progress(f"cpu baseline: oracle on sampled pairs (~{args.cpu_seconds:.0f} s)")
+        threads = ctypes.CDLL("libgomp.so.1").omp_get_max_threads()
+        zs = synth.z_host(wl, [0, n // 2])[:, :, :].reshape(-1, c_z)
+        m = min(len(zs), 64 * threads)
+        t0 = time.perf_counter()
+        oracle.transition(zs[:m], w_host["w1"], w_host["w2"], w_host["w3"])
+        per_pair = (time.perf_counter() - t0) / m
+        m = int(min(len(zs), max(m, args.cpu_seconds / per_pair)))
+        t0 = time.perf_counter()
+        oracle.transition(zs[:m], w_host["w1"], w_host["w2"], w_host["w3"])
+        t_run = time.perf_counter() - t0
+        t_full = t_run / m * n_pairs
+        cpu = {"value": round(flops / t_full / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+               "sample": f"{m} of {n_pairs} pairs in {t_run:.1f} s (fp64); extrapolated transition time "
+                         f"{t_full:.0f} s",
+               "ms_per_transition_extrapolated": round(t_full * 1e3, 1)}
+    line = {
+        "metric": TRANS_METRIC,
+        "value": round(achieved, 1),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.bf16 else "f32",
+        "data": "synthetic (seeded; the same pair tensor as the attention workload)",
+        "config": {"workload": name, "n_tokens": n, "c_z": c_z, "hidden": hidden, "pairs": n_pairs,
+                   "z_bytes": n_pairs * c_z * wl.elem_bytes, "calibration_bytes": cal},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": stored_traffic(name, TRANS_SOURCES), "kernel": "trans_kernel",
+                     "kernel_ms": round(kms, 4), "algorithmic_flops_per_launch": flops,
+                     "hbm_GBps": round(hbm / (kms * 1e-3) / 1e9, 1)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -414,6 +516,8 @@ def main():
         return sparse_main(args, synth.ATOM_WORKLOADS[args.workload])
     if args.workload in synth.KNN_WORKLOADS:
         return knn_main(args, synth.KNN_WORKLOADS[args.workload])
+    if args.workload in synth.TRANSITION_WORKLOADS:
+        return transition_main(args, args.workload)
     wl = synth.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()

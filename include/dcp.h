@@ -253,10 +253,38 @@ int dcp_knn_topk(const float* x_q, int64_t n_q, const float* x_c, int64_t n_c, i
 int dcp_topk_merge(int64_t n_rows, int32_t k, const int32_t* idx_a, const float* d2_a, const int32_t* idx_b,
                    const float* d2_b, int32_t* idx_out, float* d2_out, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Pair transition (Appendix "Manual SwiGLU decomposition"): the SwiGLU
+ * feed-forward update of the pair track with its residual, per pair,
+ *   N = LayerNorm(z),  z <- z + W3 (SiLU(W1 N) * W2 N),  SiLU(a) = a / (1 + e^-a),
+ * W1, W2: [hidden, c_z], W3: [c_z, hidden] (fp32, nn.Linear layout, no bias);
+ * LayerNorm over c_z with optional gamma, beta ([c_z] fp32, NULL = 1 / 0),
+ * biased variance, eps inside the square root.
+ * ------------------------------------------------------------------------- */
+
+/* Workspace bytes for dcp_pair_transition (written to *bytes). Host-only. */
+int dcp_transition_workspace_size(int32_t c_z, int32_t hidden, int32_t act_dtype, size_t* bytes);
+
+/* The transition of n_pairs consecutive pairs z[n_pairs, c_z] (any stripe of
+ * rows of a contiguous pair tensor). z_out may equal z_in (in place) or must
+ * not overlap it; both 16-byte aligned, act_dtype.
+ * act_dtype = BF16: c_z = 128 and hidden = 512 only; the weights (gamma folded
+ * into W1 and W2, beta into per-unit biases), the normalised pair vector and
+ * SiLU(A) * B enter the matrix cores as bf16 with fp32 accumulation; the
+ * result is rounded to bf16. Needs dcp_transition_workspace_size() bytes of
+ * workspace (256-byte aligned; prepared weights, rewritten on every call).
+ * act_dtype = F32: c_z <= 256, hidden <= 1024, fp32 throughout, no workspace
+ * (workspace may be NULL). n_pairs = 0 is a no-op. */
+int dcp_pair_transition(int64_t n_pairs, int32_t c_z, int32_t hidden, int32_t act_dtype, float ln_eps,
+                        const float* w1, const float* w2, const float* w3, const float* ln_gamma,
+                        const float* ln_beta, const void* z_in, void* z_out, void* workspace, size_t workspace_bytes,
+                        void* stream);
+
 /* Optional timing hook: when both are non-NULL hipEvent_t handles, the calling
- * thread's next dcp_pair_bias_attention, dcp_sparse_pair_bias_attention and
- * dcp_knn_topk calls record `start` just before and `stop` just after the
- * attention (or kNN) kernel, after any projections, on that call's stream. Pass NULL, NULL to clear.
+ * thread's next dcp_pair_bias_attention, dcp_sparse_pair_bias_attention,
+ * dcp_knn_topk and dcp_pair_transition calls record `start` just before and
+ * `stop` just after the main kernel (after any projections; around the
+ * weight preparation and the transition kernel), on that call's stream. Pass NULL, NULL to clear.
  * Host-only. */
 int dcp_set_timing_events(void* start_event, void* stop_event);
 

@@ -4,7 +4,8 @@ Every step of the computation runs in the library's HIP kernels; PyTorch is
 used for device memory and streams. The functions carry the C names
 (``dcp_pair_bias_attention``, ``dcp_bias_project``, ``dcp_block_merge``,
 ``dcp_workspace_size``, ``dcp_sparse_pair_bias_attention``,
-``dcp_sparse_workspace_size``, ``dcp_knn_topk``, ``dcp_topk_merge``) and accept torch tensors (device pointers are taken
+``dcp_sparse_workspace_size``, ``dcp_knn_topk``, ``dcp_topk_merge``,
+``dcp_pair_transition``, ``dcp_transition_workspace_size``) and accept torch tensors (device pointers are taken
 from ``data_ptr()``) or plain integer addresses. Loading fails loudly when the
 library has not been built: there is no fallback.
 """
@@ -21,7 +22,7 @@ DCP_F32, DCP_BF16 = 0, 1
 DCP_OK, DCP_ERR_INVALID_ARGUMENT, DCP_ERR_UNSUPPORTED, DCP_ERR_WORKSPACE, DCP_ERR_HIP = 0, -1, -2, -3, -4
 EXPORTS = ("dcp_workspace_size", "dcp_pair_bias_attention", "dcp_bias_project", "dcp_block_merge",
            "dcp_sparse_workspace_size", "dcp_sparse_pair_bias_attention", "dcp_knn_topk", "dcp_topk_merge",
-           "dcp_set_timing_events",
+           "dcp_transition_workspace_size", "dcp_pair_transition", "dcp_set_timing_events",
            "dcp_last_error", "dcp_version")
 
 
@@ -68,10 +69,12 @@ def lib() -> ctypes.CDLL:
                                                      vp, sz, vp]
         L.dcp_knn_topk.argtypes = [vp, i64, vp, i64, i64, i64, vp, vp, i32, i32, vp, vp, vp]
         L.dcp_topk_merge.argtypes = [i64, i32, vp, vp, vp, vp, vp, vp, vp]
+        L.dcp_transition_workspace_size.argtypes = [i32, i32, i32, P(sz)]
+        L.dcp_pair_transition.argtypes = [i64, i32, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.dcp_set_timing_events.argtypes = [vp, vp]
         for f in (L.dcp_workspace_size, L.dcp_pair_bias_attention, L.dcp_bias_project, L.dcp_block_merge,
                   L.dcp_sparse_workspace_size, L.dcp_sparse_pair_bias_attention, L.dcp_knn_topk, L.dcp_topk_merge,
-                  L.dcp_set_timing_events):
+                  L.dcp_transition_workspace_size, L.dcp_pair_transition, L.dcp_set_timing_events):
             f.restype = ctypes.c_int
         L.dcp_last_error.restype = ctypes.c_char_p
         L.dcp_last_error.argtypes = []
@@ -173,6 +176,20 @@ def dcp_topk_merge(n_rows: int, k: int, idx_a: Ptr, d2_a: Ptr, idx_b: Ptr, d2_b:
                    stream=None) -> None:
     _check(lib().dcp_topk_merge(n_rows, k, _ptr(idx_a), _ptr(d2_a), _ptr(idx_b), _ptr(d2_b), _ptr(idx_out),
                                 _ptr(d2_out), _stream(stream)))
+
+
+def dcp_transition_workspace_size(c_z: int, hidden: int, act_dtype: int) -> int:
+    out = ctypes.c_size_t()
+    _check(lib().dcp_transition_workspace_size(c_z, hidden, act_dtype, ctypes.byref(out)))
+    return out.value
+
+
+def dcp_pair_transition(n_pairs: int, c_z: int, hidden: int, act_dtype: int, ln_eps: float, w1: Ptr, w2: Ptr, w3: Ptr,
+                        ln_gamma: Ptr, ln_beta: Ptr, z_in: Ptr, z_out: Ptr, workspace: Ptr, workspace_bytes: int,
+                        stream=None) -> None:
+    _check(lib().dcp_pair_transition(n_pairs, c_z, hidden, act_dtype, ln_eps, _ptr(w1), _ptr(w2), _ptr(w3),
+                                     _ptr(ln_gamma), _ptr(ln_beta), _ptr(z_in), _ptr(z_out), _ptr(workspace),
+                                     workspace_bytes, _stream(stream)))
 
 
 def dcp_set_timing_events(start_event: Optional[int], stop_event: Optional[int]) -> None:

@@ -611,4 +611,96 @@ int dcp_topk_merge(int64_t n_rows, int32_t k, const int32_t* idx_a, const float*
   return ok();
 }
 
+// ----------------------------------------------------------------------------- pair transition
+static int check_transition(int32_t c_z, int32_t hidden, int32_t act_dtype, bool* fast) {
+  if (c_z < 1 || hidden < 1) return fail(DCP_ERR_INVALID_ARGUMENT, "c_z and hidden must be >= 1");
+  if (act_dtype != DCP_F32 && act_dtype != DCP_BF16)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "act_dtype must be DCP_F32 or DCP_BF16");
+  if (act_dtype == DCP_BF16) {
+    if (c_z != dcp::kTransCz || hidden != dcp::kTransHidden)
+      return fail(DCP_ERR_UNSUPPORTED, "bf16 transition needs c_z = %d and hidden = %d (got %d, %d)", dcp::kTransCz,
+                  dcp::kTransHidden, c_z, hidden);
+    *fast = true;
+    return DCP_OK;
+  }
+  if (c_z > dcp::kGenMaxCz || hidden > dcp::kTransGenMaxHidden)
+    return fail(DCP_ERR_UNSUPPORTED, "fp32 transition needs c_z <= %d and hidden <= %d", dcp::kGenMaxCz,
+                dcp::kTransGenMaxHidden);
+  *fast = false;
+  return DCP_OK;
+}
+
+int dcp_transition_workspace_size(int32_t c_z, int32_t hidden, int32_t act_dtype, size_t* bytes) {
+  if (!bytes) return fail(DCP_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  bool fast;
+  const int rc = check_transition(c_z, hidden, act_dtype, &fast);
+  if (rc) return rc;
+  *bytes = fast ? round_up(dcp::trans_prep_bytes(), 256) : 0;
+  return ok();
+}
+
+int dcp_pair_transition(int64_t n_pairs, int32_t c_z, int32_t hidden, int32_t act_dtype, float ln_eps,
+                        const float* w1, const float* w2, const float* w3, const float* ln_gamma,
+                        const float* ln_beta, const void* z_in, void* z_out, void* workspace, size_t workspace_bytes,
+                        void* stream) {
+  bool fast;
+  int rc = check_transition(c_z, hidden, act_dtype, &fast);
+  if (rc) return rc;
+  if (n_pairs < 0) return fail(DCP_ERR_INVALID_ARGUMENT, "n_pairs must be >= 0");
+  if (!(ln_eps >= 0.0f) || !isfinite(ln_eps)) return fail(DCP_ERR_INVALID_ARGUMENT, "ln_eps must be finite and >= 0");
+  if (!w1 || !w2 || !w3) return fail(DCP_ERR_INVALID_ARGUMENT, "w1, w2 and w3 are required");
+  if (!z_in || !z_out) return fail(DCP_ERR_INVALID_ARGUMENT, "z_in and z_out are required");
+  if (n_pairs == 0) return ok();
+  if (!aligned(z_in, 16) || !aligned(z_out, 16))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "z_in and z_out must be 16-byte aligned");
+  const size_t zbytes = (size_t)n_pairs * c_z * (act_dtype == DCP_BF16 ? 2 : 4);
+  const char *zi = static_cast<const char*>(z_in), *zo = static_cast<const char*>(z_out);
+  if (zi != zo && zi < zo + zbytes && zo < zi + zbytes)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "z_out must equal z_in or not overlap it");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  if (fast) {
+    const size_t need = round_up(dcp::trans_prep_bytes(), 256);
+    if (!workspace || !aligned(workspace, 256))
+      return fail(DCP_ERR_WORKSPACE, "workspace must be a 256-byte aligned device pointer");
+    if (workspace_bytes < need)
+      return fail(DCP_ERR_WORKSPACE, "workspace too small: %zu bytes given, %zu needed", workspace_bytes, need);
+    dcp::TransArgs a{};
+    a.n_pairs = n_pairs;
+    a.w1 = w1;
+    a.w2 = w2;
+    a.w3 = w3;
+    a.gamma = ln_gamma;
+    a.beta = ln_beta;
+    a.z_in = z_in;
+    a.z_out = z_out;
+    a.w_prep = workspace;
+    a.b_prep = reinterpret_cast<float*>(static_cast<char*>(workspace) + (dcp::trans_prep_bytes() - 2 * dcp::kTransHidden * sizeof(float)));
+    a.eps = ln_eps;
+    if (g_ev_start && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_start), st)) != hipSuccess)
+      return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
+    e = dcp::launch_transition(a, st);
+  } else {
+    dcp::TransGenArgs a{};
+    a.n_pairs = n_pairs;
+    a.c_z = c_z;
+    a.hidden = hidden;
+    a.w1 = w1;
+    a.w2 = w2;
+    a.w3 = w3;
+    a.gamma = ln_gamma;
+    a.beta = ln_beta;
+    a.z_in = static_cast<const float*>(z_in);
+    a.z_out = static_cast<float*>(z_out);
+    a.eps = ln_eps;
+    if (g_ev_start && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_start), st)) != hipSuccess)
+      return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
+    e = dcp::launch_transition_gen(a, st);
+  }
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "transition launch failed: %s", hipGetErrorString(e));
+  if (g_ev_stop && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_stop), st)) != hipSuccess)
+    return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 }  // extern "C"

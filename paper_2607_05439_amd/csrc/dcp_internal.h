@@ -176,6 +176,33 @@ struct TopkMergeArgs {
   float* d2_out;
 };
 
+// Pair transition: the matrix-core path serves c_z = 128 with a 4x expansion;
+// the fp32 path c_z <= 256 and hidden <= 1024.
+constexpr int kTransCz = 128;
+constexpr int kTransHidden = 512;
+constexpr int kTransGenMaxHidden = 1024;
+
+struct TransArgs {
+  int64_t n_pairs;
+  const float *w1, *w2, *w3, *gamma, *beta;
+  const void* z_in;    // [n_pairs][128] bf16
+  void* z_out;         // may equal z_in
+  void* w_prep;        // operand tiles (trans_prep_bytes(): tiles then biases)
+  float* b_prep;       // [2][512] inside w_prep
+  float eps;
+};
+
+struct TransGenArgs {
+  int64_t n_pairs;
+  int32_t c_z, hidden;
+  const float *w1, *w2, *w3, *gamma, *beta;
+  const float* z_in;
+  float* z_out;        // may equal z_in
+  float eps;
+};
+
+size_t trans_prep_bytes();
+
 hipError_t launch_fast_proj(const FastProjArgs& a, hipStream_t st);
 hipError_t launch_fast_attn(const FastAttnArgs& a, hipStream_t st);
 hipError_t launch_fast_bias(const FastBiasArgs& a, hipStream_t st);
@@ -187,5 +214,7 @@ hipError_t launch_sparse_proj(const SparseProjArgs& a, hipStream_t st);
 hipError_t launch_sparse_attn(const SparseAttnArgs& a, bool bf16, hipStream_t st);
 hipError_t launch_knn(const KnnArgs& a, hipStream_t st);
 hipError_t launch_topk_merge(const TopkMergeArgs& a, hipStream_t st);
+hipError_t launch_transition(const TransArgs& a, hipStream_t st);
+hipError_t launch_transition_gen(const TransGenArgs& a, hipStream_t st);
 
 }  // namespace dcp

@@ -38,6 +38,7 @@ T_S, T_Z, T_WQ, T_WK, T_WV, T_WG, T_WB, T_ZBASE, T_MASK, T_GAMMA, T_BETA, T_BB =
 # atom path: single track A, pair track P, neighbour draws, ragged draws, weights
 (T_A, T_P, T_NBR, T_NBR_RAG, T_AWQ, T_AWK, T_AWV, T_AWG, T_AWB, T_AGAMMA, T_ABETA, T_ABB) = range(13, 25)
 T_XYZ = 25  # atom coordinates
+T_TW1, T_TW2, T_TW3, T_TGAMMA, T_TBETA = range(26, 31)  # pair transition weights
 
 
 # ----------------------------------------------------------------------------- numpy definition
@@ -359,6 +360,42 @@ def p_fill_device(wl: AtomWorkload, ptr: int, row0: int, n_rows: int, stream: in
                                  stream)
     if rc != 0:
         raise RuntimeError(f"synth_dev_z_rows failed ({rc})")
+
+
+# ----------------------------------------------------------------------------- pair transition
+TRANSITION_WORKLOADS = {
+    # name: (pair-tensor workload whose z the transition updates, hidden units)
+    "trans40_f32": ("adhoc40_f32", 128),
+    "trans192_bf16": ("adhoc192_bf16", 512),
+    "trans24000_bf16": ("asm24000_bf16", 512),
+}
+
+
+def transition_workload(name: str):
+    """(pair-tensor Workload, hidden) of a transition workload."""
+    zname, hidden = TRANSITION_WORKLOADS[name]
+    if zname == "adhoc40_f32":
+        wl = Workload("adhoc40_f32", 40, 32, 32, 1, 32, "f32", 1, ((0, 40),))
+    elif zname == "adhoc192_bf16":
+        wl = Workload("adhoc192_bf16", 192, 128, 128, 16, 24, "bf16", 1, ((0, 192),))
+    else:
+        wl = WORKLOADS[zname]
+    return wl, hidden
+
+
+def transition_weights(wl: "Workload", hidden: int, affine: bool = False) -> Dict[str, Optional[np.ndarray]]:
+    """W1, W2 [hidden, c_z], W3 [c_z, hidden] ~ N(0, 1/fan_in); gamma, beta when affine."""
+    c = wl.c_z
+    out: Dict[str, Optional[np.ndarray]] = {}
+    for name, tid, rows, fan in (("w1", T_TW1, hidden, c), ("w2", T_TW2, hidden, c), ("w3", T_TW3, c, hidden)):
+        out[name] = (normal(key(wl.seed, tid), 0, rows * fan) * np.float32(1.0 / np.sqrt(fan))
+                     ).astype(np.float32).reshape(rows, fan)
+    if affine:
+        out["gamma"] = (np.float32(1.0) + np.float32(0.25) * normal(key(wl.seed, T_TGAMMA), 0, c)).astype(np.float32)
+        out["beta"] = normal(key(wl.seed, T_TBETA), 0, c)
+    else:
+        out["gamma"] = out["beta"] = None
+    return out
 
 
 # ----------------------------------------------------------------------------- kNN workloads

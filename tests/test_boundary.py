@@ -239,3 +239,31 @@ def test_topk_merge_bad_arguments():
     assert L.dcp_topk_merge(-1, 8, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == E
     assert L.dcp_topk_merge(10, 8, FAKE, None, FAKE, FAKE, FAKE, FAKE, None) == E
     assert L.dcp_topk_merge(0, 8, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == dcp.DCP_OK
+
+
+# ----------------------------------------------------------------------------- pair transition
+def trans(n=1000, c_z=128, hidden=512, dt=dcp.DCP_BF16, eps=1e-5, w=FAKE, zi=FAKE, zo=FAKE * 64, ws=FAKE * 4,
+          ws_bytes=1 << 30):
+    return dcp.lib().dcp_pair_transition(n, c_z, hidden, dt, ctypes.c_float(eps), w, w, w, None, None, zi, zo, ws,
+                                         ws_bytes, None)
+
+
+def test_transition_arguments():
+    E, U, W = dcp.DCP_ERR_INVALID_ARGUMENT, dcp.DCP_ERR_UNSUPPORTED, dcp.DCP_ERR_WORKSPACE
+    assert 390_000 < dcp.dcp_transition_workspace_size(128, 512, dcp.DCP_BF16) < 400_000
+    assert dcp.dcp_transition_workspace_size(64, 100, dcp.DCP_F32) == 0
+    assert trans(c_z=64) == U                    # bf16 needs 128 / 512
+    assert trans(hidden=256) == U
+    assert trans(dt=dcp.DCP_F32, c_z=300) == U
+    assert trans(dt=dcp.DCP_F32, hidden=2048) == U
+    assert trans(dt=5) == E
+    assert trans(c_z=0) == E
+    assert trans(n=-1) == E
+    assert trans(eps=-1.0) == E
+    assert trans(w=None) == E
+    assert trans(zi=None) == E
+    assert trans(zi=FAKE + 8) == E               # misaligned
+    assert trans(zi=FAKE, zo=FAKE + 256) == E    # overlapping, not equal
+    assert trans(ws=None) == W
+    assert trans(ws_bytes=1000) == W
+    assert trans(n=0, ws=None) == dcp.DCP_OK
