@@ -37,7 +37,7 @@ constexpr int kCz = kTransCz;       // 128
 constexpr int kHid = kTransHidden;  // 512
 constexpr int kHt = kHid / 16;      // hidden tiles of 16 units
 constexpr int kTileBytes = 12 * 1024;  // per hidden tile: W1 4 KB, W2 4 KB, W3 4 KB
-constexpr int kChunkTiles = 4;          // hidden tiles per LDS chunk
+constexpr int kChunkTiles = 4;          // hidden tiles per LDS chunk (two tile pairs)
 constexpr int kChunks = kHt / kChunkTiles;
 constexpr int kChunkBytes = kChunkTiles * kTileBytes;  // 48 KB
 constexpr int kDmaPerWave = kChunkBytes / 4 / 1024;    // 1 KB DMA instructions per wave per chunk
@@ -49,43 +49,54 @@ constexpr float kLog2e = 1.44269504088896340736f;
 __host__ __device__ inline int out_channel(int ct, int r) { return 32 * (ct >> 1) + 8 * (r >> 2) + 4 * (ct & 1) + (r & 3); }
 
 // ----------------------------------------------------------------------------- weight preparation
-// One thread per 16-byte (W1, W2) or 8-byte (W3) operand fragment.
+// Scaling: W1 (and its bias) carry a factor -log2(e), so the kernel's
+// A' = -log2(e) A gives sigmoid(A) = 1 / (1 + 2^A') with no extra multiply, and
+// SiLU(A) B = A B sigmoid(A) = -ln(2) A' B / (1 + 2^A'); the factor -ln(2)
+// goes into W3. Layout per pair of hidden tiles (32 units, 24 KB):
+//   W1 and W2 A operands of v_mfma_f32_16x16x32_bf16 for each of the two
+//   tiles: [tile][mat][ks][lane] 16 B (row = unit, k-slots = channels
+//   32 ks + 8 (lane/16) .. +7), 16 KB;
+//   W3 A operands of v_mfma_f32_16x16x32_bf16 over the 32 units: [ct][lane]
+//   16 B (row = channel out_channel(ct, lane%16), k-slot j of lane group g =
+//   unit 4g + j of the first tile for j < 4, of the second for j >= 4, the
+//   order in which the lane holds SiLU(A) B), 8 KB.
+constexpr int kPairBytes = 2 * kTileBytes;
 __global__ void __launch_bounds__(256) trans_prep_kernel(TransArgs a) {
+  const float s1 = -kLog2e, s3 = -0.69314718055994530942f;
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  const int per_tile = 2 * 4 * 64 + 8 * 64;  // fragments per hidden tile
-  if (t < kHt * per_tile) {
-    const int ht = t / per_tile, f = t % per_tile;
-    char* tile = static_cast<char*>(a.w_prep) + (size_t)ht * kTileBytes;
-    if (f < 512) {
-      // W1 (mat 0) or W2 (mat 1), k-step ks, lane: row = unit 16 ht + lane%16,
-      // channels 32 ks + 8 (lane/16) .. +7, times gamma
-      const int mat = f / 256, ks = (f / 64) % 4, lane = f % 64;
+  const int per_pair = 2 * 2 * 4 * 64 + 8 * 64;  // 16-byte fragments per tile pair
+  if (t < (kHt / 2) * per_pair) {
+    const int hp = t / per_pair, f = t % per_pair;
+    char* base = static_cast<char*>(a.w_prep) + (size_t)hp * kPairBytes;
+    bf16x8 v;
+    if (f < 1024) {
+      const int tile = f / 512, mat = (f / 256) % 2, ks = (f / 64) % 4, lane = f % 64;
       const float* w = mat ? a.w2 : a.w1;
-      const int unit = 16 * ht + (lane & 15), c0 = 32 * ks + 8 * (lane >> 4);
-      bf16x8 v;
+      const float sc = mat ? 1.0f : s1;
+      const int unit = 16 * (2 * hp + tile) + (lane & 15), c0 = 32 * ks + 8 * (lane >> 4);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = (__bf16)(w[unit * kCz + c0 + i] * (a.gamma ? a.gamma[c0 + i] : 1.0f));
-      *reinterpret_cast<u32x4*>(tile + mat * 4096 + ks * 1024 + lane * 16) = __builtin_bit_cast(u32x4, v);
+      for (int i = 0; i < 8; ++i) v[i] = (__bf16)(w[unit * kCz + c0 + i] * (a.gamma ? a.gamma[c0 + i] : 1.0f) * sc);
+      *reinterpret_cast<u32x4*>(base + tile * 8192 + mat * 4096 + ks * 1024 + lane * 16) = __builtin_bit_cast(u32x4, v);
     } else {
-      // W3, output tile ct, lane: row = channel out_channel(ct, lane%16),
-      // hidden units 16 ht + 4 (lane/16) .. +3
-      const int g = f - 512, ct = g / 64, lane = g % 64;
-      const int ch = out_channel(ct, lane & 15), u0 = 16 * ht + 4 * (lane >> 4);
-      bf16x4 v;
+      const int f3 = f - 1024, ct = f3 / 64, lane = f3 % 64, g = lane >> 4;
+      const int ch = out_channel(ct, lane & 15);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = (__bf16)a.w3[ch * kHid + u0 + i];
-      *reinterpret_cast<u32x2*>(tile + 8192 + ct * 512 + lane * 8) = __builtin_bit_cast(u32x2, v);
+      for (int j = 0; j < 8; ++j) {
+        const int unit = 16 * (2 * hp + (j >> 2)) + 4 * g + (j & 3);
+        v[j] = (__bf16)(a.w3[ch * kHid + unit] * s3);
+      }
+      *reinterpret_cast<u32x4*>(base + 16384 + ct * 1024 + lane * 16) = __builtin_bit_cast(u32x4, v);
     }
   }
-  // biases b1 = W1 beta, b2 = W2 beta (fp32, per hidden unit)
-  const int u = t - kHt * per_tile;
+  // biases b1 = -log2(e) W1 beta, b2 = W2 beta (fp32, per hidden unit)
+  const int u = t - (kHt / 2) * per_pair;
   if (u >= 0 && u < 2 * kHid) {
     const int mat = u / kHid, unit = u % kHid;
     const float* w = mat ? a.w2 : a.w1;
     float s = 0.0f;
     if (a.beta)
       for (int c = 0; c < kCz; ++c) s = fmaf(w[unit * kCz + c], a.beta[c], s);
-    a.b_prep[u] = s;
+    a.b_prep[u] = mat ? s : s * s1;
   }
 }
 
@@ -119,14 +130,20 @@ __global__ void __launch_bounds__(256, 1) trans_kernel(TransArgs a) {
     const bool last_group = grp + gridDim.x >= n_groups;
     // z of this wave's 4 pair tiles: lane (n, g) holds pair 16p + n, channels 32 ks + 8g .. +7
     const int64_t pair0 = grp * 256 + wave * 64;
+    // z is read twice: here for the LayerNorm and again for the residual at
+    // the end of the group (a few microseconds later, from L2), so that its
+    // registers are free while the products run
+    auto load_z = [&](u32x4 (&zz)[4][4]) {
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const int64_t pr = min(pair0 + 16 * p + n, a.n_pairs - 1);
+        const u32x4* src = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.z_in) + pr * kCz + 8 * g);
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) zz[p][ks] = src[4 * ks];
+      }
+    };
     u32x4 zr[4][4];
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const int64_t pr = min(pair0 + 16 * p + n, a.n_pairs - 1);
-      const u32x4* src = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.z_in) + pr * kCz + 8 * g);
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) zr[p][ks] = __builtin_nontemporal_load(src + 4 * ks);
-    }
+    load_z(zr);
     // LayerNorm (two passes over the pair's 128 channels: 32 per lane, 4 lanes)
     bf16x8 nv[4][4];
 #pragma unroll
@@ -161,7 +178,7 @@ __global__ void __launch_bounds__(256, 1) trans_kernel(TransArgs a) {
 #pragma unroll
       for (int p = 0; p < 4; ++p) acc[ct][p] = zero;
 
-    for (int c = 0; c < kChunks; ++c, ++seq) {
+    auto run_chunk = [&](int c, bool last_chunk, u32x4 (&zres)[4][4]) {
       const int b = seq & 1;
       barrier_lds();  // every wave is done with buffer b ^ 1 (the previous chunk)
       const bool more = c + 1 < kChunks || !last_group;
@@ -172,48 +189,63 @@ __global__ void __launch_bounds__(256, 1) trans_kernel(TransArgs a) {
         wait_vm<0>();
       barrier_lds();  // and every other wave's
       const char* chunk = s_w[b];
-#pragma unroll 1
-      for (int t = 0; t < kChunkTiles; ++t) {
-        const char* tile = chunk + t * kTileBytes;
-        const int ht = c * kChunkTiles + t;
-        // A = W1' N + b1, B = W2' N + b2 (rows: hidden units 16 ht + 4g + i; columns: pairs)
-        f32x4 ha[4], hb[4];
-        const float4 b1 = *reinterpret_cast<const float4*>(s_b + 16 * ht + 4 * g);
-        const float4 b2 = *reinterpret_cast<const float4*>(s_b + kHid + 16 * ht + 4 * g);
+      // first products of tile pair q: A' = W1' N + b1', B = W2' N + b2
+      // (rows: hidden units 16 ht + 4g + i; columns: pairs), tiles ht = 2q', 2q'+1
+      auto first = [&](int q, f32x4 (&ha)[2][4], f32x4 (&hb)[2][4]) {
+        const char* pr = chunk + q * kPairBytes;
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          ha[p] = f32x4{b1.x, b1.y, b1.z, b1.w};
-          hb[p] = f32x4{b2.x, b2.y, b2.z, b2.w};
-        }
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-          const bf16x8 w1 = as_bf16x8(*reinterpret_cast<const u32x4*>(tile + ks * 1024 + lane * 16));
-          const bf16x8 w2 = as_bf16x8(*reinterpret_cast<const u32x4*>(tile + 4096 + ks * 1024 + lane * 16));
+        for (int tt = 0; tt < 2; ++tt) {
+          const int ht = (c * kChunkTiles / 2 + q) * 2 + tt;
+          const float4 b1 = *reinterpret_cast<const float4*>(s_b + 16 * ht + 4 * g);
+          const float4 b2 = *reinterpret_cast<const float4*>(s_b + kHid + 16 * ht + 4 * g);
 #pragma unroll
           for (int p = 0; p < 4; ++p) {
-            ha[p] = mfma32(w1, nv[p][ks], ha[p]);
-            hb[p] = mfma32(w2, nv[p][ks], hb[p]);
+            ha[tt][p] = f32x4{b1.x, b1.y, b1.z, b1.w};
+            hb[tt][p] = f32x4{b2.x, b2.y, b2.z, b2.w};
+          }
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks) {
+            const bf16x8 w1 = as_bf16x8(*reinterpret_cast<const u32x4*>(pr + tt * 8192 + ks * 1024 + lane * 16));
+            const bf16x8 w2 = as_bf16x8(*reinterpret_cast<const u32x4*>(pr + tt * 8192 + 4096 + ks * 1024 + lane * 16));
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+              ha[tt][p] = mfma32(w1, nv[p][ks], ha[tt][p]);
+              hb[tt][p] = mfma32(w2, nv[p][ks], hb[tt][p]);
+            }
           }
         }
-        // h = SiLU(A) * B, as the B operand (k-slots = hidden units 4g .. 4g+3)
-        bf16x4 hv[4];
+      };
+      // h' = A' B / (1 + 2^A') as the B operand over the 32 units of the pair
+      // (k-slot j: unit 4g + j of tile 0 for j < 4, of tile 1 for j >= 4), then
+      // out^T += W3'' h'^T
+      auto second = [&](int q, const f32x4 (&ha)[2][4], const f32x4 (&hb)[2][4]) {
+        bf16x8 hv[4];
 #pragma unroll
         for (int p = 0; p < 4; ++p)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float x = ha[p][i];
-            const float sg = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-kLog2e * x));
-            hv[p][i] = (__bf16)(x * sg * hb[p][i]);
+          for (int j = 0; j < 8; ++j) {
+            const float x = ha[j >> 2][p][j & 3];
+            hv[p][j] = (__bf16)(x * hb[j >> 2][p][j & 3] * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x)));
           }
-        // out^T += W3' h^T
+        const char* pr = chunk + q * kPairBytes + 16384;
 #pragma unroll
         for (int ct = 0; ct < 8; ++ct) {
-          const bf16x4 w3 = as_bf16x4(*reinterpret_cast<const u32x2*>(tile + 8192 + ct * 512 + lane * 8));
+          const bf16x8 w3 = as_bf16x8(*reinterpret_cast<const u32x4*>(pr + ct * 1024 + lane * 16));
 #pragma unroll
-          for (int p = 0; p < 4; ++p) acc[ct][p] = mfma16(w3, hv[p], acc[ct][p]);
+          for (int p = 0; p < 4; ++p) acc[ct][p] = mfma32(w3, hv[p], acc[ct][p]);
         }
-      }
-    }
+      };
+      f32x4 ha0[2][4], hb0[2][4], ha1[2][4], hb1[2][4];
+      first(0, ha0, hb0);
+      first(1, ha1, hb1);
+      if (last_chunk) load_z(zres);  // the residual's z, issued once the normalised z is dead
+      second(0, ha0, hb0);
+      second(1, ha1, hb1);
+      ++seq;
+    };
+    u32x4 zres[4][4];
+    for (int c = 0; c < kChunks - 1; ++c) run_chunk(c, false, zres);
+    run_chunk(kChunks - 1, true, zres);
     // residual and store: accumulator (ct = 2 ks + s, register i) is channel
     // 32 ks + 8g + 4s + i, element 4s + i of the lane's loaded chunk ks
 #pragma unroll
@@ -226,7 +258,7 @@ __global__ void __launch_bounds__(256, 1) trans_kernel(TransArgs a) {
         bf16x8 o;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const uint32_t w = zr[p][ks][e >> 1];
+          const uint32_t w = zres[p][ks][e >> 1];
           const float zin = __uint_as_float((e & 1) ? (w & 0xFFFF0000u) : (w << 16));
           o[e] = (__bf16)(zin + acc[2 * ks + (e >> 2)][p][e & 3]);
         }
@@ -282,7 +314,7 @@ __global__ void __launch_bounds__(256) trans_gen_kernel(TransGenArgs a) {
 size_t trans_prep_bytes() { return (size_t)kHt * kTileBytes + 2 * kHid * sizeof(float); }
 
 hipError_t launch_transition(const TransArgs& a, hipStream_t st) {
-  const int prep_threads = kHt * (2 * 4 * 64 + 8 * 64) + 2 * kHid;
+  const int prep_threads = (kHt / 2) * (2 * 2 * 4 * 64 + 8 * 64) + 2 * kHid;
   hipLaunchKernelGGL(trans_prep_kernel, dim3((prep_threads + 255) / 256), dim3(256), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
