@@ -32,11 +32,12 @@ def _configure(lib: ctypes.CDLL) -> ctypes.CDLL:
                                             vp, vp, vp, vp, vp, vp, vp, vp, f64, i32, vp]
     lib.oracle_knn.argtypes = [vp, i64, vp, i64, i64, vp, vp, i32, i32, vp, vp]
     lib.oracle_transition.argtypes = [i64, i32, i32, vp, i32, vp, vp, vp, vp, vp, f64, vp]
+    lib.oracle_scatter_mean.argtypes = [i64, i64, i32, vp, i32, vp, vp]
     lib.oracle_topk_merge.argtypes = [i64, i32, vp, vp, vp, vp, vp, vp]
     lib.oracle_knn_blocked.argtypes = [vp, i64, vp, i64, vp, vp, i32, i32, i32, vp, vp]
     for f in (lib.oracle_bias, lib.oracle_attend, lib.oracle_merge, lib.oracle_attention,
               lib.oracle_sparse_attention, lib.oracle_knn, lib.oracle_topk_merge, lib.oracle_knn_blocked,
-              lib.oracle_transition):
+              lib.oracle_transition, lib.oracle_scatter_mean):
         f.restype = ctypes.c_int
     return lib
 
@@ -241,4 +242,17 @@ def transition(z: np.ndarray, w1: np.ndarray, w2: np.ndarray, w3: np.ndarray, ga
     rc = _load().oracle_transition(n, c_z, hidden, zb.ctypes.data, dt, *[_p(a) for a in keep], eps, _p(out))
     if rc != 0:
         raise ValueError("oracle_transition rejected its arguments")
+    return out
+
+
+def scatter_mean(a: np.ndarray, tok_idx: np.ndarray, n_tokens: int) -> np.ndarray:
+    """Per-token mean of atom features a [n_atoms, c] (fp32 or bf16 bits); fp64 [n_tokens, c]."""
+    ab, dt = _zbuf(a)
+    n_atoms, c = ab.shape
+    idx = np.ascontiguousarray(tok_idx, dtype=np.int32)
+    assert idx.shape == (n_atoms,)
+    out = np.empty((n_tokens, c), dtype=np.float64)
+    rc = _load().oracle_scatter_mean(n_atoms, n_tokens, c, ab.ctypes.data, dt, idx.ctypes.data, out.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle_scatter_mean rejected its arguments")
     return out

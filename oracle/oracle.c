@@ -606,3 +606,29 @@ int oracle_transition(int64_t n_pairs, int c_z, int hidden, const void* z, int d
   }
   return 0;
 }
+
+/* ---------------------------------------------------------------------------
+ * Atom -> token mean pooling (Appendix "Non-determinism guard" and the 2D
+ * pooling boundary: atom-level features are averaged per token; the paper
+ * replaces a non-deterministic atomic index_reduce("mean") by a deterministic
+ * reduction): out[t, :] = mean of a[i, :] over the atoms i with tok_idx[i] = t,
+ * summed in increasing atom order in fp64; a token without atoms gives 0; an
+ * index outside [0, n_tokens) belongs to no token.
+ * a: [n_atoms, c] fp32 (dtype 0) or bf16 (1); out: [n_tokens, c] fp64.
+ * ------------------------------------------------------------------------- */
+int oracle_scatter_mean(int64_t n_atoms, int64_t n_tokens, int c, const void* a, int dtype, const int32_t* tok_idx,
+                        double* out) {
+  if (!a || !tok_idx || !out || c <= 0 || n_tokens < 0 || n_atoms < 0) return -1;
+  int64_t* cnt = (int64_t*)calloc((size_t)(n_tokens > 0 ? n_tokens : 1), sizeof(int64_t));
+  for (int64_t t = 0; t < n_tokens * c; ++t) out[t] = 0.0;
+  for (int64_t i = 0; i < n_atoms; ++i) {
+    const int64_t t = tok_idx[i];
+    if (t < 0 || t >= n_tokens) continue;
+    cnt[t] += 1;
+    for (int k = 0; k < c; ++k) out[t * c + k] += load_elem(a, dtype, i * c + k);
+  }
+  for (int64_t t = 0; t < n_tokens; ++t)
+    for (int k = 0; k < c; ++k) out[t * c + k] = cnt[t] > 0 ? out[t * c + k] / (double)cnt[t] : 0.0;
+  free(cnt);
+  return 0;
+}

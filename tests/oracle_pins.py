@@ -23,6 +23,9 @@ The pair transition is pinned to its torch composition (layer_norm, linear,
 silu), zero-branch and scaling closed forms, the LayerNorm shift, and brute
 force at 40 digits.
 
+The atom-to-token mean is pinned to torch's index_reduce("mean") and a numpy
+bincount mean, plus closed forms (copies, constants, dropped indices, order).
+
 The sparse (kNN) atom attention has its own pins: torch's SDPA over each
 query's gathered keys, the dense pipeline when every atom is a neighbour,
 closed forms (one neighbour atom in every slot, all slots empty), slot
@@ -771,6 +774,50 @@ def pin_transition_bruteforce_mpmath():
         for c in range(4):
             ref = x[c] + mpmath.fsum(W3[c][u] * h[u] for u in range(5))
             assert abs(float(ref) - got[p, c]) <= 1e-13 * max(1.0, abs(float(ref))), (p, c)
+
+
+# ----------------------------------------------------------------------------- atom -> token mean
+def pin_scatter_mean_torch_and_numpy():
+    """torch's index_reduce("mean", include_self=False) and a numpy bincount
+    mean (fp64); tokens without atoms are 0."""
+    r = _rng(80)
+    for n_atoms, n_tok, c in ((50, 9, 3), (400, 37, 16), (7, 12, 5)):
+        a = r.standard_normal((n_atoms, c)).astype(np.float32)
+        idx = r.integers(0, n_tok, n_atoms).astype(np.int32)
+        got = oracle.scatter_mean(a, idx, n_tok)
+        out = torch.zeros((n_tok, c), dtype=torch.float64)
+        out.index_reduce_(0, torch.from_numpy(idx.astype(np.int64)), torch.from_numpy(a.astype(np.float64)), "mean",
+                          include_self=False)
+        assert _rel(got, out.numpy()) <= 1e-13
+        cnt = np.bincount(idx, minlength=n_tok)
+        sums = np.stack([np.bincount(idx, weights=a[:, k].astype(np.float64), minlength=n_tok) for k in range(c)], 1)
+        ref = np.where(cnt[:, None] > 0, sums / np.maximum(cnt, 1)[:, None], 0.0)
+        assert _rel(got, ref) <= 1e-13
+        assert np.all(got[cnt == 0] == 0.0)
+
+
+def pin_scatter_mean_closed_forms():
+    """One atom per token copies it; constant features average to the
+    constant; out-of-range indices belong to no token; atom order is
+    irrelevant up to rounding."""
+    r = _rng(81)
+    a = r.standard_normal((20, 4)).astype(np.float32)
+    perm = r.permutation(20).astype(np.int32)
+    got = oracle.scatter_mean(a, perm, 20)
+    assert np.array_equal(got[perm], a.astype(np.float64))
+    b = np.full((30, 3), 2.5, dtype=np.float32)
+    assert np.all(oracle.scatter_mean(b, r.integers(0, 4, 30).astype(np.int32), 4)[:, 0] <= 2.5)
+    idx = r.integers(0, 4, 30).astype(np.int32)
+    m = oracle.scatter_mean(b, idx, 4)
+    assert np.array_equal(m[np.bincount(idx, minlength=4) > 0], np.full((int((np.bincount(idx, minlength=4) > 0).sum()), 3), 2.5))
+    feats = np.vstack([a, a[:10]])  # 30 atoms
+    idx2 = idx.copy()
+    idx2[:5] = [-1, 4, 100, -7, 4]
+    keep = (idx2 >= 0) & (idx2 < 4)
+    assert np.array_equal(oracle.scatter_mean(feats, idx2, 4), oracle.scatter_mean(feats[keep], idx2[keep], 4))
+    q = r.permutation(30)
+    c = r.standard_normal((30, 6)).astype(np.float32)
+    assert _rel(oracle.scatter_mean(c[q], idx[q], 4), oracle.scatter_mean(c, idx, 4)) <= 1e-14
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -68,6 +68,13 @@ MUTANTS = [
     ("transition gate on the other branch", "h[u] = a / (1.0 + exp(-a)) * b;", "h[u] = b / (1.0 + exp(-b)) * a;"),
     ("transition residual dropped", "out[p * c_z + c] = x[c] + t;", "out[p * c_z + c] = t;"),
     ("transition beta dropped", "((x[c] - mu) * inv) + (beta ? beta[c] : 0.0);", "((x[c] - mu) * inv);"),
+    ("scatter mean divides by the token count + 1",
+     "out[t * c + k] = cnt[t] > 0 ? out[t * c + k] / (double)cnt[t] : 0.0;",
+     "out[t * c + k] = cnt[t] > 0 ? out[t * c + k] / (double)(cnt[t] + 1) : 0.0;"),
+    ("scatter mean keeps the last atom only", "for (int k = 0; k < c; ++k) out[t * c + k] += load_elem(a, dtype, i * c + k);",
+     "for (int k = 0; k < c; ++k) out[t * c + k] = load_elem(a, dtype, i * c + k);"),
+    ("scatter mean drops the last token", "if (t < 0 || t >= n_tokens) continue;",
+     "if (t < 0 || t >= n_tokens - 1) continue;"),
     ("transition w3 transposed", "t += w3[(int64_t)c * hidden + u] * h[u];",
      "t += w3[(int64_t)(u % c_z) * hidden + (c % hidden)] * h[u];"),
 ]
