@@ -36,6 +36,8 @@ PEAK_FP32_TFLOPS = 157.3  # MI355X fp32 vector, published
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 matrix cores, published
 TRANS_SOURCES = ("paper_2607_05439_amd/csrc/transition.hip", "paper_2607_05439_amd/csrc/cdna4.h")
 TRANS_METRIC = "ms per pair transition (LayerNorm + SwiGLU + residual) + matrix-core TFLOP/s"
+SCATTER_SOURCES = ("paper_2607_05439_amd/csrc/scatter.hip",)
+SCATTER_METRIC = "us per deterministic atom-to-token mean + achieved HBM GB/s"
 
 
 def progress(msg):
@@ -490,6 +492,93 @@ def transition_main(args, name):
     print(json.dumps(line), flush=True)
 
 
+def scatter_main(args, name):
+    import numpy as np
+    import torch
+    import paper_2607_05439_amd as dcp
+    import oracle
+    import synth
+
+    n_tok, c, dt = synth.SCATTER_WORKLOADS[name]
+    dev = torch.device("cuda:0")
+    sp = torch.cuda.current_stream().cuda_stream
+    idx_host = synth.token_index(n_tok)
+    n_atoms = len(idx_host)
+    bf16 = dt == "bf16"
+    a_host = synth.atom_features(n_atoms, c, bf16)
+    progress(f"workload {name}: {n_atoms} atoms -> {n_tok} tokens, {c} channels, {dt} features")
+    a = (torch.from_numpy(a_host.view(np.int16)).view(torch.bfloat16) if bf16 else torch.from_numpy(a_host)).to(dev)
+    idx = torch.from_numpy(idx_host).to(dev)
+    out = torch.empty((n_tok, c), dtype=torch.float32, device=dev)
+    ws_bytes = dcp.dcp_scatter_mean_workspace_size(n_tok, c)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    in_dtype = dcp.DCP_BF16 if bf16 else dcp.DCP_F32
+    hip = Hip()
+
+    def step(evs=None):
+        if evs is not None:
+            dcp.dcp_set_timing_events(*evs)
+        dcp.dcp_scatter_mean(n_atoms, n_tok, c, in_dtype, dcp.DCP_F32, a, idx, out, ws, ws_bytes, sp)
+        if evs is not None:
+            dcp.dcp_set_timing_events(None, None)
+
+    cal = 1 << 28
+    src = torch.empty(cal, dtype=torch.uint8, device=dev)
+    dst = torch.empty(cal, dtype=torch.uint8, device=dev)
+    synth.device_copy(src.data_ptr(), dst.data_ptr(), cal, sp)
+    torch.cuda.synchronize()
+    del src, dst
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(hip.event(), hip.event()) for _ in range(args.steps)]
+    t_start, t_stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    progress(f"timing {args.steps} steps")
+    t_start.record()
+    for i in range(args.steps):
+        step(evs[i])
+    t_stop.record()
+    torch.cuda.synchronize()
+    ms_per_step = t_start.elapsed_time(t_stop) / args.steps
+    kms = sum(hip.elapsed_ms(x, y) for x, y in evs) / len(evs)
+    alg = n_atoms * c * a.element_size() + n_atoms * 4 + n_tok * c * 4  # features and indices in, means out
+    achieved = alg / (kms * 1e-3) / 1e9
+    progress(f"{ms_per_step * 1e3:.1f} us per pooling (kernels {kms * 1e3:.1f} us): {achieved:.0f} GB/s")
+    cpu = None
+    if not args.no_cpu_baseline:
+        t0 = time.perf_counter()
+        reps = 0
+        while time.perf_counter() - t0 < min(args.cpu_seconds, 10.0):
+            oracle.scatter_mean(a_host, idx_host, n_tok)
+            reps += 1
+        t_one = (time.perf_counter() - t0) / reps
+        cpu = {"value": round(alg / t_one / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+               "sample": f"the whole pooling, {reps} repetitions (single-threaded fp64), {t_one * 1e3:.1f} ms each",
+               "ms_per_pooling": round(t_one * 1e3, 2)}
+    line = {
+        "metric": SCATTER_METRIC,
+        "value": round(achieved, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dt,
+        "data": "synthetic (seeded; 4-14 atoms per token, ordered by token)",
+        "config": {"workload": name, "n_atoms": n_atoms, "n_tokens": n_tok, "c": c, "calibration_bytes": cal,
+                   "algorithmic_bytes": alg},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": stored_traffic(name, SCATTER_SOURCES),
+                     "kernel": "scatter (zero + accum + final)", "kernel_ms": round(kms, 5),
+                     "algorithmic_bytes_per_launch": alg},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -518,6 +607,8 @@ def main():
         return knn_main(args, synth.KNN_WORKLOADS[args.workload])
     if args.workload in synth.TRANSITION_WORKLOADS:
         return transition_main(args, args.workload)
+    if args.workload in synth.SCATTER_WORKLOADS:
+        return scatter_main(args, args.workload)
     wl = synth.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()

@@ -280,11 +280,40 @@ int dcp_pair_transition(int64_t n_pairs, int32_t c_z, int32_t hidden, int32_t ac
                         const float* ln_beta, const void* z_in, void* z_out, void* workspace, size_t workspace_bytes,
                         void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Atom -> token mean pooling (Appendix "Non-determinism guard" and the 2D
+ * pooling boundary): out[t, :] = mean of a[i, :] over the atoms i with
+ * tok_idx[i] = t; a token without atoms gives 0; an index outside
+ * [0, n_tokens) belongs to no token.
+ *
+ * Deterministic for any index pattern and on any device: features are summed
+ * as 64-bit fixed-point integers (value * 2^32, rounded to nearest), whose
+ * addition does not depend on order, then divided by the count in fp64 and
+ * rounded to out_dtype. Each feature is clamped to |x| <= 2^30 and each token's
+ * sum must stay below 2^31 in magnitude; the absolute rounding of a feature is
+ * at most 2^-33. NaN features give unspecified values for their token.
+ * ------------------------------------------------------------------------- */
+
+/* Workspace bytes for dcp_scatter_mean (written to *bytes). Host-only. */
+int dcp_scatter_mean_workspace_size(int64_t n_tokens, int32_t c, size_t* bytes);
+
+/*   a        [n_atoms, c] in_dtype (may be NULL when n_atoms = 0)
+ *   tok_idx  [n_atoms] int32 token of each atom (any order)
+ *   out      [n_tokens, c] out_dtype
+ *   c        1 <= c <= 512
+ * Device pointers aligned to their element size; workspace of at least
+ * dcp_scatter_mean_workspace_size() bytes, 256-byte aligned. n_tokens = 0 is a
+ * no-op. */
+int dcp_scatter_mean(int64_t n_atoms, int64_t n_tokens, int32_t c, int32_t in_dtype, int32_t out_dtype, const void* a,
+                     const int32_t* tok_idx, void* out, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Optional timing hook: when both are non-NULL hipEvent_t handles, the calling
  * thread's next dcp_pair_bias_attention, dcp_sparse_pair_bias_attention,
- * dcp_knn_topk and dcp_pair_transition calls record `start` just before and
+ * dcp_knn_topk, dcp_pair_transition and dcp_scatter_mean calls record
+ * `start` just before and
  * `stop` just after the main kernel (after any projections; around the
- * weight preparation and the transition kernel), on that call's stream. Pass NULL, NULL to clear.
+ * weight preparation and the transition kernel of a transition; around all
+ * three kernels of a pooling), on that call's stream. Pass NULL, NULL to clear.
  * Host-only. */
 int dcp_set_timing_events(void* start_event, void* stop_event);
 

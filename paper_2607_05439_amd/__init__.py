@@ -5,7 +5,8 @@ used for device memory and streams. The functions carry the C names
 (``dcp_pair_bias_attention``, ``dcp_bias_project``, ``dcp_block_merge``,
 ``dcp_workspace_size``, ``dcp_sparse_pair_bias_attention``,
 ``dcp_sparse_workspace_size``, ``dcp_knn_topk``, ``dcp_topk_merge``,
-``dcp_pair_transition``, ``dcp_transition_workspace_size``) and accept torch tensors (device pointers are taken
+``dcp_pair_transition``, ``dcp_transition_workspace_size``, ``dcp_scatter_mean``,
+``dcp_scatter_mean_workspace_size``) and accept torch tensors (device pointers are taken
 from ``data_ptr()``) or plain integer addresses. Loading fails loudly when the
 library has not been built: there is no fallback.
 """
@@ -22,7 +23,8 @@ DCP_F32, DCP_BF16 = 0, 1
 DCP_OK, DCP_ERR_INVALID_ARGUMENT, DCP_ERR_UNSUPPORTED, DCP_ERR_WORKSPACE, DCP_ERR_HIP = 0, -1, -2, -3, -4
 EXPORTS = ("dcp_workspace_size", "dcp_pair_bias_attention", "dcp_bias_project", "dcp_block_merge",
            "dcp_sparse_workspace_size", "dcp_sparse_pair_bias_attention", "dcp_knn_topk", "dcp_topk_merge",
-           "dcp_transition_workspace_size", "dcp_pair_transition", "dcp_set_timing_events",
+           "dcp_transition_workspace_size", "dcp_pair_transition", "dcp_scatter_mean_workspace_size",
+           "dcp_scatter_mean", "dcp_set_timing_events",
            "dcp_last_error", "dcp_version")
 
 
@@ -71,10 +73,13 @@ def lib() -> ctypes.CDLL:
         L.dcp_topk_merge.argtypes = [i64, i32, vp, vp, vp, vp, vp, vp, vp]
         L.dcp_transition_workspace_size.argtypes = [i32, i32, i32, P(sz)]
         L.dcp_pair_transition.argtypes = [i64, i32, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.dcp_scatter_mean_workspace_size.argtypes = [i64, i32, P(sz)]
+        L.dcp_scatter_mean.argtypes = [i64, i64, i32, i32, i32, vp, vp, vp, vp, sz, vp]
         L.dcp_set_timing_events.argtypes = [vp, vp]
         for f in (L.dcp_workspace_size, L.dcp_pair_bias_attention, L.dcp_bias_project, L.dcp_block_merge,
                   L.dcp_sparse_workspace_size, L.dcp_sparse_pair_bias_attention, L.dcp_knn_topk, L.dcp_topk_merge,
-                  L.dcp_transition_workspace_size, L.dcp_pair_transition, L.dcp_set_timing_events):
+                  L.dcp_transition_workspace_size, L.dcp_pair_transition, L.dcp_scatter_mean_workspace_size,
+                  L.dcp_scatter_mean, L.dcp_set_timing_events):
             f.restype = ctypes.c_int
         L.dcp_last_error.restype = ctypes.c_char_p
         L.dcp_last_error.argtypes = []
@@ -190,6 +195,18 @@ def dcp_pair_transition(n_pairs: int, c_z: int, hidden: int, act_dtype: int, ln_
     _check(lib().dcp_pair_transition(n_pairs, c_z, hidden, act_dtype, ln_eps, _ptr(w1), _ptr(w2), _ptr(w3),
                                      _ptr(ln_gamma), _ptr(ln_beta), _ptr(z_in), _ptr(z_out), _ptr(workspace),
                                      workspace_bytes, _stream(stream)))
+
+
+def dcp_scatter_mean_workspace_size(n_tokens: int, c: int) -> int:
+    out = ctypes.c_size_t()
+    _check(lib().dcp_scatter_mean_workspace_size(n_tokens, c, ctypes.byref(out)))
+    return out.value
+
+
+def dcp_scatter_mean(n_atoms: int, n_tokens: int, c: int, in_dtype: int, out_dtype: int, a: Ptr, tok_idx: Ptr,
+                     out: Ptr, workspace: Ptr, workspace_bytes: int, stream=None) -> None:
+    _check(lib().dcp_scatter_mean(n_atoms, n_tokens, c, in_dtype, out_dtype, _ptr(a), _ptr(tok_idx), _ptr(out),
+                                  _ptr(workspace), workspace_bytes, _stream(stream)))
 
 
 def dcp_set_timing_events(start_event: Optional[int], stop_event: Optional[int]) -> None:

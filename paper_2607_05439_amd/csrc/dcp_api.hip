@@ -703,4 +703,63 @@ int dcp_pair_transition(int64_t n_pairs, int32_t c_z, int32_t hidden, int32_t ac
   return ok();
 }
 
+// ----------------------------------------------------------------------------- atom -> token mean
+static size_t scatter_ws(int64_t n_tokens, int32_t c) {
+  return round_up((size_t)n_tokens * c * 8, 256) + round_up((size_t)n_tokens * 4, 256);
+}
+
+static int check_scatter(int64_t n_atoms, int64_t n_tokens, int32_t c, int32_t in_dtype, int32_t out_dtype) {
+  if (n_atoms < 0 || n_tokens < 0) return fail(DCP_ERR_INVALID_ARGUMENT, "n_atoms and n_tokens must be >= 0");
+  if (c < 1) return fail(DCP_ERR_INVALID_ARGUMENT, "c must be >= 1");
+  if (c > dcp::kScatterMaxC) return fail(DCP_ERR_UNSUPPORTED, "c must be <= %d (got %d)", dcp::kScatterMaxC, c);
+  if ((in_dtype != DCP_F32 && in_dtype != DCP_BF16) || (out_dtype != DCP_F32 && out_dtype != DCP_BF16))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "dtypes must be DCP_F32 or DCP_BF16");
+  return DCP_OK;
+}
+
+int dcp_scatter_mean_workspace_size(int64_t n_tokens, int32_t c, size_t* bytes) {
+  if (!bytes) return fail(DCP_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  const int rc = check_scatter(0, n_tokens, c, DCP_F32, DCP_F32);
+  if (rc) return rc;
+  *bytes = n_tokens == 0 ? 0 : scatter_ws(n_tokens, c);
+  return ok();
+}
+
+int dcp_scatter_mean(int64_t n_atoms, int64_t n_tokens, int32_t c, int32_t in_dtype, int32_t out_dtype, const void* a,
+                     const int32_t* tok_idx, void* out, void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_scatter(n_atoms, n_tokens, c, in_dtype, out_dtype);
+  if (rc) return rc;
+  if (n_tokens == 0) return ok();
+  if (!out || (n_atoms > 0 && (!a || !tok_idx)))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "out (and a, tok_idx when n_atoms > 0) are required");
+  const size_t ea = in_dtype == DCP_BF16 ? 2 : 4, eo = out_dtype == DCP_BF16 ? 2 : 4;
+  if ((a && !aligned(a, ea)) || (tok_idx && !aligned(tok_idx, 4)) || !aligned(out, eo))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "a, tok_idx and out must be aligned to their element size");
+  const size_t need = scatter_ws(n_tokens, c);
+  if (!workspace || !aligned(workspace, 256))
+    return fail(DCP_ERR_WORKSPACE, "workspace must be a 256-byte aligned device pointer");
+  if (workspace_bytes < need)
+    return fail(DCP_ERR_WORKSPACE, "workspace too small: %zu bytes given, %zu needed", workspace_bytes, need);
+  dcp::ScatterArgs s{};
+  s.n_atoms = n_atoms;
+  s.n_tokens = n_tokens;
+  s.c = c;
+  s.a_bf16 = in_dtype == DCP_BF16;
+  s.out_bf16 = out_dtype == DCP_BF16;
+  s.a = a;
+  s.tok_idx = tok_idx;
+  s.acc = static_cast<int64_t*>(workspace);
+  s.cnt = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + round_up((size_t)n_tokens * c * 8, 256));
+  s.out = out;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  if (g_ev_start && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_start), st)) != hipSuccess)
+    return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
+  if ((e = dcp::launch_scatter_mean(s, st)) != hipSuccess)
+    return fail(DCP_ERR_HIP, "scatter-mean launch failed: %s", hipGetErrorString(e));
+  if (g_ev_stop && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_stop), st)) != hipSuccess)
+    return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 }  // extern "C"

@@ -203,6 +203,19 @@ struct TransGenArgs {
 
 size_t trans_prep_bytes();
 
+// Atom -> token mean: up to 512 channels.
+constexpr int kScatterMaxC = 512;
+
+struct ScatterArgs {
+  int64_t n_atoms, n_tokens;
+  int32_t c, a_bf16, out_bf16;
+  const void* a;          // [n_atoms][c]
+  const int32_t* tok_idx; // [n_atoms]
+  int64_t* acc;           // [n_tokens][c] fixed-point sums (workspace)
+  uint32_t* cnt;          // [n_tokens] (workspace)
+  void* out;              // [n_tokens][c]
+};
+
 hipError_t launch_fast_proj(const FastProjArgs& a, hipStream_t st);
 hipError_t launch_fast_attn(const FastAttnArgs& a, hipStream_t st);
 hipError_t launch_fast_bias(const FastBiasArgs& a, hipStream_t st);
@@ -216,5 +229,6 @@ hipError_t launch_knn(const KnnArgs& a, hipStream_t st);
 hipError_t launch_topk_merge(const TopkMergeArgs& a, hipStream_t st);
 hipError_t launch_transition(const TransArgs& a, hipStream_t st);
 hipError_t launch_transition_gen(const TransGenArgs& a, hipStream_t st);
+hipError_t launch_scatter_mean(const ScatterArgs& a, hipStream_t st);
 
 }  // namespace dcp

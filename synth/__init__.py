@@ -39,6 +39,7 @@ T_S, T_Z, T_WQ, T_WK, T_WV, T_WG, T_WB, T_ZBASE, T_MASK, T_GAMMA, T_BETA, T_BB =
 (T_A, T_P, T_NBR, T_NBR_RAG, T_AWQ, T_AWK, T_AWV, T_AWG, T_AWB, T_AGAMMA, T_ABETA, T_ABB) = range(13, 25)
 T_XYZ = 25  # atom coordinates
 T_TW1, T_TW2, T_TW3, T_TGAMMA, T_TBETA = range(26, 31)  # pair transition weights
+T_ATOMS_PER_TOK, T_AFEAT = 31, 32  # atom -> token pooling
 
 
 # ----------------------------------------------------------------------------- numpy definition
@@ -396,6 +397,26 @@ def transition_weights(wl: "Workload", hidden: int, affine: bool = False) -> Dic
     else:
         out["gamma"] = out["beta"] = None
     return out
+
+
+# ----------------------------------------------------------------------------- atom -> token pooling
+SCATTER_WORKLOADS = {
+    # name: (tokens, channels, feature dtype)
+    "pool300_f32": (300, 64, "f32"),
+    "pool24000_bf16": (24000, 128, "bf16"),
+}
+
+
+def token_index(n_tokens: int, seed: int = 0) -> np.ndarray:
+    """Token of each atom, atoms ordered by token: token t has 4 + word(t) % 11
+    atoms (4 .. 14, the heavy-atom counts of residues; mean 9)."""
+    counts = (4 + word_np(key(seed, T_ATOMS_PER_TOK), np.arange(n_tokens, dtype=np.uint64)) % np.uint64(11)
+              ).astype(np.int64)
+    return np.repeat(np.arange(n_tokens, dtype=np.int32), counts)
+
+
+def atom_features(n_atoms: int, c: int, bf16: bool, seed: int = 0) -> np.ndarray:
+    return normal(key(seed, T_AFEAT), 0, n_atoms * c, bf16=bf16).reshape(n_atoms, c)
 
 
 # ----------------------------------------------------------------------------- kNN workloads

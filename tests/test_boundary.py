@@ -267,3 +267,24 @@ def test_transition_arguments():
     assert trans(ws=None) == W
     assert trans(ws_bytes=1000) == W
     assert trans(n=0, ws=None) == dcp.DCP_OK
+
+
+# ----------------------------------------------------------------------------- atom -> token mean
+def test_scatter_mean_arguments():
+    E, U, W = dcp.DCP_ERR_INVALID_ARGUMENT, dcp.DCP_ERR_UNSUPPORTED, dcp.DCP_ERR_WORKSPACE
+    assert dcp.dcp_scatter_mean_workspace_size(24000, 128) >= 24000 * 128 * 8 + 24000 * 4
+    L = dcp.lib()
+    ok = lambda **kw: L.dcp_scatter_mean(kw.get("na", 100), kw.get("nt", 10), kw.get("c", 128), kw.get("di", 1),
+                                         kw.get("do", 0), kw.get("a", FAKE), kw.get("idx", FAKE), kw.get("out", FAKE),
+                                         kw.get("ws", FAKE), kw.get("wsb", 1 << 30), None)
+    assert ok(c=0) == E
+    assert ok(c=513) == U
+    assert ok(na=-1) == E
+    assert ok(di=4) == E
+    assert ok(a=None) == E
+    assert ok(idx=None) == E
+    assert ok(out=None) == E
+    assert ok(idx=FAKE + 2) == E
+    assert ok(ws=None) == W
+    assert ok(wsb=100) == W
+    assert ok(nt=0, out=None, ws=None) == dcp.DCP_OK
