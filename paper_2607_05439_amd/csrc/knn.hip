@@ -8,16 +8,24 @@
 // smaller candidate index. The 64-bit key (d2 bits << 32) | index orders
 // exactly that way (d2 >= 0).
 //
-// knn_kernel: a workgroup of 16 waves serves 16 consecutive query rows, one per
-// wave. Candidates are staged through LDS in tiles of 2048 (structure of
-// arrays) shared by the 16 waves, visited starting at the tile that holds the
-// queries themselves when they are candidates (their sequence neighbours are
-// close in space, which makes the running threshold tight early; the result
-// does not depend on the order). Per 64 candidates a wave computes the keys,
-// keeps those below its current k-th key in a 64-entry LDS buffer, and when the
-// buffer would overflow merges it into its sorted top-k (bitonic sort of the
-// buffer across lanes, then both lists placed by rank with binary searches).
-// topk_merge_kernel: one wave per row, the same rank merge of two sorted lists.
+// knn_kernel: a workgroup of 8 waves serves 32 consecutive query rows, 4 per
+// wave (their coordinates and thresholds are wave-uniform scalars). Candidates
+// are staged through LDS in tiles of 2048 as (x, y, z, group) and shared by the
+// 8 waves; tiles are visited starting at the one that holds the queries
+// themselves when they are candidates (their sequence neighbours are close in
+// space, which makes the thresholds tight early; the result does not depend on
+// the order). A lane takes one candidate per 64-candidate step and computes its
+// distance to the 4 queries; a step goes further for a query only when some
+// lane's distance bits do not exceed the high word of that query's current
+// k-th key (an exact prefilter: the bits of a non-negative float order like
+// the float, and the key orders by d2 first). The exact key test then picks
+// the candidates that enter the query's 64-entry LDS buffer. The sorted top-k
+// lives in registers (entry 64s + lane in slot s); a full buffer is sorted
+// (bitonic network across lanes) and merged slot by slot: the lane-wise
+// minimum of a sorted slot and the reversed sorted carry is a bitonic sequence
+// that holds the 64 smallest of the two, the maximum holds the other 64, and
+// one bitonic merge pass sorts each.
+// topk_merge_kernel: one wave per row, a rank merge of two sorted lists.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -26,29 +34,238 @@
 namespace dcp {
 namespace {
 
-constexpr int kKnnWaves = 16;
-constexpr int kTile = 2048;  // candidates per LDS tile
+constexpr int kKnnWaves = 8;
+constexpr int kKnnQ = 4;                          // query rows per wave
+constexpr int kKnnRows = kKnnWaves * kKnnQ;       // query rows per workgroup
+constexpr int kTile = 2048;                       // candidates per LDS tile
 constexpr uint64_t kNoKey = ~0ULL;
 
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
-  const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m);
-  const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m);
+// Value of lane (lane ^ M).
+template <int M>
+__device__ __forceinline__ uint32_t xor_lane(uint32_t x) {
+  if constexpr (M == 1) return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, true);
+  if constexpr (M == 2) return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x4E, 0xF, 0xF, true);
+  if constexpr (M == 4) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x101F);
+  if constexpr (M == 8) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x201F);
+  if constexpr (M == 16) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x401F);
+  if constexpr (M >= 32) return (uint32_t)__shfl_xor((int)x, M);
+}
+
+template <int M>
+__device__ __forceinline__ uint64_t xor_lane64(uint64_t v) {
+  const uint32_t lo = xor_lane<M>((uint32_t)v), hi = xor_lane<M>((uint32_t)(v >> 32));
   return ((uint64_t)hi << 32) | lo;
 }
 
-// Ascending bitonic sort of one key per lane across the wave.
+// One compare-exchange stage of a bitonic network over the wave: lanes whose
+// bit M is clear keep the minimum of the pair when `up`, else the maximum.
+template <int SIZE, int M>
+__device__ __forceinline__ uint64_t bitonic_stage(uint64_t v, int lane) {
+  const uint64_t p = xor_lane64<M>(v);
+  const bool up = SIZE >= 64 || (lane & SIZE) == 0;
+  const bool keep_min = ((lane & M) == 0) == up;
+  return keep_min ? (p < v ? p : v) : (p > v ? p : v);
+}
+
+// Merge pass of size SIZE: sorts every bitonic run of SIZE lanes (ascending
+// runs where bit SIZE of the lane is clear; the whole wave ascending at 64).
+template <int SIZE>
+__device__ __forceinline__ uint64_t bitonic_pass(uint64_t v, int lane) {
+  if constexpr (SIZE > 32) v = bitonic_stage<SIZE, 32>(v, lane);
+  if constexpr (SIZE > 16) v = bitonic_stage<SIZE, 16>(v, lane);
+  if constexpr (SIZE > 8) v = bitonic_stage<SIZE, 8>(v, lane);
+  if constexpr (SIZE > 4) v = bitonic_stage<SIZE, 4>(v, lane);
+  if constexpr (SIZE > 2) v = bitonic_stage<SIZE, 2>(v, lane);
+  return bitonic_stage<SIZE, 1>(v, lane);
+}
+
+// Ascending sort of one key per lane across the wave.
 __device__ __forceinline__ uint64_t wave_sort(uint64_t v, int lane) {
+  v = bitonic_pass<2>(v, lane);
+  v = bitonic_pass<4>(v, lane);
+  v = bitonic_pass<8>(v, lane);
+  v = bitonic_pass<16>(v, lane);
+  v = bitonic_pass<32>(v, lane);
+  return bitonic_pass<64>(v, lane);
+}
+
+__device__ __forceinline__ void wave_lds_sync() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_wave_barrier();
+  asm volatile("" ::: "memory");
+}
+
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// State of one query row: its sorted top-k (KS slots of 64 keys), the number
+// of valid entries, the k-th key, and the LDS buffer of pending keys.
+template <int KS>
+struct QueryTopk {
+  uint64_t top[KS];
+  uint64_t tau;  // keys below tau may enter (kNoKey until k entries exist)
+  int count, bcount;
+  uint64_t* buf;
+  float x, y, z;
+  int32_t g;
+
+  __device__ __forceinline__ void init(uint64_t* b) {
 #pragma unroll
-  for (int size = 2; size <= 64; size <<= 1) {
+    for (int s = 0; s < KS; ++s) top[s] = kNoKey;
+    tau = kNoKey;
+    count = 0;
+    bcount = 0;
+    buf = b;
+  }
+
+  // merge the bcount pending keys into the sorted top-k
+  __device__ __forceinline__ void flush(int lane, int k) {
+    uint64_t carry = lane < bcount ? buf[lane] : kNoKey;
+    carry = wave_sort(carry, lane);
 #pragma unroll
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      const uint64_t p = shfl_xor_u64(v, stride);
-      const bool up = (lane & size) == 0 || size == 64;
-      const bool lower = (lane & stride) == 0;
-      v = (lower == up) ? (p < v ? p : v) : (p > v ? p : v);
+    for (int s = 0; s < KS; ++s) {
+      const uint64_t r = xor_lane64<63>(carry);  // reversed: descending
+      const uint64_t lo = r < top[s] ? r : top[s];
+      const uint64_t hi = r < top[s] ? top[s] : r;
+      top[s] = bitonic_pass<64>(lo, lane);
+      if (s + 1 < KS) carry = bitonic_pass<64>(hi, lane);
+    }
+    count = min(k, count + bcount);
+    bcount = 0;
+    uint64_t last = top[0];  // slot of entry k - 1, chosen without dynamic register indexing
+#pragma unroll
+    for (int s = 1; s < KS; ++s)
+      if (s == ((k - 1) >> 6)) last = top[s];
+    tau = count == k ? readlane64(last, (k - 1) & 63) : kNoKey;
+    wave_lds_sync();  // the buffer has been read before it is refilled
+  }
+
+  // the exact test and the append of one 64-candidate step
+  template <int MODE>
+  __device__ __forceinline__ void offer(uint32_t d2bits, uint32_t index, bool valid, int32_t g_c, int lane,
+                                        int k) {
+    const uint64_t key = ((uint64_t)d2bits << 32) | index;
+    bool take = valid && key < tau;
+    if constexpr (MODE == 1) take = take && g_c == g;
+    if constexpr (MODE == 2) take = take && g_c != g;
+    const uint64_t mask = __ballot(take);
+    if (mask == 0) return;
+    const int n_new = __popcll(mask);
+    if (bcount + n_new > 64) flush(lane, k);
+    const int pos = bcount + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                                            __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+    if (take) buf[pos] = key;
+    wave_lds_sync();
+    bcount += n_new;
+  }
+};
+
+__device__ __forceinline__ float dist2(float qx, float qy, float qz, float4 c) {
+  // the distance is part of the definition: each operation rounded, in this
+  // order, never fused into multiply-adds
+#pragma clang fp contract(off)
+  const float dx = qx - c.x, dy = qy - c.y, dz = qz - c.z;
+  return (dx * dx + dy * dy) + dz * dz;
+}
+
+template <int KS, int MODE>
+__global__ void __launch_bounds__(64 * kKnnWaves) knn_kernel(KnnArgs a) {
+  __shared__ float4 s_c[kTile];  // x, y, z, group bits
+  __shared__ uint64_t s_buf[kKnnWaves][kKnnQ][64];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t r0 = (int64_t)blockIdx.x * kKnnRows;
+  const int64_t rw = r0 + wave * kKnnQ;
+  const int k = a.k;
+
+  QueryTopk<KS> q[kKnnQ];
+#pragma unroll
+  for (int j = 0; j < kKnnQ; ++j) {
+    const int64_t rr = min(rw + j, a.n_q - 1);  // rows past n_q repeat the last one and are not written
+    q[j].init(s_buf[wave][j]);
+    q[j].x = a.x_q[3 * rr];
+    q[j].y = a.x_q[3 * rr + 1];
+    q[j].z = a.x_q[3 * rr + 2];
+    q[j].g = MODE ? a.group_q[rr] : 0;
+  }
+
+  const int64_t n_tiles = (a.n_c + kTile - 1) / kTile;
+  int64_t t0 = 0;
+  if (a.q_self0 >= 0 && n_tiles > 0) t0 = ((a.q_self0 + r0) / kTile) % n_tiles;
+  for (int64_t tt = 0; tt < n_tiles; ++tt) {
+    const int64_t tile = (t0 + tt) % n_tiles;
+    const int64_t c0 = tile * kTile;
+    const int n_here = (int)min((int64_t)kTile, a.n_c - c0);
+    __syncthreads();  // the previous tile has been read by every wave
+    for (int i = threadIdx.x; i < kTile; i += 64 * kKnnWaves) {
+      float4 v;
+      if (i < n_here) {
+        const float* p = a.x_c + 3 * (c0 + i);
+        v = make_float4(p[0], p[1], p[2], __int_as_float(MODE ? a.group_c[c0 + i] : 0));
+      } else {
+        v = make_float4(__builtin_nanf(""), 0.f, 0.f, 0.f);  // never passes the prefilter of a full top-k
+      }
+      s_c[i] = v;
+    }
+    __syncthreads();
+    const uint32_t index0 = (uint32_t)(a.c_index0 + c0);
+    // two steps of 64 candidates at a time; entries past n_here are padding
+    // (NaN distance) that the exact test rejects. In the tile that holds the
+    // wave's own queries the steps start just before them and wrap around, so
+    // their sequence neighbours come first.
+    const int n_pairs = (n_here + 127) >> 7;
+    int pr = 0;
+    if (a.q_self0 >= 0) {
+      const int64_t self = a.q_self0 + rw - c0;
+      if (self >= 0 && self < n_here) pr = max(0, (int)(self >> 7) - 1);
+    }
+    for (int t = 0; t < n_pairs; ++t, pr = pr + 1 == n_pairs ? 0 : pr + 1) {
+      const int s = pr << 7;
+      const float4 ca = s_c[s + lane], cb = s_c[s + 64 + lane];
+      float da[kKnnQ], db[kKnnQ];
+      uint64_t ma[kKnnQ], mb[kKnnQ], any = 0;
+#pragma unroll
+      for (int j = 0; j < kKnnQ; ++j) {
+        da[j] = dist2(q[j].x, q[j].y, q[j].z, ca);
+        db[j] = dist2(q[j].x, q[j].y, q[j].z, cb);
+        const uint32_t th = (uint32_t)(q[j].tau >> 32);
+        ma[j] = __ballot(__float_as_uint(da[j]) <= th);
+        mb[j] = __ballot(__float_as_uint(db[j]) <= th);
+        any |= ma[j] | mb[j];
+      }
+      if (any == 0) continue;
+      // a flush lowers tau after the prefilter: the masks stay a superset
+#pragma unroll
+      for (int j = 0; j < kKnnQ; ++j) {
+        if (ma[j])
+          q[j].template offer<MODE>(__float_as_uint(da[j]), index0 + s + lane, s + lane < n_here,
+                                    __float_as_int(ca.w), lane, k);
+        if (mb[j])
+          q[j].template offer<MODE>(__float_as_uint(db[j]), index0 + s + 64 + lane, s + 64 + lane < n_here,
+                                    __float_as_int(cb.w), lane, k);
+      }
     }
   }
-  return v;
+#pragma unroll
+  for (int j = 0; j < kKnnQ; ++j) {
+    const int64_t r = rw + j;
+    if (r >= a.n_q) break;
+    if (q[j].bcount > 0) q[j].flush(lane, k);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int i = 64 * s + lane;
+      if (i < k) {
+        const bool have = i < q[j].count;
+        const uint64_t t = q[j].top[s];
+        a.idx_out[r * k + i] = have ? (int32_t)(uint32_t)t : -1;
+        if (a.d2_out) a.d2_out[r * k + i] = have ? __uint_as_float((uint32_t)(t >> 32)) : __builtin_inff();
+      }
+    }
+  }
 }
 
 // Number of entries of the sorted a[0, n) that are < x (or <= x when `or_equal`).
@@ -63,117 +280,6 @@ __device__ __forceinline__ int rank_in(const uint64_t* a, int n, uint64_t x, boo
       hi = mid;
   }
   return lo;
-}
-
-__device__ __forceinline__ void wave_lds_sync() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_wave_barrier();
-  asm volatile("" ::: "memory");
-}
-
-template <int KMAX, int MODE>
-__global__ void __launch_bounds__(64 * kKnnWaves) knn_kernel(KnnArgs a) {
-  __shared__ float s_x[kTile], s_y[kTile], s_z[kTile];
-  __shared__ int32_t s_g[MODE ? kTile : 1];
-  __shared__ uint64_t s_top[kKnnWaves][2][KMAX];
-  __shared__ uint64_t s_buf[kKnnWaves][64];
-
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int64_t r0 = (int64_t)blockIdx.x * kKnnWaves;
-  const int64_t r = r0 + wave;
-  const bool active = r < a.n_q;
-  const int64_t rr = active ? r : a.n_q - 1;
-  const float qx = a.x_q[3 * rr], qy = a.x_q[3 * rr + 1], qz = a.x_q[3 * rr + 2];
-  const int32_t qg = MODE ? a.group_q[rr] : 0;
-  const int k = a.k;
-
-  int cur = 0, count = 0, bcount = 0;
-  uint64_t tau = kNoKey;  // keys below tau may enter the top-k
-  uint64_t* buf = s_buf[wave];
-
-  // merge the buffer (bcount unsorted keys) into the sorted top-k
-  auto flush = [&]() {
-    uint64_t v = lane < bcount ? buf[lane] : kNoKey;
-    v = wave_sort(v, lane);
-    wave_lds_sync();
-    buf[lane] = v;
-    wave_lds_sync();
-    const uint64_t* top = s_top[wave][cur];
-    uint64_t* nxt = s_top[wave][cur ^ 1];
-    if (lane < bcount) {
-      const int pos = lane + rank_in(top, count, v, false);
-      if (pos < k) nxt[pos] = v;
-    }
-    for (int i = lane; i < count; i += 64) {
-      const uint64_t t = top[i];
-      const int pos = i + rank_in(buf, bcount, t, true);
-      if (pos < k) nxt[pos] = t;
-    }
-    wave_lds_sync();
-    count = min(k, count + bcount);
-    bcount = 0;
-    cur ^= 1;
-    tau = count == k ? s_top[wave][cur][k - 1] : kNoKey;
-  };
-
-  const int64_t n_tiles = (a.n_c + kTile - 1) / kTile;
-  int64_t t0 = 0;
-  if (a.q_self0 >= 0 && n_tiles > 0) t0 = ((a.q_self0 + r0) / kTile) % n_tiles;
-  for (int64_t tt = 0; tt < n_tiles; ++tt) {
-    const int64_t tile = (t0 + tt) % n_tiles;
-    const int64_t c0 = tile * kTile;
-    const int n_here = (int)min((int64_t)kTile, a.n_c - c0);
-    __syncthreads();  // the previous tile has been read by every wave
-    for (int i = threadIdx.x; i < n_here; i += 64 * kKnnWaves) {
-      const float* p = a.x_c + 3 * (c0 + i);
-      s_x[i] = p[0];
-      s_y[i] = p[1];
-      s_z[i] = p[2];
-      if constexpr (MODE != 0) s_g[i] = a.group_c[c0 + i];
-    }
-    __syncthreads();
-    if (!active) continue;
-    // 64 candidates per step, no branch on the tile tail: lanes past n_here
-    // read stale LDS (inside the tile) and are masked out of `take`
-    auto step = [&](int s) {
-      const int i = s + lane;
-      float d2;
-      {
-        // the distance is part of the definition: each operation rounded, in
-        // this order, never fused into multiply-adds
-#pragma clang fp contract(off)
-        const float dx = qx - s_x[i], dy = qy - s_y[i], dz = qz - s_z[i];
-        d2 = (dx * dx + dy * dy) + dz * dz;
-      }
-      const uint64_t key = ((uint64_t)__float_as_uint(d2) << 32) | (uint32_t)(a.c_index0 + c0 + i);
-      bool take = key < tau && i < n_here;
-      if constexpr (MODE == 1) take = take && s_g[i] == qg;
-      if constexpr (MODE == 2) take = take && s_g[i] != qg;
-      const uint64_t mask = __ballot(take);
-      if (mask == 0) return;
-      const int n_new = __popcll(mask);
-      if (bcount + n_new > 64) flush();
-      const int pos = bcount + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
-                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-      if (take) buf[pos] = key;
-      wave_lds_sync();
-      bcount += n_new;
-    };
-    for (int s = 0; s < n_here; s += 128) {
-      step(s);
-      if (s + 64 < n_here) step(s + 64);
-    }
-  }
-  if (!active) return;
-  if (bcount > 0) flush();
-  const uint64_t* top = s_top[wave][cur];
-  for (int i = lane; i < k; i += 64) {
-    const bool have = i < count;
-    const uint64_t t = have ? top[i] : kNoKey;
-    a.idx_out[r * k + i] = have ? (int32_t)(uint32_t)t : -1;
-    if (a.d2_out) a.d2_out[r * k + i] = have ? __uint_as_float((uint32_t)(t >> 32)) : __builtin_inff();
-  }
 }
 
 // One wave per row: the k smallest keys of two sorted lists (index -1 = empty).
@@ -208,22 +314,22 @@ __global__ void __launch_bounds__(256) topk_merge_kernel(TopkMergeArgs a) {
   }
 }
 
-template <int KMAX>
+template <int KS>
 hipError_t launch_knn_k(const KnnArgs& a, hipStream_t st) {
-  const dim3 grid((unsigned)((a.n_q + kKnnWaves - 1) / kKnnWaves)), block(64 * kKnnWaves);
+  const dim3 grid((unsigned)((a.n_q + kKnnRows - 1) / kKnnRows)), block(64 * kKnnWaves);
   if (a.group_mode == 1)
-    hipLaunchKernelGGL((knn_kernel<KMAX, 1>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((knn_kernel<KS, 1>), grid, block, 0, st, a);
   else if (a.group_mode == 2)
-    hipLaunchKernelGGL((knn_kernel<KMAX, 2>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((knn_kernel<KS, 2>), grid, block, 0, st, a);
   else
-    hipLaunchKernelGGL((knn_kernel<KMAX, 0>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((knn_kernel<KS, 0>), grid, block, 0, st, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_knn(const KnnArgs& a, hipStream_t st) {
-  return a.k <= 128 ? launch_knn_k<128>(a, st) : launch_knn_k<256>(a, st);
+  return a.k <= 128 ? launch_knn_k<2>(a, st) : launch_knn_k<4>(a, st);
 }
 
 hipError_t launch_topk_merge(const TopkMergeArgs& a, hipStream_t st) {

@@ -119,6 +119,16 @@ def test_topk_merge_matches_oracle():
         same((oi.cpu().numpy(), od.cpu().numpy()), ref, f"merge k={k}")
 
 
+def test_ties_on_a_grid_and_duplicates():
+    """Integer coordinates on a 9x9x9 grid: every point repeats about four
+    times and most distances tie, so the order rests on the index rule."""
+    r = np.random.default_rng(11)
+    x = r.integers(-4, 5, (3000, 3)).astype(np.float32)
+    for k in (1, 100, 256):
+        same(gpu_knn(x[:333], x, k, q_self0=0), oracle.knn(x[:333], x, k), f"grid k={k}")
+    same(gpu_knn(x[1:2], x, 7), oracle.knn(x[1:2], x, 7), "one query")
+
+
 def test_short_and_empty_candidate_sets():
     x = synth.coords(synth.KNN_WORKLOADS["knn300"])
     same(gpu_knn(x[:40], x[:30], 64), oracle.knn(x[:40], x[:30], 64), "fewer candidates than k")
