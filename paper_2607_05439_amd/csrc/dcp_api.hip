@@ -675,7 +675,7 @@ int dcp_pair_transition(int64_t n_pairs, int32_t c_z, int32_t hidden, int32_t ac
     a.z_in = z_in;
     a.z_out = z_out;
     a.w_prep = workspace;
-    a.b_prep = reinterpret_cast<float*>(static_cast<char*>(workspace) + (dcp::trans_prep_bytes() - 2 * dcp::kTransHidden * sizeof(float)));
+    a.gb_prep = reinterpret_cast<float*>(static_cast<char*>(workspace) + (dcp::trans_prep_bytes() - 2 * dcp::kTransCz * sizeof(float)));
     a.eps = ln_eps;
     if (g_ev_start && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_start), st)) != hipSuccess)
       return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));

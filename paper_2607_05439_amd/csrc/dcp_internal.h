@@ -187,8 +187,8 @@ struct TransArgs {
   const float *w1, *w2, *w3, *gamma, *beta;
   const void* z_in;    // [n_pairs][128] bf16
   void* z_out;         // may equal z_in
-  void* w_prep;        // operand tiles (trans_prep_bytes(): tiles then biases)
-  float* b_prep;       // [2][512] inside w_prep
+  void* w_prep;        // operand tiles (trans_prep_bytes(): tiles, then gamma and beta)
+  float* gb_prep;      // [2][128] gamma, beta inside w_prep
   float eps;
 };
 

@@ -4,24 +4,28 @@
 // GPU, a fused kernel in which no expanded tensor ever leaves the registers.
 //
 // bf16 path, c_z = 128, hidden = 512 (matrix cores):
-//   trans_prep_kernel  folds gamma into W1 and W2 (beta into per-unit biases),
-//                      rounds the weights to bf16 and writes them as
-//                      matrix-core operand tiles, 12 KB per 16 hidden units
-//                      (W1, W2 for v_mfma_f32_16x16x32_bf16, W3 for
-//                      v_mfma_f32_16x16x16_bf16, its rows permuted so the
-//                      output accumulator lines up with the z channels a lane
-//                      holds).
-//   trans_kernel       one workgroup (4 waves) per CU, persistent over groups
-//                      of 256 pairs (64 per wave). Per group: z loaded once
-//                      (B operands: lane (pair n, group g) holds channels
-//                      32 ks + 8g .. +7), LayerNorm in registers; then for each
-//                      16 hidden units: A = W1' N + b1 and B = W2' N + b2 as
-//                      transposed products (hidden x pairs), h = SiLU(A) * B in
-//                      registers, which is exactly the B operand layout of the
-//                      second product out^T += W3' h^T; finally z + out, bf16,
-//                      stored where z was read. Weight tiles stream through two
-//                      48 KB LDS buffers by direct-to-LDS loads, one chunk of
-//                      64 hidden units ahead.
+//   trans_prep_kernel  rounds the weights to bf16 and writes them as
+//                      matrix-core operand tiles, 24 KB per 32 hidden units
+//                      (W1, W2 and W3 for v_mfma_f32_16x16x32_bf16, W3's rows
+//                      permuted so the output accumulator lines up with the z
+//                      channels a lane holds), and gamma, beta as fp32.
+//   trans_kernel       one workgroup of 8 waves per CU (two per SIMD),
+//                      persistent over groups of 256 pairs, 32 per wave. Per
+//                      group: z (B operands: lane (pair n, group g) holds
+//                      channels 32 ks + 8g .. +7), LayerNorm with gamma and
+//                      beta in registers; then for each 32 hidden units:
+//                      A = W1' N and B = W2 N as transposed products (hidden x
+//                      pairs), h = SiLU(A) * B in registers, which is exactly
+//                      the B operand layout of the second product
+//                      out^T += W3' h^T; finally z + out, bf16, stored where z
+//                      was read. Weight tiles stream through two 48 KB LDS
+//                      buffers by direct-to-LDS loads, one chunk of 64 hidden
+//                      units ahead, and reach the registers through a short
+//                      queue of LDS reads issued a few products early; the
+//                      next group's z is staged into the other 64 KB of LDS
+//                      the same way while this group computes. On this chip
+//                      every 1 KB LDS read also costs matrix-core issue time,
+//                      which is why each weight fragment serves two pair tiles.
 // fp32 path (any c_z <= 256, hidden <= 1024): one wave per pair, plain fp32.
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -40,7 +44,10 @@ constexpr int kTileBytes = 12 * 1024;  // per hidden tile: W1 4 KB, W2 4 KB, W3 
 constexpr int kChunkTiles = 4;          // hidden tiles per LDS chunk (two tile pairs)
 constexpr int kChunks = kHt / kChunkTiles;
 constexpr int kChunkBytes = kChunkTiles * kTileBytes;  // 48 KB
-constexpr int kDmaPerWave = kChunkBytes / 4 / 1024;    // 1 KB DMA instructions per wave per chunk
+constexpr int kWaves = 8;                              // per workgroup, two per SIMD
+constexpr int kWavePairs = 32;                         // pairs per wave: two tiles of 16
+constexpr int kGroupPairs = kWaves * kWavePairs;       // 256
+constexpr int kDmaPerWave = kChunkBytes / 1024 / kWaves;  // 1 KB DMA instructions per wave per chunk
 constexpr float kLog2e = 1.44269504088896340736f;
 
 // Output channel held at accumulator row r (0..15) of output tile ct: tiles
@@ -49,8 +56,8 @@ constexpr float kLog2e = 1.44269504088896340736f;
 __host__ __device__ inline int out_channel(int ct, int r) { return 32 * (ct >> 1) + 8 * (r >> 2) + 4 * (ct & 1) + (r & 3); }
 
 // ----------------------------------------------------------------------------- weight preparation
-// Scaling: W1 (and its bias) carry a factor -log2(e), so the kernel's
-// A' = -log2(e) A gives sigmoid(A) = 1 / (1 + 2^A') with no extra multiply, and
+// Scaling: W1 carries a factor -log2(e), so the kernel's A' = -log2(e) A gives
+// sigmoid(A) = 1 / (1 + 2^A') with no extra multiply, and
 // SiLU(A) B = A B sigmoid(A) = -ln(2) A' B / (1 + 2^A'); the factor -ln(2)
 // goes into W3. Layout per pair of hidden tiles (32 units, 24 KB):
 //   W1 and W2 A operands of v_mfma_f32_16x16x32_bf16 for each of the two
@@ -60,12 +67,14 @@ __host__ __device__ inline int out_channel(int ct, int r) { return 32 * (ct >> 1
 //   16 B (row = channel out_channel(ct, lane%16), k-slot j of lane group g =
 //   unit 4g + j of the first tile for j < 4, of the second for j >= 4, the
 //   order in which the lane holds SiLU(A) B), 8 KB.
+// After the tiles: gamma and beta (fp32, 1 and 0 when absent).
 constexpr int kPairBytes = 2 * kTileBytes;
+constexpr int kPrepFragments = (kHt / 2) * (2 * 2 * 4 * 64 + 8 * 64);  // 16-byte fragments
 __global__ void __launch_bounds__(256) trans_prep_kernel(TransArgs a) {
   const float s1 = -kLog2e, s3 = -0.69314718055994530942f;
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  const int per_pair = 2 * 2 * 4 * 64 + 8 * 64;  // 16-byte fragments per tile pair
-  if (t < (kHt / 2) * per_pair) {
+  const int per_pair = 2 * 2 * 4 * 64 + 8 * 64;
+  if (t < kPrepFragments) {
     const int hp = t / per_pair, f = t % per_pair;
     char* base = static_cast<char*>(a.w_prep) + (size_t)hp * kPairBytes;
     bf16x8 v;
@@ -75,7 +84,7 @@ __global__ void __launch_bounds__(256) trans_prep_kernel(TransArgs a) {
       const float sc = mat ? 1.0f : s1;
       const int unit = 16 * (2 * hp + tile) + (lane & 15), c0 = 32 * ks + 8 * (lane >> 4);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = (__bf16)(w[unit * kCz + c0 + i] * (a.gamma ? a.gamma[c0 + i] : 1.0f) * sc);
+      for (int i = 0; i < 8; ++i) v[i] = (__bf16)(w[unit * kCz + c0 + i] * sc);
       *reinterpret_cast<u32x4*>(base + tile * 8192 + mat * 4096 + ks * 1024 + lane * 16) = __builtin_bit_cast(u32x4, v);
     } else {
       const int f3 = f - 1024, ct = f3 / 64, lane = f3 % 64, g = lane >> 4;
@@ -88,168 +97,200 @@ __global__ void __launch_bounds__(256) trans_prep_kernel(TransArgs a) {
       *reinterpret_cast<u32x4*>(base + 16384 + ct * 1024 + lane * 16) = __builtin_bit_cast(u32x4, v);
     }
   }
-  // biases b1 = -log2(e) W1 beta, b2 = W2 beta (fp32, per hidden unit)
-  const int u = t - (kHt / 2) * per_pair;
-  if (u >= 0 && u < 2 * kHid) {
-    const int mat = u / kHid, unit = u % kHid;
-    const float* w = mat ? a.w2 : a.w1;
-    float s = 0.0f;
-    if (a.beta)
-      for (int c = 0; c < kCz; ++c) s = fmaf(w[unit * kCz + c], a.beta[c], s);
-    a.b_prep[u] = mat ? s : s * s1;
-  }
+  const int u = t - kPrepFragments;
+  if (u >= 0 && u < 2 * kCz)
+    a.gb_prep[u] = u < kCz ? (a.gamma ? a.gamma[u] : 1.0f) : (a.beta ? a.beta[u - kCz] : 0.0f);
 }
 
 // ----------------------------------------------------------------------------- fused transition
-__global__ void __launch_bounds__(256, 1) trans_kernel(TransArgs a) {
-  __shared__ __attribute__((aligned(16))) char s_w[2][kChunkBytes];  // 96 KB
-  __shared__ __attribute__((aligned(16))) float s_b[2 * kHid];        // b1, b2
+__global__ void __launch_bounds__(64 * kWaves) trans_kernel(TransArgs a) {
+  __shared__ __attribute__((aligned(16))) char s_w[2][kChunkBytes];        // 96 KB of weights
+  __shared__ __attribute__((aligned(16))) u32x4 s_z[kWaves][8][64];        // 64 KB: next group's z
   const int tid = threadIdx.x, lane = tid & 63, n = lane & 15, g = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int64_t n_groups = (a.n_pairs + 255) / 256;
+  const int64_t n_groups = (a.n_pairs + kGroupPairs - 1) / kGroupPairs;
   const __amdgpu_buffer_rsrc_t wres =
       __builtin_amdgcn_make_buffer_rsrc(a.w_prep, 0, kHt * kTileBytes, kRawBufferFlags);
-  // chunk c of the weights (48 KB) into LDS buffer b: this wave's 12 KB quarter
+  // chunk c of the weights (48 KB) into LDS buffer b: this wave's 6 KB eighth
   auto chunk_dma = [&](int c, int b) {
     const uint32_t base = lds_addr(&s_w[b][0]) + (uint32_t)(wave * kDmaPerWave * 1024);
 #pragma unroll
     for (int i = 0; i < kDmaPerWave; ++i)
       dma_b128(wres, c * kChunkBytes + (wave * kDmaPerWave + i) * 1024 + lane * 16, base + (uint32_t)(i * 1024));
   };
+  // z of this wave's 32 pairs of group gr, slot i = 4p + ks: lane (n, g) gets
+  // pair 16p + n, channels 32 ks + 8g .. +7 (the B operand it needs), at
+  // s_z[wave][i][lane]; pairs past n_pairs read as zeros (buffer range check)
+  auto z_rsrc = [&](int64_t gr) {
+    const int64_t pair0 = gr * kGroupPairs + wave * kWavePairs;
+    const int64_t left = (a.n_pairs - pair0) * (int64_t)(kCz * 2);  // negative past the end: no records
+    const uint32_t bytes = (uint32_t)max((int64_t)0, min(left, (int64_t)(kWavePairs * kCz * 2)));
+    return __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(static_cast<const uint16_t*>(a.z_in) + pair0 * kCz), 0, (int)bytes, kRawBufferFlags);
+  };
+  auto z_dma = [&](__amdgpu_buffer_rsrc_t zr, int i) {
+    const int p = i >> 2, ks = i & 3;
+    dma_b128(zr, (16 * p + n) * (kCz * 2) + (32 * ks + 8 * g) * 2, lds_addr(&s_z[wave][i][0]));
+  };
 
   int64_t grp = blockIdx.x;
   if (grp >= n_groups) return;  // whole workgroup, before any barrier
-  // biases in LDS, so the chunk loop issues no global loads of its own (their
-  // waits would also wait for the weight loads in flight)
-  for (int i = tid; i < 2 * kHid; i += 256) s_b[i] = a.b_prep[i];
-  __syncthreads();
+  {
+    const __amdgpu_buffer_rsrc_t zr = z_rsrc(grp);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) z_dma(zr, i);
+  }
   chunk_dma(0, 0);
+  wait_vm<kDmaPerWave>();  // the first group's z has landed (each wave reads only its own slots)
   int seq = 0;  // chunk sequence number across groups (buffer = seq & 1)
-  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
   for (; grp < n_groups; grp += gridDim.x) {
     const bool last_group = grp + gridDim.x >= n_groups;
-    // z of this wave's 4 pair tiles: lane (n, g) holds pair 16p + n, channels 32 ks + 8g .. +7
-    const int64_t pair0 = grp * 256 + wave * 64;
-    // z is read twice: here for the LayerNorm and again for the residual at
-    // the end of the group (a few microseconds later, from L2), so that its
-    // registers are free while the products run
-    auto load_z = [&](u32x4 (&zz)[4][4]) {
+    const int64_t pair0 = grp * kGroupPairs + wave * kWavePairs;
+    // LayerNorm of the staged z (two passes over the pair's 128 channels: 32
+    // per lane, 4 lanes), then gamma and beta (from global memory: small and
+    // cached)
+    bf16x8 nv[2][4];
+    {
+      float x[2][4][8], rstd[2];
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const int64_t pr = min(pair0 + 16 * p + n, a.n_pairs - 1);
-        const u32x4* src = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.z_in) + pr * kCz + 8 * g);
+      for (int p = 0; p < 2; ++p) {
+        float s = 0.0f;
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) zz[p][ks] = src[4 * ks];
+        for (int ks = 0; ks < 4; ++ks) {
+          const u32x4 zz = s_z[wave][4 * p + ks][lane];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const uint32_t w = zz[i >> 1];
+            x[p][ks][i] = __uint_as_float((i & 1) ? (w & 0xFFFF0000u) : (w << 16));
+            s += x[p][ks][i];
+          }
+        }
+        const float mu = sum4(s) * (1.0f / kCz);
+        float v = 0.0f;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            x[p][ks][i] -= mu;
+            v = fmaf(x[p][ks][i], x[p][ks][i], v);
+          }
+        rstd[p] = __builtin_amdgcn_rsqf(sum4(v) * (1.0f / kCz) + a.eps);
       }
-    };
-    u32x4 zr[4][4];
-    load_z(zr);
-    // LayerNorm (two passes over the pair's 128 channels: 32 per lane, 4 lanes)
-    bf16x8 nv[4][4];
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      float x[4][8], s = 0.0f;
+      for (int ks = 0; ks < 4; ++ks) {
+        const int c0 = 32 * ks + 8 * g;
+        const float4 ga = *reinterpret_cast<const float4*>(a.gb_prep + c0);
+        const float4 gb = *reinterpret_cast<const float4*>(a.gb_prep + c0 + 4);
+        const float4 ba = *reinterpret_cast<const float4*>(a.gb_prep + kCz + c0);
+        const float4 bb = *reinterpret_cast<const float4*>(a.gb_prep + kCz + c0 + 4);
+        const float gm[8] = {ga.x, ga.y, ga.z, ga.w, gb.x, gb.y, gb.z, gb.w};
+        const float bt[8] = {ba.x, ba.y, ba.z, ba.w, bb.x, bb.y, bb.z, bb.w};
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
+        for (int p = 0; p < 2; ++p)
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const uint32_t w = zr[p][ks][i >> 1];
-          x[ks][i] = __uint_as_float((i & 1) ? (w & 0xFFFF0000u) : (w << 16));
-          s += x[ks][i];
-        }
-      const float mu = sum4(s) * (1.0f / kCz);
-      float v = 0.0f;
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          x[ks][i] -= mu;
-          v = fmaf(x[ks][i], x[ks][i], v);
-        }
-      const float rstd = __builtin_amdgcn_rsqf(sum4(v) * (1.0f / kCz) + a.eps);
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) nv[p][ks][i] = (__bf16)(x[ks][i] * rstd);
+          for (int i = 0; i < 8; ++i) nv[p][ks][i] = (__bf16)fmaf(x[p][ks][i] * rstd[p], gm[i], bt[i]);
+      }
     }
-    f32x4 acc[8][4];  // out^T: output tile ct, pair tile p
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+    f32x4 acc[8][2];  // out^T: output tile ct, pair tile p
 #pragma unroll
     for (int ct = 0; ct < 8; ++ct)
 #pragma unroll
-      for (int p = 0; p < 4; ++p) acc[ct][p] = zero;
+      for (int p = 0; p < 2; ++p) acc[ct][p] = zero;
 
-    auto run_chunk = [&](int c, bool last_chunk, u32x4 (&zres)[4][4]) {
+    bf16x8 hv[2];
+    // h' = A' B / (1 + 2^A') of one tile pair, as the B operand over its 32
+    // units (k-slot j: unit 4g + j of tile 0 for j < 4, of tile 1 for j >= 4)
+    auto silu = [&](const f32x4 (&ha)[2][2], const f32x4 (&hb)[2][2]) {
+#pragma unroll
+      for (int p = 0; p < 2; ++p)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float x = ha[j >> 2][p][j & 3];
+          hv[p][j] = (__bf16)(x * hb[j >> 2][p][j & 3] * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x)));
+        }
+    };
+    // the residual's z: global memory again (recently staged, so mostly from
+    // L2), issued in the last chunk once the normalised z is dead
+    u32x4 zres[2][4];
+    auto load_zres = [&]() {
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        const int64_t pr = min(pair0 + 16 * p + n, a.n_pairs - 1);
+        const u32x4* src = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.z_in) + pr * kCz + 8 * g);
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) zres[p][ks] = src[4 * ks];
+      }
+    };
+    const bool stage_next = !last_group;
+    const __amdgpu_buffer_rsrc_t znext = z_rsrc(stage_next ? grp + gridDim.x : grp);
+    f32x4 h[2][2][2];  // first products of one tile pair: [W1' | W2][tile][pair tile]
+    for (int c = 0; c < kChunks; ++c) {
       const int b = seq & 1;
       barrier_lds();  // every wave is done with buffer b ^ 1 (the previous chunk)
       const bool more = c + 1 < kChunks || !last_group;
       if (more) chunk_dma((c + 1) % kChunks, b ^ 1);
-      if (more)
-        wait_vm<kDmaPerWave>();  // this wave's loads of chunk c have landed
-      else
+      // the next group's z, staged over chunks 0..6 (two slots in chunk 0),
+      // after this chunk's weight loads so that the wait below does not
+      // include it; everything staged has landed by chunk 7's wait
+      if (stage_next && c < 7) {
+        if (c == 0) z_dma(znext, 0);
+        z_dma(znext, c + 1);
+      }
+      if (!more)
         wait_vm<0>();
+      else if (stage_next && c == 0)
+        wait_vm<kDmaPerWave + 2>();  // this wave's loads of chunk c have landed
+      else if (stage_next && c < 7)
+        wait_vm<kDmaPerWave + 1>();
+      else
+        wait_vm<kDmaPerWave>();
       barrier_lds();  // and every other wave's
       const char* chunk = s_w[b];
-      // first products of tile pair q: A' = W1' N + b1', B = W2' N + b2
-      // (rows: hidden units 16 ht + 4g + i; columns: pairs), tiles ht = 2q', 2q'+1
-      auto first = [&](int q, f32x4 (&ha)[2][4], f32x4 (&hb)[2][4]) {
-        const char* pr = chunk + q * kPairBytes;
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt) {
-          const int ht = (c * kChunkTiles / 2 + q) * 2 + tt;
-          const float4 b1 = *reinterpret_cast<const float4*>(s_b + 16 * ht + 4 * g);
-          const float4 b2 = *reinterpret_cast<const float4*>(s_b + kHid + 16 * ht + 4 * g);
-#pragma unroll
-          for (int p = 0; p < 4; ++p) {
-            ha[tt][p] = f32x4{b1.x, b1.y, b1.z, b1.w};
-            hb[tt][p] = f32x4{b2.x, b2.y, b2.z, b2.w};
-          }
-#pragma unroll
-          for (int ks = 0; ks < 4; ++ks) {
-            const bf16x8 w1 = as_bf16x8(*reinterpret_cast<const u32x4*>(pr + tt * 8192 + ks * 1024 + lane * 16));
-            const bf16x8 w2 = as_bf16x8(*reinterpret_cast<const u32x4*>(pr + tt * 8192 + 4096 + ks * 1024 + lane * 16));
-#pragma unroll
-            for (int p = 0; p < 4; ++p) {
-              ha[tt][p] = mfma32(w1, nv[p][ks], ha[tt][p]);
-              hb[tt][p] = mfma32(w2, nv[p][ks], hb[tt][p]);
-            }
-          }
-        }
+      // The chunk's 48 weight fragments (1 KB per wave each) in use order:
+      // per tile pair q, 16 first-product fragments (tile tt, k-step ks,
+      // matrix W1'/W2), then 8 W3'' fragments (output tile ct). They are
+      // read from LDS kAhead fragments before their products, through a
+      // queue of registers, so the LDS latency stays off the critical path.
+      constexpr int kFrags = 2 * 24;
+      constexpr int kAhead = 4;
+      auto frag = [&](int f) {
+        const int q = f / 24, r = f % 24;
+        const int off = r < 16 ? (r >> 3) * 8192 + (r & 1) * 4096 + ((r >> 1) & 3) * 1024 : 16384 + (r - 16) * 1024;
+        return *reinterpret_cast<const u32x4*>(chunk + q * kPairBytes + off + lane * 16);
       };
-      // h' = A' B / (1 + 2^A') as the B operand over the 32 units of the pair
-      // (k-slot j: unit 4g + j of tile 0 for j < 4, of tile 1 for j >= 4), then
-      // out^T += W3'' h'^T
-      auto second = [&](int q, const f32x4 (&ha)[2][4], const f32x4 (&hb)[2][4]) {
-        bf16x8 hv[4];
+      u32x4 wq[kAhead];
 #pragma unroll
-        for (int p = 0; p < 4; ++p)
+      for (int f = 0; f < kAhead; ++f) wq[f] = frag(f);
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const float x = ha[j >> 2][p][j & 3];
-            hv[p][j] = (__bf16)(x * hb[j >> 2][p][j & 3] * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x)));
+      for (int f = 0; f < kFrags; ++f) {
+        const bf16x8 w = as_bf16x8(wq[f % kAhead]);
+        if (f + kAhead < kFrags) wq[f % kAhead] = frag(f + kAhead);
+        const int r = f % 24;
+        if (r < 16) {
+          // A' = W1' N or B = W2 N (rows: hidden units 16 ht + 4g + i; columns: pairs)
+          const int tt = r >> 3, ks = (r >> 1) & 3, m = r & 1;
+#pragma unroll
+          for (int p = 0; p < 2; ++p) h[m][tt][p] = mfma32(w, nv[p][ks], ks == 0 ? zero : h[m][tt][p]);
+        } else {
+          if (r == 16) {
+            silu(h[0], h[1]);
+            if (c == kChunks - 1 && f == 40) load_zres();  // the residual's z, once the normalised z is dead
           }
-        const char* pr = chunk + q * kPairBytes + 16384;
+          // out^T += W3'' h'^T
 #pragma unroll
-        for (int ct = 0; ct < 8; ++ct) {
-          const bf16x8 w3 = as_bf16x8(*reinterpret_cast<const u32x4*>(pr + ct * 1024 + lane * 16));
-#pragma unroll
-          for (int p = 0; p < 4; ++p) acc[ct][p] = mfma32(w3, hv[p], acc[ct][p]);
+          for (int p = 0; p < 2; ++p) acc[r - 16][p] = mfma32(w, hv[p], acc[r - 16][p]);
         }
-      };
-      f32x4 ha0[2][4], hb0[2][4], ha1[2][4], hb1[2][4];
-      first(0, ha0, hb0);
-      first(1, ha1, hb1);
-      if (last_chunk) load_z(zres);  // the residual's z, issued once the normalised z is dead
-      second(0, ha0, hb0);
-      second(1, ha1, hb1);
+        // keep each step's read where it is: the compiler would otherwise
+        // move the reads next to their uses
+        __builtin_amdgcn_sched_barrier(0);
+      }
       ++seq;
-    };
-    u32x4 zres[4][4];
-    for (int c = 0; c < kChunks - 1; ++c) run_chunk(c, false, zres);
-    run_chunk(kChunks - 1, true, zres);
+    }
     // residual and store: accumulator (ct = 2 ks + s, register i) is channel
     // 32 ks + 8g + 4s + i, element 4s + i of the lane's loaded chunk ks
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
+    for (int p = 0; p < 2; ++p) {
       const int64_t pr = pair0 + 16 * p + n;
       if (pr >= a.n_pairs) continue;
       u32x4* dst = reinterpret_cast<u32x4*>(static_cast<uint16_t*>(a.z_out) + pr * kCz + 8 * g);
@@ -311,16 +352,16 @@ __global__ void __launch_bounds__(256) trans_gen_kernel(TransGenArgs a) {
 
 }  // namespace
 
-size_t trans_prep_bytes() { return (size_t)kHt * kTileBytes + 2 * kHid * sizeof(float); }
+size_t trans_prep_bytes() { return (size_t)kHt * kTileBytes + 2 * kCz * sizeof(float); }
 
 hipError_t launch_transition(const TransArgs& a, hipStream_t st) {
-  const int prep_threads = (kHt / 2) * (2 * 2 * 4 * 64 + 8 * 64) + 2 * kHid;
+  const int prep_threads = kPrepFragments + 2 * kCz;
   hipLaunchKernelGGL(trans_prep_kernel, dim3((prep_threads + 255) / 256), dim3(256), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t n_groups = (a.n_pairs + 255) / 256;
-  const int64_t grid = n_groups < 256 ? n_groups : 256;
-  hipLaunchKernelGGL(trans_kernel, dim3((unsigned)grid), dim3(256), 0, st, a);
+  const int64_t n_groups = (a.n_pairs + kGroupPairs - 1) / kGroupPairs;
+  const int64_t grid = n_groups < 256 ? n_groups : 256;  // one persistent workgroup per CU
+  hipLaunchKernelGGL(trans_kernel, dim3((unsigned)grid), dim3(64 * kWaves), 0, st, a);
   return hipGetLastError();
 }
 
