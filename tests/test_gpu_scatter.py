@@ -61,6 +61,67 @@ def test_any_order_is_bit_identical():
     assert np.array_equal(pool(a, idx, n_tok), base)
 
 
+def ordered_case(name):
+    """Atoms in token order (the usual layout), with the structures a run-based
+    reduction has to stitch together: tokens across run boundaries, gaps,
+    out-of-range indices, long runs."""
+    r = np.random.default_rng(len(name))
+    if name == "gaps_and_out_of_range":
+        n_tok, c = 400, 72
+        idx = np.sort(np.concatenate([r.integers(-3, 0, 40), r.choice(np.arange(400)[::3], 900),
+                                      r.integers(400, 405, 30)])).astype(np.int32)
+    elif name == "one_token_over_many_runs":
+        n_tok, c = 50, 128
+        idx = np.sort(np.concatenate([np.full(3000, 7), r.integers(0, 50, 500), np.full(1000, 49)])).astype(np.int32)
+    elif name == "long_runs":  # more than 64 atoms per token on average: runs of 384 atoms
+        n_tok, c = 3, 512
+        idx = np.sort(r.integers(0, 3, 1000)).astype(np.int32)
+    elif name == "run_boundaries":  # tokens of exactly 64 and 65 atoms, aligned and not
+        n_tok, c = 40, 64
+        idx = np.repeat(np.arange(40), [64, 65, 1, 63] * 10).astype(np.int32)
+    elif name == "single_atom":
+        n_tok, c = 5, 8
+        idx = np.array([2], dtype=np.int32)
+    elif name == "odd_channel_count":
+        n_tok, c = 30, 33
+        idx = np.sort(r.integers(0, 30, 200)).astype(np.int32)
+    else:  # all out of range
+        n_tok, c = 6, 16
+        idx = np.array([-1, -1, 6, 9], dtype=np.int32)
+    a = (r.standard_normal((len(idx), c)) * 3).astype(np.float32)
+    return a, idx, n_tok
+
+
+@pytest.mark.parametrize("name", ["gaps_and_out_of_range", "one_token_over_many_runs", "long_runs", "run_boundaries",
+                                  "single_atom", "all_out_of_range", "odd_channel_count"])
+def test_ordered_atoms_match_oracle_and_shuffled_atoms(name):
+    """Ordered atoms against the oracle, and bit for bit against a shuffled
+    copy of the same atoms."""
+    a, idx, n_tok = ordered_case(name)
+    assert np.all(np.diff(idx) >= 0)
+    got = pool(a, idx, n_tok)
+    ref = oracle.scatter_mean(a, idx, n_tok)
+    err = rel_err(got, ref) if np.abs(ref).max() > 0 else float(np.abs(got).max())
+    log(f"case ordered {name}: {len(idx)} atoms, {n_tok} tokens, rel err {err:.3e}")
+    assert err <= 1e-6
+    present = np.zeros(n_tok, bool)
+    present[idx[(idx >= 0) & (idx < n_tok)]] = True
+    assert np.all(got[~present] == 0.0)
+    if len(idx) > 1:
+        p = np.random.default_rng(1).permutation(len(idx))
+        while np.all(np.diff(idx[p]) >= 0):
+            p = np.random.default_rng(int(p[0]) + 2).permutation(len(idx))
+        assert np.array_equal(pool(a[p], idx[p], n_tok), got)
+    assert np.array_equal(pool(a, idx, n_tok, DCP_BF16), pool(a[::-1][::-1].copy(), idx, n_tok, DCP_BF16))
+    # bf16 features (rows of 2c bytes) through the same paths
+    ab = synth.bf16_round(a)
+    got_b = pool(ab, idx, n_tok)
+    ref_b = oracle.scatter_mean(ab, idx, n_tok)
+    assert (rel_err(got_b, ref_b) if np.abs(ref_b).max() > 0 else float(np.abs(got_b).max())) <= 1e-6
+    if len(idx) > 1:
+        assert np.array_equal(pool(ab[p], idx[p], n_tok), got_b)
+
+
 @pytest.mark.parametrize("c", [1, 63, 65, 300, 512])
 def test_channel_counts_and_edge_indices(c):
     r = np.random.default_rng(c)
