@@ -114,6 +114,28 @@ int dcp_pair_bias_attention(const dcp_shape* shape, const dcp_weights* weights, 
                             int32_t n_key_blocks, void* out, void* workspace, size_t workspace_bytes,
                             void* stream);
 
+/* One ring step (Appendix "Q/K/V layout and the ring loop": a query stripe
+ * against the key block visiting this rank; the 2D scheme's inner loop): the
+ * partial attention state of query rows [q_row0, q_row0 + n_q) over the keys
+ * [k0, k1) only, for merging with dcp_block_merge. Arguments as for
+ * dcp_pair_bias_attention, with k0, k1 in place of n_key_blocks and:
+ *   m_out    [H, n_q] fp32: a reference logit in natural-log units, at least
+ *            the largest logit of the row and head over the range (the fused
+ *            path rounds it up to a whole number of base-2 units); -inf when
+ *            the range holds no unmasked key
+ *   l_out    [H, n_q] fp32: sum over the range of exp(logit - m)
+ *   acc_out  [n_q, H, d] fp32: sum over the range of exp(logit - m) v_j
+ *   gate_out [n_q, H*d] fp32 sigmoid(W_g s_i), or NULL
+ * Merging the partials of ranges that cover [0, N) with gate_out as the gate
+ * gives dcp_pair_bias_attention's output. Needs dcp_workspace_size(shape,
+ * n_q, 1) bytes of workspace. 0 <= k0 <= k1 <= N; k0 = k1 gives the empty
+ * state (-inf, 0, 0). The output buffers must not overlap the inputs or the
+ * workspace. */
+int dcp_pair_bias_attention_partial(const dcp_shape* shape, const dcp_weights* weights, const void* s,
+                                    const void* z_rows, const uint8_t* key_mask, int64_t q_row0, int64_t n_q,
+                                    int64_t k0, int64_t k1, float* m_out, float* l_out, float* acc_out,
+                                    float* gate_out, void* workspace, size_t workspace_bytes, void* stream);
+
 /* The pair bias alone (Methods, "RFDiffusion 3 preliminaries and notation":
  * B = f_B(Z)), materialised: bias_out[r, c, h] = sum_k W_b[h,k] LN(z_tile[r, c, :])_k + b_b[h]
  * including gamma, beta and b_b, for r < n_rows, c < n_cols. Pair (r, c) is

@@ -134,38 +134,16 @@ int check_call(const dcp_shape* sh, int64_t n_q, int32_t n_kb, Path* path) {
 
 }  // namespace
 
-extern "C" {
-
-const char* dcp_last_error(void) { return g_err; }
-
-const char* dcp_version(void) { return "dcp-mi355x 0.1 (gfx950)"; }
-
-int dcp_set_timing_events(void* start_event, void* stop_event) {
-  if ((start_event == nullptr) != (stop_event == nullptr))
-    return fail(DCP_ERR_INVALID_ARGUMENT, "timing events must both be set or both be NULL");
-  g_ev_start = start_event;
-  g_ev_stop = stop_event;
-  return ok();
-}
-
-int dcp_workspace_size(const dcp_shape* shape, int64_t n_q, int32_t n_key_blocks, size_t* bytes) {
-  if (!bytes) return fail(DCP_ERR_INVALID_ARGUMENT, "bytes is NULL");
-  Path path;
-  const int rc = check_call(shape, n_q, n_key_blocks, &path);
-  if (rc) return rc;
-  if (n_q == 0) {
-    *bytes = 0;
-    return ok();
-  }
-  Layout L;
-  make_layout(shape, path, n_q, n_key_blocks, &L);
-  *bytes = L.total;
-  return ok();
-}
-
-int dcp_pair_bias_attention(const dcp_shape* shape, const dcp_weights* w, const void* s, const void* z_rows,
-                            const uint8_t* key_mask, int64_t q_row0, int64_t n_q, int32_t n_key_blocks, void* out,
-                            void* workspace, size_t workspace_bytes, void* stream) {
+// Shared by the full call and the one-range partial: projections, the
+// attention over keys [k_lo, k_lo + k_len) in n_key_blocks blocks, then the
+// merge (into out, or into the partial state when `part` is set).
+struct PartialOut {
+  float *m, *l, *acc, *gate;
+};
+static int run_attention(const dcp_shape* shape, const dcp_weights* w, const void* s, const void* z_rows,
+                         const uint8_t* key_mask, int64_t q_row0, int64_t n_q, int32_t n_key_blocks, int64_t k_lo,
+                         int64_t k_len, void* out, const PartialOut* part, void* workspace, size_t workspace_bytes,
+                         void* stream) {
   Path path;
   int rc = check_call(shape, n_q, n_key_blocks, &path);
   if (rc) return rc;
@@ -175,15 +153,26 @@ int dcp_pair_bias_attention(const dcp_shape* shape, const dcp_weights* w, const 
   if (!w) return fail(DCP_ERR_INVALID_ARGUMENT, "weights is NULL");
   if (!w->w_q || !w->w_k || !w->w_v || !w->w_g || !w->w_b)
     return fail(DCP_ERR_INVALID_ARGUMENT, "w_q, w_k, w_v, w_g and w_b are required");
-  if (!s || !z_rows || !out) return fail(DCP_ERR_INVALID_ARGUMENT, "s, z_rows and out are required");
+  if (!s || !z_rows || (!out && !part)) return fail(DCP_ERR_INVALID_ARGUMENT, "s, z_rows and out are required");
+  if (part && (!part->m || !part->l || !part->acc))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "m_out, l_out and acc_out are required");
   if (n_q == 0) return ok();
-  if (!aligned(s, 16) || !aligned(z_rows, 16) || !aligned(out, 16))
+  if (!aligned(s, 16) || !aligned(z_rows, 16) || (out && !aligned(out, 16)))
     return fail(DCP_ERR_INVALID_ARGUMENT, "s, z_rows and out must be 16-byte aligned");
+  if (part && (!aligned(part->m, 4) || !aligned(part->l, 4) || !aligned(part->acc, 4) ||
+               (part->gate && !aligned(part->gate, 4))))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "m_out, l_out, acc_out and gate_out must be 4-byte aligned");
   if (path == kPathFast && (!aligned(w->w_q, 16) || !aligned(w->w_k, 16) || !aligned(w->w_v, 16) ||
                             !aligned(w->w_g, 16)))
     return fail(DCP_ERR_INVALID_ARGUMENT, "w_q, w_k, w_v and w_g must be 16-byte aligned");
   Layout L;
   make_layout(shape, path, n_q, n_key_blocks, &L);
+  // a key range shorter than N: as many segments as the range allows (fewer
+  // parts than the layout holds, so the same workspace serves)
+  if (path == kPathFast && k_len < shape->n_tokens) {
+    L.n_seg = fast_segments(k_len > 0 ? k_len : 1, n_q, n_key_blocks);
+    L.n_parts = n_key_blocks * L.n_seg;
+  }
   if (!workspace || !aligned(workspace, 256))
     return fail(DCP_ERR_WORKSPACE, "workspace must be a 256-byte aligned device pointer");
   if (workspace_bytes < L.total)
@@ -230,6 +219,8 @@ int dcp_pair_bias_attention(const dcp_shape* shape, const dcp_weights* w, const 
     aa.n_q = n_q;
     aa.nq_pad = L.nq_pad;
     aa.n_pad = L.n_pad;
+    aa.k_lo = k_lo;
+    aa.k_len = k_len;
     aa.n_kb = n_key_blocks;
     aa.n_seg = L.n_seg;
     aa.eps = shape->ln_eps;
@@ -238,7 +229,7 @@ int dcp_pair_bias_attention(const dcp_shape* shape, const dcp_weights* w, const 
     aa.acc_parts = reinterpret_cast<float*>(ws + L.off_acc);
     if (g_ev_start && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_start), st)) != hipSuccess)
       return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
-    if ((e = dcp::launch_fast_attn(aa, st)) != hipSuccess)
+    if (k_len > 0 && (e = dcp::launch_fast_attn(aa, st)) != hipSuccess)
       return fail(DCP_ERR_HIP, "attention launch failed: %s", hipGetErrorString(e));
     if (g_ev_stop && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_stop), st)) != hipSuccess)
       return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
@@ -275,6 +266,8 @@ int dcp_pair_bias_attention(const dcp_shape* shape, const dcp_weights* w, const 
     aa.c_z = shape->c_z;
     aa.n_heads = shape->n_heads;
     aa.head_dim = shape->head_dim;
+    aa.k_lo = k_lo;
+    aa.k_len = k_len;
     aa.n_kb = n_key_blocks;
     aa.eps = shape->ln_eps;
     aa.m_parts = reinterpret_cast<float*>(ws + L.off_m);
@@ -282,26 +275,85 @@ int dcp_pair_bias_attention(const dcp_shape* shape, const dcp_weights* w, const 
     aa.acc_parts = reinterpret_cast<float*>(ws + L.off_acc);
     if (g_ev_start && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_start), st)) != hipSuccess)
       return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
-    if ((e = dcp::launch_gen_attn(aa, st)) != hipSuccess)
+    if (k_len > 0 && (e = dcp::launch_gen_attn(aa, st)) != hipSuccess)
       return fail(DCP_ERR_HIP, "attention launch failed: %s", hipGetErrorString(e));
     if (g_ev_stop && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_stop), st)) != hipSuccess)
       return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));
   }
   dcp::MergeArgs ma{};
-  ma.n_parts = L.n_parts;
+  ma.n_parts = k_len > 0 ? L.n_parts : 0;  // an empty range merges to the empty state
   ma.n_heads = shape->n_heads;
   ma.head_dim = shape->head_dim;
   ma.n_rows = n_q;
   ma.m = reinterpret_cast<const float*>(ws + L.off_m);
   ma.l = reinterpret_cast<const float*>(ws + L.off_l);
   ma.acc = reinterpret_cast<const float*>(ws + L.off_acc);
-  ma.gate = reinterpret_cast<const float*>(ws + L.off_g);
-  ma.out = out;
-  ma.out_bf16 = shape->out_dtype == DCP_BF16;
   ma.log2_units = log2_units;
+  if (part) {
+    ma.m_out = part->m;
+    ma.l_out = part->l;
+    ma.acc_out = part->acc;
+    ma.m_natural = 1;
+    if (part->gate && (e = hipMemcpyAsync(part->gate, ws + L.off_g, (size_t)n_q * hd * sizeof(float),
+                                          hipMemcpyDeviceToDevice, st)) != hipSuccess)
+      return fail(DCP_ERR_HIP, "gate copy failed: %s", hipGetErrorString(e));
+  } else {
+    ma.gate = reinterpret_cast<const float*>(ws + L.off_g);
+    ma.out = out;
+    ma.out_bf16 = shape->out_dtype == DCP_BF16;
+  }
   if ((e = dcp::launch_merge(ma, st)) != hipSuccess)
     return fail(DCP_ERR_HIP, "merge launch failed: %s", hipGetErrorString(e));
   return ok();
+}
+
+extern "C" {
+
+const char* dcp_last_error(void) { return g_err; }
+
+const char* dcp_version(void) { return "dcp-mi355x 0.1 (gfx950)"; }
+
+int dcp_set_timing_events(void* start_event, void* stop_event) {
+  if ((start_event == nullptr) != (stop_event == nullptr))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "timing events must both be set or both be NULL");
+  g_ev_start = start_event;
+  g_ev_stop = stop_event;
+  return ok();
+}
+
+int dcp_workspace_size(const dcp_shape* shape, int64_t n_q, int32_t n_key_blocks, size_t* bytes) {
+  if (!bytes) return fail(DCP_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  Path path;
+  const int rc = check_call(shape, n_q, n_key_blocks, &path);
+  if (rc) return rc;
+  if (n_q == 0) {
+    *bytes = 0;
+    return ok();
+  }
+  Layout L;
+  make_layout(shape, path, n_q, n_key_blocks, &L);
+  *bytes = L.total;
+  return ok();
+}
+
+int dcp_pair_bias_attention(const dcp_shape* shape, const dcp_weights* w, const void* s, const void* z_rows,
+                            const uint8_t* key_mask, int64_t q_row0, int64_t n_q, int32_t n_key_blocks, void* out,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  return run_attention(shape, w, s, z_rows, key_mask, q_row0, n_q, n_key_blocks, 0, shape ? shape->n_tokens : 0, out,
+                       nullptr, workspace, workspace_bytes, stream);
+}
+
+int dcp_pair_bias_attention_partial(const dcp_shape* shape, const dcp_weights* w, const void* s, const void* z_rows,
+                                    const uint8_t* key_mask, int64_t q_row0, int64_t n_q, int64_t k0, int64_t k1,
+                                    float* m_out, float* l_out, float* acc_out, float* gate_out, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  if (!shape) return fail(DCP_ERR_INVALID_ARGUMENT, "shape is NULL");
+  if (k0 < 0 || k1 < k0 || k1 > shape->n_tokens)
+    return fail(DCP_ERR_INVALID_ARGUMENT, "need 0 <= k0 <= k1 <= n_tokens (k0 %lld, k1 %lld)", (long long)k0,
+                (long long)k1);
+  const PartialOut part{m_out, l_out, acc_out, gate_out};
+  return run_attention(shape, w, s, z_rows, key_mask, q_row0, n_q, 1, k0, k1 - k0, nullptr, &part, workspace,
+                       workspace_bytes, stream);
 }
 
 int dcp_bias_project(const dcp_shape* shape, const dcp_weights* w, const void* z_tile, int64_t n_rows, int64_t n_cols,

@@ -11,6 +11,10 @@ namespace dcp {
 constexpr int kFastCz = 128;   // pair channels
 constexpr int kFastH = 16;     // heads
 constexpr int kFastD = 24;     // head dim
+// Logits of the fused path are in base-2 units plus this offset inside the
+// kernel (exact power-of-two rescaling); its partial maxima are written
+// without it
+constexpr float kFastShift = 192.0f;
 constexpr int kFastDp = 32;    // head dim padded to the MFMA k width
 constexpr int kTileQ = 16;     // query rows per wave
 constexpr int kTileK = 16;     // keys per tile
@@ -67,6 +71,7 @@ struct FastAttnArgs {
   const uint16_t *q, *k, *vt;
   const uint32_t* tile_valid;
   int64_t n_tok, n_q, nq_pad, n_pad;
+  int64_t k_lo, k_len;  // keys [k_lo, k_lo + k_len), split into n_kb blocks x n_seg segments
   int32_t n_kb, n_seg;
   float eps;
   float *m_parts, *l_parts, *acc_parts;  // [P][H][n_q], [P][H][n_q], [P][n_q][H][d]
@@ -97,6 +102,7 @@ struct GenAttnArgs {
   const float *w_b, *gamma;
   const float *q, *k, *v;
   int64_t n_tok, n_q;
+  int64_t k_lo, k_len;  // keys [k_lo, k_lo + k_len), split into n_kb blocks
   int32_t c_z, n_heads, head_dim, n_kb;
   float eps;
   float *m_parts, *l_parts, *acc_parts;
@@ -119,7 +125,8 @@ struct MergeArgs {
   float *m_out, *l_out, *acc_out;
   void* out;
   int32_t out_bf16;
-  int32_t log2_units;  // 1: m is in base-2 units with integer differences
+  int32_t log2_units;  // 1: m is in base-2 units with integer differences (the fused path)
+  int32_t m_natural;   // with log2_units: write m_out in natural-log units
 };
 
 // Sparse (kNN) atom attention: the paper's atom-attention shape (4 heads of

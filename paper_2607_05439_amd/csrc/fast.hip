@@ -39,7 +39,7 @@ constexpr float kLog2e = 1.44269504088896340736f;
 // subtraction logit - max is then exact, the softmax weights do not depend on
 // which keys were seen before, and rescaling factors are exact powers of two:
 // key blocks of any size give the same weights.
-constexpr float kShift = 192.0f;
+constexpr float kShift = kFastShift;
 
 // Bias weights as A operands: row = head (lane % 16), k-step s holds channels
 // 32s + 8g .. 32s + 8g + 7. W' = scale * W_b * diag(gamma), centred per head
@@ -301,7 +301,9 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
   const int64_t q0 = (active ? qt : n_qt - 1) * kTileQ;
   const int part = blockIdx.y;
   int64_t start, end;
-  part_range(a.n_tok, a.n_kb, a.n_seg, part, &start, &end);
+  part_range(a.k_len, a.n_kb, a.n_seg, part, &start, &end);
+  start += a.k_lo;
+  end += a.k_lo;
   const int64_t t_begin = start >> 4, t_end = (end + 15) >> 4;
   const int64_t n_tiles_all = a.n_pad / 16;
 

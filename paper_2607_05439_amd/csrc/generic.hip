@@ -82,7 +82,8 @@ __global__ void __launch_bounds__(64) gen_attn_kernel(GenAttnArgs a) {
   __syncthreads();
 
   int64_t size, start;
-  chunk_of(a.n_tok, a.n_kb, part, &size, &start);
+  chunk_of(a.k_len, a.n_kb, part, &size, &start);
+  start += a.k_lo;
   const float scale = 1.0f / sqrtf((float)d);
   const float* qr = a.q + row * hd;
   for (int64_t j = start + lane; j < start + size; j += 64) {

@@ -32,7 +32,9 @@ __global__ void __launch_bounds__(256) merge_kernel(MergeArgs a) {
     }
     if (a.acc_out) a.acc_out[t] = acc;
     if (x % a.head_dim == 0) {
-      if (a.m_out) a.m_out[(int64_t)h * a.n_rows + r] = mx;
+      if (a.m_out)
+        a.m_out[(int64_t)h * a.n_rows + r] =
+            (a.log2_units && a.m_natural && mx != -INFINITY) ? mx * 0.69314718055994530942f : mx;
       if (a.l_out) a.l_out[(int64_t)h * a.n_rows + r] = l;
     }
     if (a.out) {

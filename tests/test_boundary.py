@@ -93,6 +93,28 @@ def test_bad_ranges():
                                              1 << 40, None) == E
 
 
+def partial(sh, k0=0, k1=4000, m=FAKE, l=FAKE, acc=FAKE, gate=0, ws=FAKE, ws_bytes=1 << 40, n_q=24000):
+    return dcp.lib().dcp_pair_bias_attention_partial(ctypes.byref(sh), ctypes.byref(weights()), FAKE, FAKE, None, 0,
+                                                     n_q, k0, k1, m, l, acc, gate, ws, ws_bytes, None)
+
+
+def test_partial_rejections():
+    E = dcp.DCP_ERR_INVALID_ARGUMENT
+    sh = shape()
+    assert partial(sh, k0=-1) == E
+    assert partial(sh, k0=10, k1=9) == E
+    assert partial(sh, k1=24001) == E
+    assert partial(sh, m=0) == E and "m_out" in dcp.dcp_last_error()
+    assert partial(sh, acc=0) == E
+    assert partial(sh, m=FAKE + 2) == E  # misaligned
+    need = dcp.dcp_workspace_size(sh, 24000, 1)
+    assert partial(sh, ws_bytes=need - 1) == dcp.DCP_ERR_WORKSPACE
+    assert partial(sh, n_q=0, ws=0, ws_bytes=0) == dcp.DCP_OK
+    assert dcp.lib().dcp_pair_bias_attention_partial(None, ctypes.byref(weights()), FAKE, FAKE, None, 0, 1, 0, 1, FAKE,
+                                                     FAKE, FAKE, 0, FAKE, 1 << 40, None) == E
+    assert partial(shape(c_z=100), ws_bytes=1 << 40) == dcp.DCP_ERR_UNSUPPORTED
+
+
 def test_bad_workspace():
     sh = shape()
     need = dcp.dcp_workspace_size(sh, 24000, 6)
