@@ -592,8 +592,8 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(see DESIGN.md for how the layer would shard); run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures a single GPU: the library has no multi-GPU path (no collectives or "
+              "sharding across GPUs); run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
