@@ -572,7 +572,7 @@ def scatter_main(args, name):
                    "algorithmic_bytes": alg},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": stored_traffic(name, SCATTER_SOURCES),
-                     "kernel": "scatter (zero + accum + final)", "kernel_ms": round(kms, 5),
+                     "kernel": "pooling (plan + sum; the any-order accumulation and division exit on ordered atoms)", "kernel_ms": round(kms, 5),
                      "algorithmic_bytes_per_launch": alg},
         "cpu_baseline": cpu,
     }

@@ -310,10 +310,16 @@ int dcp_pair_transition(int64_t n_pairs, int32_t c_z, int32_t hidden, int32_t ac
  *
  * Deterministic for any index pattern and on any device: features are summed
  * as 64-bit fixed-point integers (value * 2^32, rounded to nearest), whose
- * addition does not depend on order, then divided by the count in fp64 and
- * rounded to out_dtype. Each feature is clamped to |x| <= 2^30 and each token's
- * sum must stay below 2^31 in magnitude; the absolute rounding of a feature is
- * at most 2^-33. NaN features give unspecified values for their token.
+ * addition does not depend on order, then scaled by 2^-32 and by the count's
+ * reciprocal (1/count rounded to fp64) in fp64 and rounded to out_dtype, so
+ * any permutation of the atoms gives the same bits. Each feature is clamped to
+ * |x| <= 2^30 and each token's sum must stay below 2^31 in magnitude; the
+ * absolute rounding of a feature is at most 2^-33. NaN features give
+ * unspecified values for their token.
+ *
+ * Atoms ordered by token (tok_idx non-decreasing, the model's layout) take a
+ * path without atomics that reads each feature once; the order is checked on
+ * the device, and any other order takes a path with 64-bit integer atomics.
  * ------------------------------------------------------------------------- */
 
 /* Workspace bytes for dcp_scatter_mean (written to *bytes). Host-only. */
@@ -335,7 +341,7 @@ int dcp_scatter_mean(int64_t n_atoms, int64_t n_tokens, int32_t c, int32_t in_dt
  * `start` just before and
  * `stop` just after the main kernel (after any projections; around the
  * weight preparation and the transition kernel of a transition; around all
- * three kernels of a pooling), on that call's stream. Pass NULL, NULL to clear.
+ * kernels of a pooling), on that call's stream. Pass NULL, NULL to clear.
  * Host-only. */
 int dcp_set_timing_events(void* start_event, void* stop_event);
 

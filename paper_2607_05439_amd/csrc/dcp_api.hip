@@ -757,7 +757,8 @@ int dcp_pair_transition(int64_t n_pairs, int32_t c_z, int32_t hidden, int32_t ac
 
 // ----------------------------------------------------------------------------- atom -> token mean
 static size_t scatter_ws(int64_t n_tokens, int32_t c) {
-  return round_up((size_t)n_tokens * c * 8, 256) + round_up((size_t)n_tokens * 4, 256);
+  return round_up((size_t)n_tokens * c * 8, 256) + round_up((size_t)n_tokens * 4, 256) +
+         round_up(dcp::kScatterFlags * sizeof(int32_t), 256) + round_up((size_t)n_tokens * 16, 256);
 }
 
 static int check_scatter(int64_t n_atoms, int64_t n_tokens, int32_t c, int32_t in_dtype, int32_t out_dtype) {
@@ -802,6 +803,8 @@ int dcp_scatter_mean(int64_t n_atoms, int64_t n_tokens, int32_t c, int32_t in_dt
   s.tok_idx = tok_idx;
   s.acc = static_cast<int64_t*>(workspace);
   s.cnt = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + round_up((size_t)n_tokens * c * 8, 256));
+  s.flags = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(s.cnt) + round_up((size_t)n_tokens * 4, 256));
+  s.plan = reinterpret_cast<int64_t*>(reinterpret_cast<char*>(s.flags) + round_up(dcp::kScatterFlags * sizeof(int32_t), 256));
   s.out = out;
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e;

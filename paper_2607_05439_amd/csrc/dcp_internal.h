@@ -212,6 +212,7 @@ size_t trans_prep_bytes();
 
 // Atom -> token mean: up to 512 channels.
 constexpr int kScatterMaxC = 512;
+constexpr int kScatterFlags = 256;  // most order-check flags of one pooling call
 
 struct ScatterArgs {
   int64_t n_atoms, n_tokens;
@@ -221,6 +222,9 @@ struct ScatterArgs {
   int64_t* acc;           // [n_tokens][c] fixed-point sums (workspace)
   uint32_t* cnt;          // [n_tokens] (workspace)
   void* out;              // [n_tokens][c]
+  int32_t* flags;         // [kScatterFlags] order-check flags (workspace); NULL: general path only
+  int32_t n_flags;        // flags written by this call (set by the launcher)
+  int64_t* plan;          // [n_tokens][2] first atom and atom count of each token (workspace)
 };
 
 hipError_t launch_fast_proj(const FastProjArgs& a, hipStream_t st);
@@ -237,5 +241,6 @@ hipError_t launch_topk_merge(const TopkMergeArgs& a, hipStream_t st);
 hipError_t launch_transition(const TransArgs& a, hipStream_t st);
 hipError_t launch_transition_gen(const TransGenArgs& a, hipStream_t st);
 hipError_t launch_scatter_mean(const ScatterArgs& a, hipStream_t st);
+int scatter_order_flags(int64_t n_atoms);  // plan workgroups (one flag each) for n_atoms (<= kScatterFlags)
 
 }  // namespace dcp

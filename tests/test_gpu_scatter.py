@@ -79,6 +79,9 @@ def ordered_case(name):
     elif name == "run_boundaries":  # tokens of exactly 64 and 65 atoms, aligned and not
         n_tok, c = 40, 64
         idx = np.repeat(np.arange(40), [64, 65, 1, 63] * 10).astype(np.int32)
+    elif name == "end_gap_at_tile_edge":  # 128 atoms (two 64-atom tiles exactly), trailing empty tokens
+        n_tok, c = 50, 32
+        idx = np.sort(r.integers(0, 21, 128)).astype(np.int32)
     elif name == "single_atom":
         n_tok, c = 5, 8
         idx = np.array([2], dtype=np.int32)
@@ -93,7 +96,7 @@ def ordered_case(name):
 
 
 @pytest.mark.parametrize("name", ["gaps_and_out_of_range", "one_token_over_many_runs", "long_runs", "run_boundaries",
-                                  "single_atom", "all_out_of_range", "odd_channel_count"])
+                                  "end_gap_at_tile_edge", "single_atom", "all_out_of_range", "odd_channel_count"])
 def test_ordered_atoms_match_oracle_and_shuffled_atoms(name):
     """Ordered atoms against the oracle, and bit for bit against a shuffled
     copy of the same atoms."""
@@ -160,3 +163,66 @@ def test_pool24000_whole_workload():
     log(f"  rel err {err:.3e}")
     assert err <= 1e-6
     assert np.array_equal(pool(a, idx, n_tok), got)
+
+
+@pytest.mark.parametrize("c,bf16", [(8, True), (16, True), (24, True), (40, True), (136, True), (264, True),
+                                    (512, True), (4, False), (12, False), (300, False), (512, False)])
+def test_ordered_row_widths(c, bf16):
+    """Ordered atoms with feature rows of 1 to 128 sixteen-byte chunks (lane
+    groups of every width, and rows split over two slices): against the oracle
+    and bit for bit against a shuffled copy."""
+    r = np.random.default_rng(c + bf16)
+    n_tok = 90
+    idx = np.sort(np.concatenate([r.integers(0, n_tok, 700), [0, n_tok - 1]])).astype(np.int32)
+    idx[idx == 33] = 34  # one empty token inside
+    a = r.standard_normal((len(idx), c)).astype(np.float32)
+    if bf16:
+        a = synth.bf16_round(a)
+    got = pool(a, idx, n_tok)
+    ref = oracle.scatter_mean(a, idx, n_tok)
+    log(f"case ordered width c={c} bf16={bf16}: rel err {rel_err(got, ref):.3e}")
+    assert rel_err(got, ref) <= 1e-6
+    assert np.all(got[33] == 0.0)
+    p = np.random.default_rng(7).permutation(len(idx))
+    assert np.array_equal(pool(a[p], idx[p], n_tok), got)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_wide_magnitudes_every_feature_within_fixed_point_bound(bf16):
+    """Features from 1e-12 to 2^28 in magnitude (rounding of tiny values, the
+    exact conversion for large ones): every output within the fixed-point
+    rounding (2^-33 per feature) plus the output rounding of the oracle's fp64
+    mean, and bit-identical to a shuffled copy (the any-order path)."""
+    r = np.random.default_rng(11 + bf16)
+    n_tok, c = 300, 64
+    idx = np.sort(r.integers(0, n_tok, 700)).astype(np.int32)
+    mag = 10.0 ** r.uniform(-12, 8.4, (len(idx), c))
+    a = np.clip(r.choice([-1.0, 1.0], (len(idx), c)) * mag, -2.0**28, 2.0**28).astype(np.float32)
+    if bf16:
+        a = synth.bf16_round(a)
+    got = pool(a, idx, n_tok).astype(np.float64)
+    ref = oracle.scatter_mean(a, idx, n_tok)
+    bound = 2.0**-33 + 2.0**-24 * np.abs(ref)
+    worst = float(np.max(np.abs(got - ref) / bound))
+    log(f"case wide magnitudes bf16={bf16}: worst error / bound {worst:.3f}")
+    assert worst <= 1.0
+    p = np.random.default_rng(3).permutation(len(idx))
+    assert np.array_equal(pool(a[p], idx[p], n_tok), got.astype(np.float32))
+
+
+def test_one_inversion_takes_the_any_order_path():
+    """A sorted index with one adjacent pair swapped deep inside a long array
+    (one order-check flag of many set): still the exact means, bit-identical
+    to the fully sorted atoms."""
+    r = np.random.default_rng(21)
+    n_tok, c = 9000, 32
+    idx = np.sort(r.integers(0, n_tok, 80000)).astype(np.int32)
+    a = r.standard_normal((len(idx), c)).astype(np.float32)
+    k = int(np.nonzero(np.diff(idx[60000:]) > 0)[0][0]) + 60000  # idx[k] < idx[k + 1]
+    p = np.arange(len(idx))
+    p[k], p[k + 1] = k + 1, k
+    assert np.any(np.diff(idx[p]) < 0)
+    sorted_out = pool(a, idx, n_tok)
+    swapped = pool(a[p], idx[p], n_tok)
+    assert rel_err(swapped, oracle.scatter_mean(a, idx, n_tok)) <= 1e-6
+    assert np.array_equal(swapped, sorted_out)
