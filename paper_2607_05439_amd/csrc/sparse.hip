@@ -342,11 +342,11 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
   constexpr int LPH = kD / EPL;      // lanes per head (4 | 8)
   constexpr int KS = KMAX / 64;      // slots per lane in slot order
   constexpr int kUnroll = 4;         // K (and V) loads per lane per batch
-  constexpr int kBatch = NPI * kUnroll;  // slots per batch (32 | 16)
+  constexpr int kBatch = NPI * kUnroll;  // slots per batch (16 | 8)
   constexpr int kPad = 32;           // list length granularity
   constexpr int kPasses = KMAX / 16; // bias passes of 16 slots
   static_assert(kPad % 16 == 0 && kPad % kBatch == 0 && KMAX % kPad == 0, "list padding");
-  __shared__ uint32_t s_kv[kWaves][KMAX];  // byte offset of the K/V row, or out of range (padding)
+  __shared__ uint32_t s_kv[kWaves][KMAX + kBatch];  // byte offset of the K/V row, or out of range (padding)
   __shared__ uint32_t s_p[kWaves][KMAX];   // byte offset of the pair vector in this query's P row
   __shared__ __attribute__((aligned(16))) float s_b[kWaves][KMAX][kH];  // bias (base-2 units), -inf for padding
 
@@ -433,25 +433,32 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
 #pragma unroll
   for (int e = 0; e < EPL; ++e) acc[e] = 0.0f;
 
-  // one register buffer of K/V rows per batch; the next batch's loads are
-  // issued as soon as this batch's registers are free (more buffers cost
+  // one register buffer of K rows and one of V rows per batch; the next
+  // batch's K rows are requested as soon as this batch's logits are formed and
+  // its V rows as soon as this batch's weighted sum is done (more buffers cost
   // occupancy, which hides the gather latency better)
   u32x4 kw[1][kUnroll], vw[1][kUnroll];
-  auto issue_batch = [&](int buf, int b0) {
-    int off[kUnroll];
+  auto offsets = [&](int b0, int (&off)[kUnroll]) {
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) off[u] = (int)(lkv[b0 + NPI * u + grp] + 16u * c);
-    // K first: the logits can start while V is still arriving
+  };
+  auto issue_k = [&](int buf, const int (&off)[kUnroll]) {
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) kw[buf][u] = __builtin_amdgcn_raw_buffer_load_b128(kres, off[u], 0, 0);
+  };
+  auto issue_v = [&](int buf, const int (&off)[kUnroll]) {
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) vw[buf][u] = __builtin_amdgcn_raw_buffer_load_b128(vres, off[u], 0, 0);
   };
-  // one batch: logits, online softmax (integer maxima, exact power-of-two
-  // rescaling), weighted V
-  auto compute_batch = [&](int buf, int b0) {
-    float lg[kUnroll];
-    float mx = -INFINITY;
+  auto issue_batch = [&](int buf, int b0) {
+    // K first: the logits can start while V is still arriving
+    int off[kUnroll];
+    offsets(b0, off);
+    issue_k(buf, off);
+    issue_v(buf, off);
+  };
+  // one batch: logits (the only use of the K rows) ...
+  auto logits = [&](int buf, int b0, float (&lg)[kUnroll]) {
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       float dot = 0.0f;
@@ -466,8 +473,14 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
         for (int e = 0; e < EPL; ++e) dot = fmaf(qv[e], __uint_as_float(kw[buf][u][e]), dot);
       }
       lg[u] = group_sum<LPH>(dot) + lb[b0 + NPI * u + grp][hl];
-      mx = fmaxf(mx, lg[u]);
     }
+  };
+  // ... then the online softmax (integer maxima, exact power-of-two
+  // rescaling) and the weighted V
+  auto weigh = [&](int buf, const float (&lg)[kUnroll]) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) mx = fmaxf(mx, lg[u]);
     mx = across_max<NPI>(mx);
     const float m_new = fmaxf(m_run, ceilf(mx));
     if (m_new != m_run) {  // lane-varying (per head); only a rescale of the state
@@ -521,10 +534,8 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
       count += __popcll(mask);
     }
     const int count_pad = (count + kPad - 1) / kPad * kPad;
-    if (lane < count_pad - count) {
-      lkv[count + lane] = (uint32_t)kOutOfRange;
-      lp[count + lane] = (uint32_t)kOutOfRange;
-    }
+    if (lane < count_pad - count) lp[count + lane] = (uint32_t)kOutOfRange;
+    if (lane < count_pad - count + kBatch) lkv[count + lane] = (uint32_t)kOutOfRange;  // and one more batch
     wave_lds_sync();
 
     // 2. every pair-vector load of the list, then the first K/V batch, so the
@@ -615,10 +626,24 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
     }
     wave_lds_sync();
 
-    // 3. batches of K/V rows
+    // 3. batches of K/V rows; the requests for the batch after the last one
+    //    read the extra padding of the list (no data), which keeps the number
+    //    of loads in flight the same on every path
+    int prev[kUnroll];  // addresses of the V loads in flight
+    offsets(0, prev);
     for (int b0 = 0; b0 < count_pad; b0 += kBatch) {
-      compute_batch(0, b0);
-      if (b0 + kBatch < count_pad) issue_batch(0, b0 + kBatch);
+      int off[kUnroll];
+      offsets(b0 + kBatch, off);
+      // the loads in flight read their addresses from prev: keep those
+      // registers until the next addresses are in others
+      asm volatile("" ::"v"(prev[0]), "v"(prev[1]), "v"(prev[2]), "v"(prev[3]));
+      float lg[kUnroll];
+      logits(0, b0, lg);
+      issue_k(0, off);
+      weigh(0, lg);
+      issue_v(0, off);
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) prev[u] = off[u];
     }
 
     // next block present among the neighbours
