@@ -226,3 +226,37 @@ def test_one_inversion_takes_the_any_order_path():
     swapped = pool(a[p], idx[p], n_tok)
     assert rel_err(swapped, oracle.scatter_mean(a, idx, n_tok)) <= 1e-6
     assert np.array_equal(swapped, sorted_out)
+
+
+def test_workspace_contents_do_not_matter():
+    """The order flags and the per-token plan are written, never cleared: a
+    workspace full of arbitrary bytes, or one left by a larger call with other
+    atoms, gives the same bits as a fresh one (ordered and shuffled atoms)."""
+    import torch
+    import paper_2607_05439_amd as dcp
+    r = np.random.default_rng(31)
+
+    def call(a, idx, n_tok, ws):
+        out = torch.full((n_tok, a.shape[1]), 7.0, dtype=torch.float32, device="cuda:0")
+        dcp.dcp_scatter_mean(len(idx), n_tok, a.shape[1], DCP_BF16 if a.dtype == np.uint16 else DCP_F32, DCP_F32,
+                             dev(a), dev(idx), out, ws, ws.numel())
+        return out.cpu().numpy()
+
+    n_tok, c = 500, 64
+    idx = np.sort(r.integers(0, n_tok, 4000)).astype(np.int32)
+    idx[idx == 100] = 101  # an empty token
+    a = r.standard_normal((len(idx), c)).astype(np.float32)
+    ref = pool(a, idx, n_tok)
+    ws_bytes = dcp.dcp_scatter_mean_workspace_size(2000, c)
+    for fill in (0xFF, 0x00, 0x7F):
+        ws = torch.full((ws_bytes,), fill, dtype=torch.uint8, device="cuda:0")
+        assert np.array_equal(call(a, idx, n_tok, ws), ref)
+    # a larger ordered call, then an unordered one, then the original, on one workspace
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda:0")
+    idx_big = np.sort(r.integers(0, 2000, 9000)).astype(np.int32)
+    a_big = r.standard_normal((len(idx_big), c)).astype(np.float32)
+    assert rel_err(call(a_big, idx_big, 2000, ws), oracle.scatter_mean(a_big, idx_big, 2000)) <= 1e-6
+    p = r.permutation(len(idx))
+    assert np.array_equal(call(a[p], idx[p], n_tok, ws), ref)
+    assert np.array_equal(call(a, idx, n_tok, ws), ref)
+    assert np.all(ref[100] == 0.0)
