@@ -43,18 +43,6 @@ __device__ __forceinline__ void swap16(float& x, float& y) {
   y = __uint_as_float(r[1]);
 }
 
-// Value of lane (lane ^ M): quad permutes for 1 and 2, bit-mask swizzles for
-// 4 to 16, a full-wave shuffle beyond.
-template <int M>
-__device__ __forceinline__ uint32_t xor_lane(uint32_t x) {
-  if constexpr (M == 1) return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, true);
-  if constexpr (M == 2) return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x4E, 0xF, 0xF, true);
-  if constexpr (M == 4) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x101F);
-  if constexpr (M == 8) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x201F);
-  if constexpr (M == 16) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x401F);
-  if constexpr (M >= 32) return (uint32_t)__shfl_xor((int)x, M);
-}
-
 // Sum / max over the four lanes n, n+16, n+32, n+48; every lane gets the same bits.
 __device__ __forceinline__ float sum4(float x) {
   float a = x, b = x;

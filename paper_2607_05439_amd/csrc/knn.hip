@@ -29,7 +29,6 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "cdna4.h"
 #include "dcp_internal.h"
 
 namespace dcp {
@@ -40,6 +39,17 @@ constexpr int kKnnQ = 4;                          // query rows per wave
 constexpr int kKnnRows = kKnnWaves * kKnnQ;       // query rows per workgroup
 constexpr int kTile = 2048;                       // candidates per LDS tile
 constexpr uint64_t kNoKey = ~0ULL;
+
+// Value of lane (lane ^ M).
+template <int M>
+__device__ __forceinline__ uint32_t xor_lane(uint32_t x) {
+  if constexpr (M == 1) return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, true);
+  if constexpr (M == 2) return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x4E, 0xF, 0xF, true);
+  if constexpr (M == 4) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x101F);
+  if constexpr (M == 8) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x201F);
+  if constexpr (M == 16) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x401F);
+  if constexpr (M >= 32) return (uint32_t)__shfl_xor((int)x, M);
+}
 
 template <int M>
 __device__ __forceinline__ uint64_t xor_lane64(uint64_t v) {
