@@ -43,7 +43,7 @@ namespace {
 
 constexpr int kRun = 64;  // atoms per wave of the general path
 constexpr double kFix = 4294967296.0;  // 2^32
-constexpr int kSlots = 16;             // atom rows per lane group in flight
+constexpr int kSlots = 4;              // atom rows per lane group in flight (few: more waves fit)
 constexpr uint32_t kNt = 2;            // cache-policy bit of a buffer load: non-temporal
 constexpr int kGatedBlocks = 1024;     // grid cap of the general path's accumulation and division
 
