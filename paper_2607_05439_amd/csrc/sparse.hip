@@ -341,8 +341,8 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
   constexpr int NPI = 64 / LPN;      // rows per load instruction (4 | 2)
   constexpr int LPH = kD / EPL;      // lanes per head (4 | 8)
   constexpr int KS = KMAX / 64;      // slots per lane in slot order
-  constexpr int kUnroll = 4;         // K (and V) loads per lane per batch
-  constexpr int kBatch = NPI * kUnroll;  // slots per batch (16 | 8)
+  constexpr int kUnroll = 2;         // K (and V) loads per lane per batch (few: more waves fit)
+  constexpr int kBatch = NPI * kUnroll;  // slots per batch (8 | 4)
   constexpr int kPad = 32;           // list length granularity
   constexpr int kPasses = KMAX / 16; // bias passes of 16 slots
   static_assert(kPad % 16 == 0 && kPad % kBatch == 0 && KMAX % kPad == 0, "list padding");
@@ -450,13 +450,6 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) vw[buf][u] = __builtin_amdgcn_raw_buffer_load_b128(vres, off[u], 0, 0);
   };
-  auto issue_batch = [&](int buf, int b0) {
-    // K first: the logits can start while V is still arriving
-    int off[kUnroll];
-    offsets(b0, off);
-    issue_k(buf, off);
-    issue_v(buf, off);
-  };
   // one batch: logits (the only use of the K rows) ...
   auto logits = [&](int buf, int b0, float (&lg)[kUnroll]) {
 #pragma unroll
@@ -538,8 +531,8 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
     if (lane < count_pad - count + kBatch) lkv[count + lane] = (uint32_t)kOutOfRange;  // and one more batch
     wave_lds_sync();
 
-    // 2. every pair-vector load of the list, then the first K/V batch, so the
-    //    bias work below overlaps the K/V latency
+    // 2. every pair-vector load of the list, then the first batch's K rows, so
+    //    the bias work below overlaps their latency
     if constexpr (kBf16) {
       // 16 slots per pass on the matrix cores: lane (n, g) holds channels
       // 4g..4g+3 of slot n; W''.p gives the heads (rows 0..3) and the row sum
@@ -551,7 +544,11 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
         const int off = 16 * ps < count_pad ? (int)(lp[16 * ps + n] + 8u * g) : kOutOfRange;
         pw[ps] = __builtin_amdgcn_raw_buffer_load_b64(pres, off, 0, kNt);
       }
-      issue_batch(0, 0);
+      {  // the first batch's K rows; its V rows follow the bias work
+        int o0[kUnroll];
+        offsets(0, o0);
+        issue_k(0, o0);
+      }
 #pragma unroll
       for (int ps = 0; ps < kPasses; ++ps) {
         if (16 * ps >= count_pad) break;
@@ -596,7 +593,11 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
         const int off = 16 * ps < count_pad ? (int)(lp[16 * ps + (lane >> 2)] + 16u * cq) : kOutOfRange;
         pw[ps] = __builtin_amdgcn_raw_buffer_load_b128(pres, off, 0, kNt);
       }
-      issue_batch(0, 0);
+      {  // the first batch's K rows; its V rows follow the bias work
+        int o0[kUnroll];
+        offsets(0, o0);
+        issue_k(0, o0);
+      }
 #pragma unroll
       for (int ps = 0; ps < kPasses; ++ps) {
         if (16 * ps >= count_pad) break;
@@ -631,12 +632,14 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
     //    of loads in flight the same on every path
     int prev[kUnroll];  // addresses of the V loads in flight
     offsets(0, prev);
+    issue_v(0, prev);
     for (int b0 = 0; b0 < count_pad; b0 += kBatch) {
       int off[kUnroll];
       offsets(b0 + kBatch, off);
       // the loads in flight read their addresses from prev: keep those
       // registers until the next addresses are in others
-      asm volatile("" ::"v"(prev[0]), "v"(prev[1]), "v"(prev[2]), "v"(prev[3]));
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) asm volatile("" ::"v"(prev[u]));
       float lg[kUnroll];
       logits(0, b0, lg);
       issue_k(0, off);
