@@ -224,7 +224,7 @@ struct ScatterArgs {
   void* out;              // [n_tokens][c]
   int32_t* flags;         // [kScatterFlags] order-check flags (workspace); NULL: general path only
   int32_t n_flags;        // flags written by this call (set by the launcher)
-  int64_t* plan;          // [n_tokens][2] first atom and atom count of each token (workspace)
+  int64_t* plan;          // [n_tokens][2] first atom and one past the last of each token (workspace)
 };
 
 hipError_t launch_fast_proj(const FastProjArgs& a, hipStream_t st);

@@ -16,10 +16,11 @@
 //                         tile's indices for a decrease (one flag per
 //                         workgroup, written whatever its value, so nothing
 //                         needs clearing first) and, where there is none,
-//                         writes each token's first atom and atom count to a
-//                         plan (count 0 for a token without atoms); a token's
-//                         entry is written by the tile of its first atom (or,
-//                         for an empty token, of the atom after the gap)
+//                         writes each token's first and one-past-last atom to
+//                         a plan: the lane at a token boundary writes the end
+//                         of the run before it and the start of the run after
+//                         it (both at the boundary for a token without atoms),
+//                         so no lane scans a long token's atoms
 //   scatter_sum_kernel    if no flag is set: consecutive tokens go to groups of
 //                         lanes, a group covering a feature row in 16-byte
 //                         chunks; each group loads all its token's rows at
@@ -156,61 +157,40 @@ __device__ __forceinline__ bool out_of_order(const int32_t* flags, int n_flags) 
   return __ballot(any != 0) != 0;
 }
 
-// plan[2t] = first atom of token t, plan[2t + 1] = its atom count, for
-// indices ordered by token. Empty tokens get count 0 and, as first atom, the
+// plan[2t] = first atom of token t, plan[2t + 1] = one past its last, for
+// indices ordered by token. Each run boundary writes the end of the run before
+// it and the start of the run after it, so every entry is written once, by the
+// tile that holds the boundary; a token without atoms gets both at the
 // position after the gap, so first atoms never decrease along the tokens.
 __global__ void __launch_bounds__(1024) scatter_plan_kernel(ScatterArgs a) {
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int64_t n = a.n_atoms, tiles = n / 64 + 1;  // positions 0..n (n: the end of the last token)
   int bad = 0;
   for (int64_t tile = (int64_t)blockIdx.x * 16 + wave; tile < tiles; tile += (int64_t)gridDim.x * 16) {
-    const int64_t i0 = tile * 64, p = i0 + lane;
+    const int64_t p = tile * 64 + lane;
     const int32_t cur = p < n ? a.tok_idx[p] : 0;
     const int32_t prv = (p >= 1 && p <= n) ? a.tok_idx[p - 1] : -1;
-    const int32_t nxt = p + 64 < n ? a.tok_idx[p + 64] : 0;
     if (__ballot(p >= 1 && p < n && prv > cur)) {  // out of order: no plan (it is never read)
       bad = 1;
       continue;
     }
-    // position p starts a run when p = 0 or its token differs from the
-    // previous atom's; the tokens strictly between the previous run's and
-    // this one's (and after the last atom's, at p = n) have no atoms
-    const bool start = p < n && (p == 0 || prv != cur);
-    const bool own = start && cur >= 0 && (int64_t)cur < a.n_tokens;
-    const uint64_t bmask = __ballot(start), omask = __ballot(own);
+    // a boundary at p: p = 0, p = n, or a token change between p - 1 and p
     int64_t g0 = 0, g1 = 0;
-    if (p <= n && (p == n || start)) {
+    if (p <= n && (p == 0 || p == n || prv != cur)) {
+      if (p > 0 && prv >= 0 && (int64_t)prv < a.n_tokens) a.plan[2 * (int64_t)prv + 1] = p;
+      if (p < n && cur >= 0 && (int64_t)cur < a.n_tokens) a.plan[2 * (int64_t)cur] = p;
+      // the tokens strictly between the two runs' tokens have no atoms
       g0 = (p == 0 ? -1 : max((int64_t)prv, (int64_t)-1)) + 1;
       g1 = p == n ? a.n_tokens : min((int64_t)cur, a.n_tokens);
     }
+    // gaps are filled by the whole wave, one at a time
     for (uint64_t m = __ballot(g1 > g0); m; m &= m - 1) {
       const int l = __builtin_ctzll(m);
-      const int64_t t0 = __shfl(g0, l), t1 = __shfl(g1, l), at = i0 + l;
+      const int64_t t0 = __shfl(g0, l), t1 = __shfl(g1, l), at = tile * 64 + l;
       for (int64_t t = t0 + lane; t < t1; t += 64) {
         a.plan[2 * t] = at;
-        a.plan[2 * t + 1] = 0;
+        a.plan[2 * t + 1] = at;
       }
-    }
-    if (omask == 0) continue;
-    // a run ends at the next boundary in the tile; the tile's last run at the
-    // first later atom with another token (or n)
-    int64_t e_tail = n;
-    const int top = 63 - __builtin_clzll(bmask);
-    if (((omask >> top) & 1) && i0 + 64 < n) {
-      const int32_t last = __shfl(cur, 63);
-      uint64_t stop = __ballot(p + 64 >= n || nxt != last);
-      int64_t j0 = i0 + 64;
-      while (!stop) {  // a token of more than 64 atoms
-        j0 += 64;
-        const int64_t j = j0 + lane;
-        stop = __ballot(j >= n || a.tok_idx[j] != last);
-      }
-      e_tail = j0 + __builtin_ctzll(stop);
-    }
-    if (own) {
-      const uint64_t above = lane == 63 ? 0 : bmask >> (lane + 1);
-      a.plan[2 * (int64_t)cur] = p;
-      a.plan[2 * (int64_t)cur + 1] = (above ? p + 1 + __builtin_ctzll(above) : e_tail) - p;
     }
   }
   bad = __syncthreads_or(bad);
@@ -243,7 +223,7 @@ __global__ void __launch_bounds__(256) scatter_sum_kernel(ScatterArgs a) {
   if (act) {
     const i64x2 e = *reinterpret_cast<const i64x2*>(a.plan + 2 * t);
     b = e[0];
-    cnt = e[1];
+    cnt = e[1] - e[0];
   }
   if (out_of_order(a.flags, a.n_flags)) {
     clear_general(a);

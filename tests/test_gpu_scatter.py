@@ -260,3 +260,20 @@ def test_workspace_contents_do_not_matter():
     assert np.array_equal(call(a[p], idx[p], n_tok, ws), ref)
     assert np.array_equal(call(a, idx, n_tok, ws), ref)
     assert np.all(ref[100] == 0.0)
+
+
+def test_token_rows_spread_over_more_than_a_gib():
+    """One token of 1.1 million atoms with 1 KiB feature rows: its rows span
+    more than 2^30 bytes, beyond a 32-bit buffer offset, so the ordered path
+    takes its 64-bit row loop. Against the oracle, next to a small token
+    before it, one after it and an empty one."""
+    r = np.random.default_rng(41)
+    n_tok, c = 4, 256
+    idx = np.repeat(np.arange(3, dtype=np.int32), [10, 1_100_000, 1000])
+    a = r.standard_normal((len(idx), c), dtype=np.float32)
+    assert int(np.sum(idx == 1)) * c * 4 > 2**30
+    got = pool(a, idx, n_tok)
+    ref = oracle.scatter_mean(a, idx, n_tok)
+    log(f"case 1.1M-atom token: rel err {rel_err(got, ref):.3e}")
+    assert rel_err(got, ref) <= 1e-6
+    assert np.all(got[3] == 0.0)
