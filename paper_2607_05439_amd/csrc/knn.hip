@@ -14,12 +14,13 @@
 // 8 waves; tiles are visited starting at the one that holds the queries
 // themselves when they are candidates (their sequence neighbours are close in
 // space, which makes the thresholds tight early; the result does not depend on
-// the order). A lane takes one candidate per 64-candidate step and computes its
-// distance to the 4 queries; a step goes further for a query only when some
-// lane's distance bits do not exceed the high word of that query's current
-// k-th key (an exact prefilter: the bits of a non-negative float order like
-// the float, and the key orders by d2 first). The exact key test then picks
-// the candidates that enter the query's 64-entry LDS buffer. The sorted top-k
+// the order). A lane takes one candidate per 64-candidate step and tests it
+// against the 4 queries with a cheap conservative bound (|c|^2 - 2 c.q by
+// three multiply-adds, |c|^2 staged with the tile, against a per-query limit
+// derived from the current k-th distance with a proven rounding margin): no
+// candidate that could enter is rejected. Only where some lane passes does the
+// step compute the distances of the definition; the exact 64-bit key test then
+// picks the candidates that enter the query's 64-entry LDS buffer. The sorted top-k
 // lives in registers (entry 64s + lane in slot s); a full buffer is sorted
 // (bitonic network across lanes) and merged slot by slot: the lane-wise
 // minimum of a sorted slot and the reversed sorted carry is a bitonic sequence
@@ -101,6 +102,11 @@ __device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
   return ((uint64_t)hi << 32) | lo;
 }
 
+// a wave-uniform value, held in a scalar register
+__device__ __forceinline__ float uniform(float v) {
+  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));
+}
+
 // State of one query row: its sorted top-k (KS slots of 64 keys), the number
 // of valid entries, the k-th key, and the LDS buffer of pending keys.
 template <int KS>
@@ -111,6 +117,26 @@ struct QueryTopk {
   uint64_t* buf;
   float x, y, z;
   int32_t g;
+  float mx, my, mz;  // -2 x, -2 y, -2 z (exact)
+  float qq, qn;      // |q|^2 and |q|
+  float lim;         // prefilter bound on |c|^2 - 2 c.q for candidates that may still enter
+
+  // The prefilter computes e = |c|^2 - 2 c.q with three multiply-adds; the
+  // exact distance is |c - q|^2 = e + |q|^2 up to rounding. If the rounded
+  // distance of the definition is at most T (the k-th key's distance), then
+  // the true distance D is at most T (1 + 6u) (u = 2^-24), so |c| <= |q| +
+  // 1.001 sqrt(T) =: rho, and e is within 6u (|c|^2 + |c||q|) <= 12u rho^2 of
+  // its true value D - |q|^2. So every candidate that may enter has
+  // e <= T - |q|^2 + 6uT + 12u rho^2; the bound below adds 32u (T + rho^2),
+  // which also covers the rounding of |q|^2 (3u rho^2) and of the bound
+  // itself (about 2u (T + rho^2)). With no
+  // finite k-th distance yet the bound is +inf or NaN, and the test
+  // "not above the bound" lets every candidate through.
+  __device__ __forceinline__ void set_limit() {
+    const float T = __uint_as_float((uint32_t)(tau >> 32));
+    const float rho = qn + 1.001f * __builtin_sqrtf(T);
+    lim = uniform((T - qq) + 0x1p-19f * (T + rho * rho));
+  }
 
   __device__ __forceinline__ void init(uint64_t* b) {
 #pragma unroll
@@ -140,6 +166,7 @@ struct QueryTopk {
     for (int s = 1; s < KS; ++s)
       if (s == ((k - 1) >> 6)) last = top[s];
     tau = count == k ? readlane64(last, (k - 1) & 63) : kNoKey;
+    set_limit();
     wave_lds_sync();  // the buffer has been read before it is refilled
   }
 
@@ -163,6 +190,8 @@ struct QueryTopk {
   }
 };
 
+__device__ __forceinline__ float norm2(float4 c) { return fmaf(c.x, c.x, fmaf(c.y, c.y, c.z * c.z)); }
+
 __device__ __forceinline__ float dist2(float qx, float qy, float qz, float4 c) {
   // the distance is part of the definition: each operation rounded, in this
   // order, never fused into multiply-adds
@@ -172,8 +201,8 @@ __device__ __forceinline__ float dist2(float qx, float qy, float qz, float4 c) {
 }
 
 template <int KS, int MODE>
-__global__ void __launch_bounds__(64 * kKnnWaves) knn_kernel(KnnArgs a) {
-  __shared__ float4 s_c[kTile];  // x, y, z, group bits
+__global__ void __launch_bounds__(64 * kKnnWaves) __attribute__((amdgpu_waves_per_eu(KS == 2 ? 6 : 1))) knn_kernel(KnnArgs a) {
+  __shared__ float4 s_c[kTile];  // x, y, z, then |c|^2 (MODE 0) or the group bits
   __shared__ uint64_t s_buf[kKnnWaves][kKnnQ][64];
 
   const int lane = threadIdx.x & 63;
@@ -191,6 +220,12 @@ __global__ void __launch_bounds__(64 * kKnnWaves) knn_kernel(KnnArgs a) {
     q[j].y = a.x_q[3 * rr + 1];
     q[j].z = a.x_q[3 * rr + 2];
     q[j].g = MODE ? a.group_q[rr] : 0;
+    q[j].mx = uniform(-2.0f * q[j].x);
+    q[j].my = uniform(-2.0f * q[j].y);
+    q[j].mz = uniform(-2.0f * q[j].z);
+    q[j].qq = uniform(fmaf(q[j].x, q[j].x, fmaf(q[j].y, q[j].y, q[j].z * q[j].z)));
+    q[j].qn = uniform(__builtin_sqrtf(q[j].qq));
+    q[j].set_limit();
   }
 
   const int64_t n_tiles = (a.n_c + kTile - 1) / kTile;
@@ -205,7 +240,8 @@ __global__ void __launch_bounds__(64 * kKnnWaves) knn_kernel(KnnArgs a) {
       float4 v;
       if (i < n_here) {
         const float* p = a.x_c + 3 * (c0 + i);
-        v = make_float4(p[0], p[1], p[2], __int_as_float(MODE ? a.group_c[c0 + i] : 0));
+        v = make_float4(p[0], p[1], p[2], 0.f);
+        v.w = MODE ? __int_as_float(a.group_c[c0 + i]) : norm2(v);
       } else {
         v = make_float4(__builtin_nanf(""), 0.f, 0.f, 0.f);  // never passes the prefilter of a full top-k
       }
@@ -226,27 +262,27 @@ __global__ void __launch_bounds__(64 * kKnnWaves) knn_kernel(KnnArgs a) {
     for (int t = 0; t < n_pairs; ++t, pr = pr + 1 == n_pairs ? 0 : pr + 1) {
       const int s = pr << 7;
       const float4 ca = s_c[s + lane], cb = s_c[s + 64 + lane];
-      float da[kKnnQ], db[kKnnQ];
+      const float cca = MODE ? norm2(ca) : ca.w, ccb = MODE ? norm2(cb) : cb.w;
       uint64_t ma[kKnnQ], mb[kKnnQ], any = 0;
 #pragma unroll
       for (int j = 0; j < kKnnQ; ++j) {
-        da[j] = dist2(q[j].x, q[j].y, q[j].z, ca);
-        db[j] = dist2(q[j].x, q[j].y, q[j].z, cb);
-        const uint32_t th = (uint32_t)(q[j].tau >> 32);
-        ma[j] = __ballot(__float_as_uint(da[j]) <= th);
-        mb[j] = __ballot(__float_as_uint(db[j]) <= th);
+        const float ea = fmaf(ca.x, q[j].mx, fmaf(ca.y, q[j].my, fmaf(ca.z, q[j].mz, cca)));
+        const float eb = fmaf(cb.x, q[j].mx, fmaf(cb.y, q[j].my, fmaf(cb.z, q[j].mz, ccb)));
+        ma[j] = __ballot(!(ea > q[j].lim));
+        mb[j] = __ballot(!(eb > q[j].lim));
         any |= ma[j] | mb[j];
       }
       if (any == 0) continue;
-      // a flush lowers tau after the prefilter: the masks stay a superset
+      // the exact distances and keys decide; a flush lowers tau after the
+      // prefilter, so the masks stay a superset
 #pragma unroll
       for (int j = 0; j < kKnnQ; ++j) {
         if (ma[j])
-          q[j].template offer<MODE>(__float_as_uint(da[j]), index0 + s + lane, s + lane < n_here,
-                                    __float_as_int(ca.w), lane, k);
+          q[j].template offer<MODE>(__float_as_uint(dist2(q[j].x, q[j].y, q[j].z, ca)), index0 + s + lane,
+                                    s + lane < n_here, __float_as_int(ca.w), lane, k);
         if (mb[j])
-          q[j].template offer<MODE>(__float_as_uint(db[j]), index0 + s + 64 + lane, s + 64 + lane < n_here,
-                                    __float_as_int(cb.w), lane, k);
+          q[j].template offer<MODE>(__float_as_uint(dist2(q[j].x, q[j].y, q[j].z, cb)), index0 + s + 64 + lane,
+                                    s + 64 + lane < n_here, __float_as_int(cb.w), lane, k);
       }
     }
   }

@@ -129,6 +129,20 @@ def test_ties_on_a_grid_and_duplicates():
     same(gpu_knn(x[1:2], x, 7), oracle.knn(x[1:2], x, 7), "one query")
 
 
+@pytest.mark.parametrize("scale,shift", [(1.0, 3000.0), (1.0, -250000.0), (1e-4, 0.0), (1e-4, 7.0), (1e5, 0.0)])
+def test_coordinate_magnitudes(scale, shift):
+    """The candidate prefilter bounds |c|^2 - 2 c.q with a rounding margin
+    that grows with |q|: structures far from the origin (where most of that
+    expression cancels), at sub-angstrom scales and at very large scales give
+    the same exact lists as the oracle."""
+    x0 = synth.coords(synth.KNN_WORKLOADS["knn5000"])
+    x = (x0.astype(np.float64) * scale + shift).astype(np.float32)
+    q = x[2000:2600]
+    log(f"case scale={scale} shift={shift}")
+    for k in (1, 128):
+        same(gpu_knn(q, x, k, q_self0=2000), oracle.knn(q, x, k), f"scale={scale} shift={shift} k={k}")
+
+
 def test_short_and_empty_candidate_sets():
     x = synth.coords(synth.KNN_WORKLOADS["knn300"])
     same(gpu_knn(x[:40], x[:30], 64), oracle.knn(x[:40], x[:30], 64), "fewer candidates than k")
