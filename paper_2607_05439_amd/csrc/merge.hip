@@ -66,16 +66,28 @@ __global__ void __launch_bounds__(256) merge4_kernel(MergeArgs a) {
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     if (mx != -INFINITY) {
       const float4* ap = reinterpret_cast<const float4*>(a.acc + (size_t)r * hd) + x4;
-      for (int p = 0; p < a.n_parts; ++p) {
-        const float mp = m[p * pm];
-        if (mp == -INFINITY) continue;
-        const float sc = a.log2_units ? ldexpf(1.0f, (int)(mp - mx)) : expf(mp - mx);
-        l = fmaf(sc, l_in[p * pm], l);
-        const float4 v = ap[p * part / 4];
-        acc.x = fmaf(sc, v.x, acc.x);
-        acc.y = fmaf(sc, v.y, acc.y);
-        acc.z = fmaf(sc, v.z, acc.z);
-        acc.w = fmaf(sc, v.w, acc.w);
+      // four parts' loads at a time (a part past the end repeats the last
+      // one and is skipped), folded in increasing order
+      for (int p0 = 0; p0 < a.n_parts; p0 += 4) {
+        float mv[4], lv[4];
+        float4 vv[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int p = min(p0 + j, a.n_parts - 1);
+          mv[j] = m[p * pm];
+          lv[j] = l_in[p * pm];
+          vv[j] = ap[p * part / 4];
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (p0 + j >= a.n_parts || mv[j] == -INFINITY) continue;
+          const float sc = a.log2_units ? ldexpf(1.0f, (int)(mv[j] - mx)) : expf(mv[j] - mx);
+          l = fmaf(sc, lv[j], l);
+          acc.x = fmaf(sc, vv[j].x, acc.x);
+          acc.y = fmaf(sc, vv[j].y, acc.y);
+          acc.z = fmaf(sc, vv[j].z, acc.z);
+          acc.w = fmaf(sc, vv[j].w, acc.w);
+        }
       }
     }
     const size_t e0 = (size_t)t * 4;  // = r * hd + 4 * x4

@@ -35,11 +35,14 @@ def test_bias_project(torch_cuda, dtype, c_z, h, tol):
     assert err <= tol
 
 
-def test_block_merge(torch_cuda):
+@pytest.mark.parametrize("D", [6, 8, 24])
+def test_block_merge(torch_cuda, D):
+    """Head sizes 6 (one channel per thread) and 8, 24 (four channels of a
+    head per thread)."""
     import paper_2607_05439_amd as dcp
-    log("case block_merge")
+    log(f"case block_merge D={D}")
     r = np.random.default_rng(5)
-    P, R, H, D = 5, 33, 4, 6
+    P, R, H = 5, 33, 4
     m = (3 * r.standard_normal((P, H, R))).astype(np.float32)
     m[1, :, ::3] = -np.inf
     m[:, 0, 7] = -np.inf  # a fully empty (row, head)
@@ -78,3 +81,37 @@ def test_device_generator_matches_host(torch_cuda, period, bf16):
     dev = z[rows].cpu()
     dev = dev.view(torch_cuda.int16).numpy().view(np.uint16) if bf16 else dev.numpy()
     assert np.array_equal(dev.view(np.uint8), host.view(np.uint8))
+
+
+def test_block_merge_forms_agree_bit_for_bit(torch_cuda):
+    """The same merge through the four-channel kernel (16-byte aligned
+    buffers) and through the one-channel kernel (buffers one element off
+    alignment): identical bits, with and without the gate, fp32 and bf16."""
+    import paper_2607_05439_amd as dcp
+    r = np.random.default_rng(8)
+    P, R, H, D = 6, 257, 16, 24
+    m = np.floor(8 * r.standard_normal((P, H, R))).astype(np.float32)
+    m[2, :, ::5] = -np.inf
+    l = (r.random((P, H, R)) + 0.5).astype(np.float32)
+    l[np.isneginf(m)] = 0
+    acc = r.standard_normal((P, R, H, D)).astype(np.float32)
+    gate = r.random((R, H * D)).astype(np.float32)
+
+    def dev_at(a, shift):  # device copy whose data starts `shift` floats into a fresh buffer
+        flat = torch_cuda.zeros(a.size + 4, dtype=torch_cuda.float32, device="cuda")
+        flat[shift:shift + a.size] = torch_cuda.from_numpy(np.ascontiguousarray(a).ravel()).cuda()
+        return flat[shift:shift + a.size].view(a.shape)
+
+    for with_gate in (True, False):
+        outs = []
+        for shift in (0, 1):
+            for dt in (DCP_F32, DCP_BF16):
+                o = torch_cuda.zeros(R * H * D + 8, dtype=torch_cuda.float32 if dt == DCP_F32 else torch_cuda.bfloat16,
+                                     device="cuda")[shift:shift + R * H * D].view(R, H * D)
+                ao = dev_at(np.zeros((R, H, D), np.float32), shift)
+                dcp.dcp_block_merge(P, R, H, D, dev_at(m, shift), dev_at(l, shift), dev_at(acc, shift), None, None,
+                                    ao, dev_at(gate, shift) if with_gate else None, o, dt)
+                outs.append((o.float().cpu().numpy(), ao.cpu().numpy()))
+        for i in range(2):  # fp32 and bf16 outputs: aligned against shifted
+            assert np.array_equal(outs[i][0], outs[2 + i][0])
+            assert np.array_equal(outs[i][1], outs[2 + i][1])
