@@ -277,3 +277,51 @@ def test_token_rows_spread_over_more_than_a_gib():
     log(f"case 1.1M-atom token: rel err {rel_err(got, ref):.3e}")
     assert rel_err(got, ref) <= 1e-6
     assert np.all(got[3] == 0.0)
+
+
+def test_graph_capture_replays():
+    """The pooling captured into a graph (the order check, the ordered sum
+    and the gated any-order kernels) and replayed three times, with eager
+    work, eager calls and synchronisations between the replays: every replay
+    gives the eager bits, for ordered and for shuffled atoms."""
+    import torch
+    import paper_2607_05439_amd as dcp
+    r = np.random.default_rng(51)
+    n_tok, c = 700, 64
+    idx = np.sort(r.integers(0, n_tok, 5000)).astype(np.int32)
+    a = r.standard_normal((len(idx), c)).astype(np.float32)
+    p = r.permutation(len(idx))
+    for name, (aa, ii) in (("ordered", (a, idx)), ("shuffled", (a[p], idx[p]))):
+        log(f"case graph capture, {name} atoms")
+        ad, idd = dev(aa), dev(ii)
+        ws_bytes = dcp.dcp_scatter_mean_workspace_size(n_tok, c)
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda:0")
+        out = torch.zeros((n_tok, c), dtype=torch.float32, device="cuda:0")
+
+        def call():
+            dcp.dcp_scatter_mean(len(ii), n_tok, c, DCP_F32, DCP_F32, ad, idd, out, ws, ws_bytes)
+
+        call()
+        torch.cuda.synchronize()
+        ref = out.clone()
+        assert rel_err(ref.cpu().numpy(), oracle.scatter_mean(aa, ii, n_tok)) <= 1e-6
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            call()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            call()
+        torch.cuda.synchronize()
+        for rep in range(3):
+            out.fill_(-1.0)
+            torch.cuda.synchronize()
+            graph.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(out, ref), (name, rep)
+            out.fill_(5.0)
+            call()
+            torch.cuda.synchronize()
+            assert torch.equal(out, ref), (name, rep)
