@@ -699,10 +699,36 @@ def main():
     ms_per_step = t_start.elapsed_time(t_stop) / args.steps
     k_ms = [hip.elapsed_ms(a, b) for evs in kernel_evs for (a, b) in evs]
     avg_kernel_ms = sum(k_ms) / len(k_ms)
+    k_sorted = sorted(k_ms)
+    launch_stats = {"median": round(k_sorted[len(k_sorted) // 2], 4), "min": round(k_sorted[0], 4),
+                    "max": round(k_sorted[-1], 4), "launches": len(k_ms)}
     achieved = (bytes_per_step / len(wl.stripes)) / (avg_kernel_ms * 1e-3) / 1e9
     value = bytes_per_step / (ms_per_step * 1e-3) / 1e9
     progress(f"{ms_per_step:.3f} ms/layer, attention kernel {avg_kernel_ms:.3f} ms/launch, "
              f"{achieved:.0f} GB/s in the kernel ({achieved / PEAK_HBM_GBPS:.1%} of peak)")
+
+    # the materialised bias alone (dcp_bias_project) on a stripe of rows: the z
+    # stream with LayerNorm and the c_z -> H projection but no attention, as a
+    # pure-stream reference beside the fused kernel (outside the timed region)
+    bias_ref = None
+    if wl.bf16 and cz == 128:
+        nr = min(256, n)
+        bout = torch.empty((nr, n, wl.n_heads), dtype=torch.float32, device=dev)
+        bsh = dcp.make_shape(n, wl.c_s, cz, wl.n_heads, wl.head_dim, dcp.DCP_BF16, dcp.DCP_F32, 1e-5)
+        run_bias = lambda: dcp.dcp_bias_project(bsh, weights, z.data_ptr(), nr, n, n * cz, bout, sp)
+        run_bias()
+        b_ms = []
+        for _ in range(5):
+            hip.record(e0, sp)
+            run_bias()
+            hip.record(e1, sp)
+            b_ms.append(hip.elapsed_ms(e0, e1))
+        b_med = sorted(b_ms)[len(b_ms) // 2]
+        zb = nr * n * cz * wl.elem_bytes
+        bias_ref = {"rows": nr, "ms_median": round(b_med, 4), "z_read_GBps": round(zb / (b_med * 1e-3) / 1e9, 1),
+                    "read_plus_write_GBps": round((zb + bout.numel() * 4) / (b_med * 1e-3) / 1e9, 1)}
+        del bout
+        progress(f"dcp_bias_project on {nr} rows: {b_med:.3f} ms, z read at {bias_ref['z_read_GBps']:.0f} GB/s")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -737,6 +763,11 @@ def main():
                      "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic,
                      "kernel": "attn_kernel", "kernel_ms": round(avg_kernel_ms, 4),
                      "algorithmic_bytes_per_launch": bytes_per_launch[0]},
+        "attn_launch_ms": launch_stats,
+        # one launch covers a stripe of query rows against n_key_blocks key blocks:
+        # the time of one (stripe, key block) tile of a grid schedule
+        "per_tile_ms": round(avg_kernel_ms / wl.n_key_blocks, 4),
+        "bias_project_stripe": bias_ref,
         "streaming_read_GBps": round(read_gbps, 1),
         "pattern_read_GBps": None if pattern_gbps is None else round(pattern_gbps, 1),
         "cpu_baseline": cpu,

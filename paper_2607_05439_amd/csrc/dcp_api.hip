@@ -67,17 +67,44 @@ int pick_path(const dcp_shape* sh, Path* p) {
 
 // Segments per key block on the fused path: enough waves to give every SIMD
 // several, without segments shorter than 64 keys.
+// Segments per key block for the fused kernel. A workgroup (kTileQ * 4 query
+// rows) holds a whole CU (160 KB of LDS), so workgroups run in rounds of
+// kSchedCUs, and a last round that fills only part of the chip leaves the rest
+// idle for a whole workgroup's time. The cost of a choice, in units of one
+// key streamed by one workgroup, is rounds x (keys per part + a fixed
+// per-workgroup cost) plus the partial states it adds (H (d+2) fp32 per row and
+// part, written then read by the merge: about 13 keys of z per row and part,
+// spread over the chip). The smallest segment count within 2% of the cheapest
+// is taken, so that more partials are only paid for a real gain. No part is
+// longer than kMaxPartKeys keys: each part's fp32 accumulator is one sequential
+// chain of per-tile matrix-core sums, and bounding its length bounds the
+// rounding difference between two blockings of the same keys.
+constexpr int64_t kSchedCUs = 256;     // CUs of an MI350X / MI355X (gfx950)
+constexpr int64_t kMaxPartKeys = 4096;
+constexpr int64_t kGroupCostKeys = 8;  // prologue (q, weights, ring fill) and epilogue, in keys
+constexpr int64_t kPartCostKeys = 13;  // partial state per row and part, in keys of z per row
+
 int fast_segments(int64_t n_tok, int64_t n_q, int32_t n_kb) {
-  const int64_t waves = (n_q + dcp::kTileQ - 1) / dcp::kTileQ * (int64_t)n_kb;
-  const int64_t target = 4 * 1024;
-  int64_t seg = (target + waves - 1) / waves;
-  const int64_t min_block = n_tok / n_kb;
-  int64_t cap = min_block / 64;
+  const int64_t groups = (n_q + 4 * dcp::kTileQ - 1) / (4 * dcp::kTileQ);
+  const int64_t block = (n_tok + n_kb - 1) / n_kb;
+  int64_t cap = (n_tok / n_kb) / 64;
   if (cap < 1) cap = 1;
-  if (seg > cap) seg = cap;
-  if (seg > 64) seg = 64;
-  if (seg < 1) seg = 1;
-  return (int)seg;
+  if (cap > 64) cap = 64;
+  int64_t seg_min = (block + kMaxPartKeys - 1) / kMaxPartKeys;
+  if (seg_min > cap) seg_min = cap;
+  double cost[65];
+  double best = 0.0;
+  for (int64_t seg = seg_min; seg <= cap; ++seg) {
+    const int64_t wgs = groups * n_kb * seg;
+    const int64_t rounds = (wgs + kSchedCUs - 1) / kSchedCUs;
+    const int64_t keys = (block + seg - 1) / seg;
+    cost[seg] = (double)rounds * (double)(keys + kGroupCostKeys) +
+                (double)n_q * (double)(n_kb * seg) * kPartCostKeys / (64.0 * kSchedCUs);
+    if (seg == seg_min || cost[seg] < best) best = cost[seg];
+  }
+  for (int64_t seg = seg_min; seg <= cap; ++seg)
+    if (cost[seg] <= 1.02 * best) return (int)seg;
+  return (int)seg_min;
 }
 
 struct Layout {
@@ -167,10 +194,11 @@ static int run_attention(const dcp_shape* shape, const dcp_weights* w, const voi
     return fail(DCP_ERR_INVALID_ARGUMENT, "w_q, w_k, w_v and w_g must be 16-byte aligned");
   Layout L;
   make_layout(shape, path, n_q, n_key_blocks, &L);
-  // a key range shorter than N: as many segments as the range allows (fewer
-  // parts than the layout holds, so the same workspace serves)
+  // a key range shorter than N: its own segment count, never more parts than
+  // the layout holds, so the same workspace serves
   if (path == kPathFast && k_len < shape->n_tokens) {
-    L.n_seg = fast_segments(k_len > 0 ? k_len : 1, n_q, n_key_blocks);
+    const int seg = fast_segments(k_len > 0 ? k_len : 1, n_q, n_key_blocks);
+    if (seg < L.n_seg) L.n_seg = seg;
     L.n_parts = n_key_blocks * L.n_seg;
   }
   if (!workspace || !aligned(workspace, 256))
