@@ -65,8 +65,6 @@ int pick_path(const dcp_shape* sh, Path* p) {
               sh->act_dtype, sh->c_s, sh->c_z, sh->n_heads, sh->head_dim);
 }
 
-// Segments per key block on the fused path: enough waves to give every SIMD
-// several, without segments shorter than 64 keys.
 // Segments per key block for the fused kernel. A workgroup (kTileQ * 4 query
 // rows) holds a whole CU (160 KB of LDS), so workgroups run in rounds of
 // kSchedCUs, and a last round that fills only part of the chip leaves the rest
