@@ -115,6 +115,11 @@ def test_affine_constants_irrelevant(torch_cuda):
     (37, 5, 19, 3, "random:6"),
     (100, 60, 40, 5, "random:30"),
     (333, 0, 333, 2, "tail:13"),
+    # one workgroup of query rows over many keys: the launch splits the keys into
+    # many short parts whose bounds do not fall on 16-key tiles (32 parts of 64
+    # keys; 7 parts of 71-72 keys per block)
+    (2048, 100, 50, 1, "random:200"),
+    (1500, 0, 64, 3, "tail:7"),
 ])
 def test_ragged_and_small(torch_cuda, n_tok, q_row0, n_q, n_kb, mask):
     log(f"case ragged N={n_tok} q_row0={q_row0} n_q={n_q} n_kb={n_kb} mask={mask}")
