@@ -123,7 +123,36 @@ def cpu_baseline(wl, s_host, w_host, mask, seconds):
     per_row = (t_run - t_fixed) / len(rows)
     n_q_total = sum(nq for _, nq in wl.stripes)
     t_layer = t_fixed * len(wl.stripes) + per_row * n_q_total
-    return {"t_layer_s": t_layer, "rows": len(rows), "t_run_s": t_run, "threads": threads, "t_fixed_s": t_fixed}
+    # the same oracle on one host thread, over a few of the sampled rows
+    gomp = ctypes.CDLL("libgomp.so.1")
+    gomp.omp_set_num_threads(1)
+    try:
+        t0 = time.perf_counter()
+        oracle.linear(s64, w_host["w_k"])
+        oracle.linear(s64, w_host["w_v"])
+        t_fixed1 = time.perf_counter() - t0
+        rows1 = rows[:: max(1, len(rows) // 8)][:8]
+        z1 = synth.z_host(wl, rows1)
+        t0 = time.perf_counter()
+        oracle.attention(s_host, z1, rows1, mask, w_host, wl.n_heads, wl.head_dim)
+        t_run1 = time.perf_counter() - t0
+    finally:
+        gomp.omp_set_num_threads(threads)
+    per_row1 = max(t_run1 - t_fixed1, 1e-9) / len(rows1)
+    t_layer1 = t_fixed1 * len(wl.stripes) + per_row1 * n_q_total
+    return {"t_layer_s": t_layer, "rows": len(rows), "t_run_s": t_run, "threads": threads, "t_fixed_s": t_fixed,
+            "t_layer_1thread_s": t_layer1, "rows_1thread": len(rows1)}
+
+
+def host_cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def sparse_cpu_baseline(wl, a_host, w_host, nbr_host, seconds):
@@ -266,7 +295,12 @@ def sparse_main(args, wl):
                "sample": f"{cb['rows']} of {wl.n_q} query atoms in {cb['t_run_s']:.1f} s (fp64, includes the k/v "
                          f"projection of all {L} atoms, {cb['t_fixed_s']:.1f} s); extrapolated layer time "
                          f"{cb['t_layer_s']:.2f} s",
-               "ms_per_layer_extrapolated": round(cb["t_layer_s"] * 1e3, 1)}
+               "ms_per_layer_extrapolated": round(cb["t_layer_s"] * 1e3, 1),
+               "host": {"cpu_model": host_cpu_model(), "logical_cpus": os.cpu_count(),
+                        "omp_max_threads": cb["threads"]},
+               "one_thread": {"value": round(bytes_per_step / cb["t_layer_1thread_s"] / 1e9, 6), "unit": "GB/s",
+                              "sample": f"{cb['rows_1thread']} of the sampled rows on one host thread",
+                              "ms_per_layer_extrapolated": round(cb["t_layer_1thread_s"] * 1e3, 1)}}
 
     line = {
         "metric": SPARSE_METRIC,
@@ -739,7 +773,12 @@ def main():
                "sample": f"{cb['rows']} of {sum(nq for _, nq in wl.stripes)} query rows in {cb['t_run_s']:.1f} s "
                          f"(fp64, includes the k/v projection of all {n} keys, {cb['t_fixed_s']:.1f} s); "
                          f"extrapolated layer time {cb['t_layer_s']:.1f} s",
-               "ms_per_layer_extrapolated": round(cb["t_layer_s"] * 1e3, 1)}
+               "ms_per_layer_extrapolated": round(cb["t_layer_s"] * 1e3, 1),
+               "host": {"cpu_model": host_cpu_model(), "logical_cpus": os.cpu_count(),
+                        "omp_max_threads": cb["threads"]},
+               "one_thread": {"value": round(bytes_per_step / cb["t_layer_1thread_s"] / 1e9, 6), "unit": "GB/s",
+                              "sample": f"{cb['rows_1thread']} of the sampled rows on one host thread",
+                              "ms_per_layer_extrapolated": round(cb["t_layer_1thread_s"] * 1e3, 1)}}
 
     traffic = stored_traffic(wl.name)
     line = {
