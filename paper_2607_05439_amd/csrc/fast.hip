@@ -481,10 +481,11 @@ __global__ void __launch_bounds__(64) bias_kernel(FastBiasArgs a) {
   const int64_t row = r0 + n;
   const int64_t rr = min(row, a.n_rows - 1);
   const u32x4* zrow = reinterpret_cast<const u32x4*>(a.z + rr * a.row_stride) + g;
-  for (int64_t c = c_begin; c < c_end; ++c) {
-    u32x4 zb[4];
+  auto load = [&](int64_t c, u32x4 (&zb)[4]) {
 #pragma unroll
     for (int s = 0; s < 4; ++s) zb[s] = __builtin_nontemporal_load(zrow + c * 16 + 4 * s);
+  };
+  auto column = [&](int64_t c, const u32x4 (&zb)[4]) {
     f32x4 acc;
     float rstd;
     pair_bias(zb, whi, wlo, a.eps, n, acc, rstd);
@@ -496,6 +497,18 @@ __global__ void __launch_bounds__(64) bias_kernel(FastBiasArgs a) {
       o.w = fmaf(acc[3], rstd, cst[3]);
       *reinterpret_cast<float4*>(a.out + (row * a.n_cols + c) * kH + 4 * g) = o;
     }
+  };
+  // Two buffers, two columns per iteration, the next column's z always in
+  // flight while one is computed. The loads are unconditional (past the end
+  // they repeat the last column, unused), so every wait is for the older
+  // buffer only, the same on every path into the loop.
+  u32x4 za[4], zb[4];
+  load(c_begin, za);
+  for (int64_t c = c_begin; c < c_end; c += 2) {
+    load(min(c + 1, c_end - 1), zb);
+    column(c, za);
+    load(min(c + 2, c_end - 1), za);
+    if (c + 1 < c_end) column(c + 1, zb);
   }
 }
 
