@@ -35,6 +35,25 @@ def test_bias_project(torch_cuda, dtype, c_z, h, tol):
     assert err <= tol
 
 
+def test_bias_project_column_chunks(torch_cuda):
+    """The fused bias kernel walks 64 columns per wave, two at a time: several
+    chunks and an odd last chunk (131 = 64 + 64 + 3 columns)."""
+    import paper_2607_05439_amd as dcp
+    log("case bias_project bf16 c_z=128 H=16, 131 columns")
+    wl = workload(n_tok=200, c_z=128, n_heads=16, head_dim=24, c_s=384, dtype="bf16")
+    d = Device(wl, affine=True)
+    r0, c0, nr, nc = 7, 60, 21, 131
+    tile = d.z[r0:r0 + nr, c0:c0 + nc]
+    out = torch_cuda.empty((nr, nc, 16), dtype=torch_cuda.float32, device="cuda")
+    dcp.dcp_bias_project(d.shape(), d.weights(), tile.data_ptr(), nr, nc, wl.n_tok * 128, out)
+    z_host = synth.z_host(wl, range(r0, r0 + nr))[:, c0:c0 + nc]
+    w = d.w_host
+    ref = oracle.bias(np.ascontiguousarray(z_host), w["w_b"], w["b_b"], w["ln_gamma"], w["ln_beta"], 1e-5)
+    err = rel_err(out.cpu().numpy(), ref)
+    log(f"  rel err {err:.3e}")
+    assert err <= 1e-4
+
+
 @pytest.mark.parametrize("D", [6, 8, 24])
 def test_block_merge(torch_cuda, D):
     """Head sizes 6 (one channel per thread) and 8, 24 (four channels of a
