@@ -89,6 +89,13 @@ typedef struct {
  * (written to *bytes). Host-only; launches nothing. */
 int dcp_workspace_size(const dcp_shape* shape, int64_t n_q, int32_t n_key_blocks, size_t* bytes);
 
+/* The same query returning the size itself (Methods, "1D row-sharding",
+ * Eq. (cross_attn): the scratch of one stripe call). Returns 0 and sets
+ * dcp_last_error() when the arguments are invalid or the shape is not
+ * supported; a valid call with n_q = 0 also returns 0 (no workspace needed)
+ * and leaves dcp_last_error() empty. Host-only; launches nothing. */
+size_t dcp_workspace_bytes(const dcp_shape* shape, int64_t n_q, int32_t n_key_blocks);
+
 /* Pair-biased gated attention of the query stripe [q_row0, q_row0 + n_q)
  * against all N keys (Methods, Eq. (cross_attn)).
  *   s           [N, c_s] act_dtype, 16-byte aligned

@@ -3,7 +3,7 @@
 Every step of the computation runs in the library's HIP kernels; PyTorch is
 used for device memory and streams. The functions carry the C names
 (``dcp_pair_bias_attention``, ``dcp_pair_bias_attention_partial``, ``dcp_bias_project``, ``dcp_block_merge``,
-``dcp_workspace_size``, ``dcp_sparse_pair_bias_attention``,
+``dcp_workspace_size``, ``dcp_workspace_bytes``, ``dcp_sparse_pair_bias_attention``,
 ``dcp_sparse_workspace_size``, ``dcp_knn_topk``, ``dcp_topk_merge``,
 ``dcp_pair_transition``, ``dcp_transition_workspace_size``, ``dcp_scatter_mean``,
 ``dcp_scatter_mean_workspace_size``) and accept torch tensors (device pointers are taken
@@ -21,7 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libdcp.so")
 
 DCP_F32, DCP_BF16 = 0, 1
 DCP_OK, DCP_ERR_INVALID_ARGUMENT, DCP_ERR_UNSUPPORTED, DCP_ERR_WORKSPACE, DCP_ERR_HIP = 0, -1, -2, -3, -4
-EXPORTS = ("dcp_workspace_size", "dcp_pair_bias_attention", "dcp_pair_bias_attention_partial", "dcp_bias_project",
+EXPORTS = ("dcp_workspace_size", "dcp_workspace_bytes", "dcp_pair_bias_attention", "dcp_pair_bias_attention_partial", "dcp_bias_project",
            "dcp_block_merge",
            "dcp_sparse_workspace_size", "dcp_sparse_pair_bias_attention", "dcp_knn_topk", "dcp_topk_merge",
            "dcp_transition_workspace_size", "dcp_pair_transition", "dcp_scatter_mean_workspace_size",
@@ -64,6 +64,8 @@ def lib() -> ctypes.CDLL:
         vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
         P = ctypes.POINTER
         L.dcp_workspace_size.argtypes = [P(DcpShape), i64, i32, P(sz)]
+        L.dcp_workspace_bytes.argtypes = [P(DcpShape), i64, i32]
+        L.dcp_workspace_bytes.restype = sz
         L.dcp_pair_bias_attention.argtypes = [P(DcpShape), P(DcpWeights), vp, vp, vp, i64, i64, i32, vp, vp, sz, vp]
         L.dcp_pair_bias_attention_partial.argtypes = [P(DcpShape), P(DcpWeights), vp, vp, vp, i64, i64, i64, i64, vp,
                                                       vp, vp, vp, vp, sz, vp]
@@ -132,6 +134,11 @@ def dcp_workspace_size(shape: DcpShape, n_q: int, n_key_blocks: int) -> int:
     out = ctypes.c_size_t()
     _check(lib().dcp_workspace_size(ctypes.byref(shape), n_q, n_key_blocks, ctypes.byref(out)))
     return out.value
+
+
+def dcp_workspace_bytes(shape: Optional[DcpShape], n_q: int, n_key_blocks: int) -> int:
+    """The size-returning query: 0 (with dcp_last_error() set) on invalid arguments."""
+    return int(lib().dcp_workspace_bytes(None if shape is None else ctypes.byref(shape), n_q, n_key_blocks))
 
 
 def dcp_pair_bias_attention(shape: DcpShape, weights: DcpWeights, s: Ptr, z_rows: Ptr, key_mask: Ptr, q_row0: int,

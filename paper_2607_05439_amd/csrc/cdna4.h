@@ -132,12 +132,14 @@ __device__ __forceinline__ void wait_vm() {
 }
 
 // Workgroup barrier without the memory-model fence (which would also wait for
-// every outstanding DMA load); LDS written by ds_write is complete because the
-// compiler waits lgkmcnt(0) before s_barrier.
+// every outstanding DMA load). It first waits for this wave's own LDS reads
+// and writes (lgkmcnt(0)): gfx950 has the back-off barrier, so the compiler
+// does not drain LDS operations before s_barrier by itself, and a read still
+// in flight there could otherwise be overtaken by another wave's refill of the
+// same LDS after the barrier. The "memory" clobbers keep every LDS access on
+// its side of the barrier.
 __device__ __forceinline__ void barrier_lds() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {

@@ -362,6 +362,22 @@ int dcp_workspace_size(const dcp_shape* shape, int64_t n_q, int32_t n_key_blocks
   return ok();
 }
 
+size_t dcp_workspace_bytes(const dcp_shape* shape, int64_t n_q, int32_t n_key_blocks) {
+  size_t bytes = 0;
+  if (!shape) {
+    fail(DCP_ERR_INVALID_ARGUMENT, "shape is NULL");
+    return 0;
+  }
+  if (n_q == 0) {
+    // a valid no-op needs no workspace; an invalid shape still reports why
+    Path path;
+    if (check_call(shape, n_q, n_key_blocks, &path) != DCP_OK) return 0;
+    ok();
+    return 0;
+  }
+  return dcp_workspace_size(shape, n_q, n_key_blocks, &bytes) == DCP_OK ? bytes : 0;
+}
+
 int dcp_pair_bias_attention(const dcp_shape* shape, const dcp_weights* w, const void* s, const void* z_rows,
                             const uint8_t* key_mask, int64_t q_row0, int64_t n_q, int32_t n_key_blocks, void* out,
                             void* workspace, size_t workspace_bytes, void* stream) {

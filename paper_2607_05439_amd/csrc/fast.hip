@@ -79,7 +79,7 @@ __device__ void bias_weights(const float* __restrict__ w_b, const float* __restr
 // z . z^T (row n at lane group n/4, register n%4) gives the sum of squares;
 // bf16 products are exact in fp32.
 __device__ __forceinline__ void pair_bias(const u32x4 (&zb)[4], const bf16x8 (&whi)[4], const bf16x8 (&wlo)[4],
-                                          float eps, int n, f32x4& acc, float& rstd) {
+                                          const f32x4& wsum, float eps, int n, f32x4& acc, float& rstd) {
   bf16x8 ones;
 #pragma unroll
   for (int i = 0; i < 8; ++i) ones[i] = (__bf16)1.0f;
@@ -106,8 +106,31 @@ __device__ __forceinline__ void pair_bias(const u32x4 (&zb)[4], const bf16x8 (&w
   swap16(lo, hi);                      // lo: even group of the pair, hi: odd group
   const float s2 = (tg & 1) ? hi : lo; // group tg: the diagonal entry
   const float mu = s1[0] * (1.0f / kCz);
-  const float var = fmaxf(s2 * (1.0f / kCz) - mu * mu, 0.0f);
+  // s2/c_z - mu^2 with the square formed exactly inside the fma: one rounding
+  // of the exact difference, so a large channel mean (|mu| >> sigma) does not
+  // cancel away the variance's significant bits
+  const float var = fmaxf(fmaf(-mu, mu, s2 * (1.0f / kCz)), 0.0f);
   rstd = __builtin_amdgcn_rsqf(var + eps);
+  // the bf16 hi + lo weights sum to wsum (not exactly 0) per head; remove
+  // wsum * mu so the projection is that of z - mu even when mu is large
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i] = fmaf(-mu, wsum[i], acc[i]);
+}
+
+// Per-head sums of the bias weight operands, sum_c (hi + lo)[h, c], in the
+// accumulator layout of pair_bias (heads 4g..4g+3 in every column): W'' . 1
+// on the matrix cores.
+__device__ __forceinline__ f32x4 bias_weight_sums(const bf16x8 (&whi)[4], const bf16x8 (&wlo)[4]) {
+  bf16x8 ones;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) ones[i] = (__bf16)1.0f;
+  f32x4 r = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    r = mfma32(whi[s], ones, r);
+    r = mfma32(wlo[s], ones, r);
+  }
+  return r;
 }
 
 // ----------------------------------------------------------------------------- projections
@@ -309,6 +332,7 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
 
   bf16x8 whi[4], wlo[4];
   bias_weights(a.w_b, a.gamma, kLog2e, lane, whi, wlo);
+  const f32x4 wsum = bias_weight_sums(whi, wlo);
   bf16x8 qreg[kH];
 #pragma unroll
   for (int h = 0; h < kH; ++h)
@@ -388,7 +412,7 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
         for (int st = 0; st < 4; ++st) zb[st] = zs.c[n][(4 * st + g) ^ n];
         f32x4 acc;
         float rstd;
-        pair_bias(zb, whi, wlo, a.eps, n, acc, rstd);
+        pair_bias(zb, whi, wlo, wsum, a.eps, n, acc, rstd);
 #pragma unroll
         for (int i = 0; i < 4; ++i) b[kk][i] = fmaf(acc[i], rstd, kShift);
       } else {
@@ -468,6 +492,7 @@ __global__ void __launch_bounds__(64) bias_kernel(FastBiasArgs a) {
   const int64_t c_end = min(c_begin + (int64_t)a.cols_per_wave, a.n_cols);
   bf16x8 whi[4], wlo[4];
   bias_weights(a.w_b, a.gamma, 1.0f, lane, whi, wlo);
+  const f32x4 wsum = bias_weight_sums(whi, wlo);
   // per-head constant sum_c W_b[h,c] beta_c + b_b[h] for heads 4g..4g+3
   float cst[4];
 #pragma unroll
@@ -488,7 +513,7 @@ __global__ void __launch_bounds__(64) bias_kernel(FastBiasArgs a) {
   auto column = [&](int64_t c, const u32x4 (&zb)[4]) {
     f32x4 acc;
     float rstd;
-    pair_bias(zb, whi, wlo, a.eps, n, acc, rstd);
+    pair_bias(zb, whi, wlo, wsum, a.eps, n, acc, rstd);
     if (row < a.n_rows) {
       float4 o;
       o.x = fmaf(acc[0], rstd, cst[0]);

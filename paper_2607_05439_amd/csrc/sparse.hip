@@ -334,7 +334,8 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
 }
 
 template <bool kBf16, int KMAX>
-__global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs a) {
+__global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(kBf16 && KMAX == 128 ? 5 : 1)))
+sparse_attn_kernel(SparseAttnArgs a) {
   constexpr int EB = kBf16 ? 2 : 4;  // bytes per element of P, K and V
   constexpr int EPL = 16 / EB;       // K/V elements per lane per 16-byte load
   constexpr int LPN = kHD / EPL;     // lanes per K/V row (16 | 32)
@@ -388,8 +389,17 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
   }
   bf16x4 whi, wlo;       // bf16 path: bias operands
   float wb[kH][4] = {};  // fp32 path: log2(e) W_b[h, ch] gamma[ch] for this lane's 4 channels
+  float wsum[kH] = {};   // bf16 path: per-head sums of the hi + lo operands (wave-uniform)
   if constexpr (kBf16) {
     bias_operands(a.w_b, a.gamma, lane, whi, wlo);
+    bf16x4 ones;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ones[i] = (__bf16)1.0f;
+    f32x4 r = {0.f, 0.f, 0.f, 0.f};
+    r = mfma16(whi, ones, r);
+    r = mfma16(wlo, ones, r);  // rows 0..3 (the heads) of every column, in lane group 0
+#pragma unroll
+    for (int h = 0; h < kH; ++h) wsum[h] = __builtin_amdgcn_readfirstlane(r[h]);
   } else {
 #pragma unroll
     for (int h = 0; h < kH; ++h)
@@ -574,13 +584,19 @@ __global__ void __launch_bounds__(64 * kWaves) sparse_attn_kernel(SparseAttnArgs
         float y0 = hb[0], y1 = hb[0];
         swap16(y0, y1);
         const float mu = y1 * (1.0f / kCap);
-        const float var = fmaxf(s2 * (1.0f / kCap) - mu * mu, 0.0f);
+        // one rounding of s2/c - mu^2 (the square exact inside the fma), and the
+        // operands' own per-head sums times mu removed: exact centring even
+        // when the channel mean is large against the spread
+        const float var = fmaxf(fmaf(-mu, mu, s2 * (1.0f / kCap)), 0.0f);
         const float rstd = __builtin_amdgcn_rsqf(var + a.eps);
         if (g == 0) {
           const bool ok = pos < count;
+          float hc[kH];
+#pragma unroll
+          for (int h = 0; h < kH; ++h) hc[h] = fmaf(-mu, wsum[h], hb[h]);
           *reinterpret_cast<float4*>(lb[pos]) =
-              ok ? make_float4(fmaf(rstd, hb[0], kShift), fmaf(rstd, hb[1], kShift), fmaf(rstd, hb[2], kShift),
-                               fmaf(rstd, hb[3], kShift))
+              ok ? make_float4(fmaf(rstd, hc[0], kShift), fmaf(rstd, hc[1], kShift), fmaf(rstd, hc[2], kShift),
+                               fmaf(rstd, hc[3], kShift))
                  : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
         }
       }

@@ -56,6 +56,7 @@ class Device:
                   for k, v in self.w_host.items()}
         self.mask = None if self.mask_host is None else torch.from_numpy(self.mask_host).to(self.dev)
         n = wl.n_tok
+        self.z_host_override = z_override
         if z_override is not None:
             self.z = self._to_dev(z_override)
         else:
@@ -105,8 +106,12 @@ class Device:
         return out
 
     def oracle_rows(self, rows: Sequence[int], n_blocks: int = 1, drop_affine: bool = False) -> np.ndarray:
-        """fp64 oracle on the generator's host copy of the same inputs."""
-        z_rows = synth.z_host(self.wl, rows)
+        """fp64 oracle on the generator's host copy of the same inputs (or on
+        the host array the device z was uploaded from)."""
+        if self.z_host_override is not None:
+            z_rows = np.ascontiguousarray(self.z_host_override[np.asarray(rows, dtype=np.int64)])
+        else:
+            z_rows = synth.z_host(self.wl, rows)
         w = dict(self.w_host)
         if drop_affine:
             w["b_b"] = None

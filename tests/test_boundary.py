@@ -56,6 +56,27 @@ def test_workspace_sizes():
     assert dcp.dcp_workspace_size(shape(), 24000, 12) > big
 
 
+def test_workspace_bytes_matches_status_form():
+    """dcp_workspace_bytes (the size-returning query) agrees with
+    dcp_workspace_size on valid shapes and is 0, with a message, on bad ones."""
+    cases = [(shape(), 24000, 6), (shape(), 24000, 1), (shape(), 3000, 4), (shape(n_tokens=12000), 3000, 4),
+             (shape(n_tokens=1024), 1024, 4), (shape(n_tokens=4800), 4800, 10), (shape(n_tokens=1), 1, 1),
+             (shape(n_tokens=128, c_s=128, c_z=32, n_heads=4, head_dim=32, act_dtype=dcp.DCP_F32), 128, 4),
+             (shape(n_tokens=50, c_s=40, c_z=64, n_heads=4, head_dim=16), 40, 3)]
+    for sh, n_q, n_kb in cases:
+        got = dcp.dcp_workspace_bytes(sh, n_q, n_kb)
+        assert got == dcp.dcp_workspace_size(sh, n_q, n_kb) > 0
+        assert dcp.dcp_last_error() == ""
+    assert dcp.dcp_workspace_bytes(shape(), 0, 6) == 0
+    assert dcp.dcp_last_error() == ""
+    bad = [(None, 10, 1), (shape(n_tokens=0), 10, 1), (shape(c_z=512), 10, 1), (shape(n_heads=32), 10, 1),
+           (shape(ln_eps=float("nan")), 10, 1), (shape(), -1, 1), (shape(), 24001, 1), (shape(), 100, 0),
+           (shape(), 100, 24001), (shape(n_tokens=0), 0, 1)]
+    for sh, n_q, n_kb in bad:
+        assert dcp.dcp_workspace_bytes(sh, n_q, n_kb) == 0
+        assert len(dcp.dcp_last_error()) > 0
+
+
 @pytest.mark.parametrize("kw,code", [
     (dict(n_tokens=0), dcp.DCP_ERR_INVALID_ARGUMENT),
     (dict(c_z=0), dcp.DCP_ERR_INVALID_ARGUMENT),
@@ -310,3 +331,4 @@ def test_scatter_mean_arguments():
     assert ok(ws=None) == W
     assert ok(wsb=100) == W
     assert ok(nt=0, out=None, ws=None) == dcp.DCP_OK
+
