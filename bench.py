@@ -118,7 +118,7 @@ def cpu_baseline(wl, s_host, w_host, mask, seconds):
     rows = sorted(int(x) for x in rng.choice(wl.n_tok, size=min(n_rows, wl.n_tok), replace=False))
     z = synth.z_host(wl, rows)
     t0 = time.perf_counter()
-    oracle.attention(s_host, z, rows, mask, w_host, wl.n_heads, wl.head_dim)
+    ref = oracle.attention(s_host, z, rows, mask, w_host, wl.n_heads, wl.head_dim)
     t_run = time.perf_counter() - t0
     per_row = (t_run - t_fixed) / len(rows)
     n_q_total = sum(nq for _, nq in wl.stripes)
@@ -141,7 +141,7 @@ def cpu_baseline(wl, s_host, w_host, mask, seconds):
     per_row1 = max(t_run1 - t_fixed1, 1e-9) / len(rows1)
     t_layer1 = t_fixed1 * len(wl.stripes) + per_row1 * n_q_total
     return {"t_layer_s": t_layer, "rows": len(rows), "t_run_s": t_run, "threads": threads, "t_fixed_s": t_fixed,
-            "t_layer_1thread_s": t_layer1, "rows_1thread": len(rows1)}
+            "t_layer_1thread_s": t_layer1, "rows_1thread": len(rows1), "row_ids": rows, "ref": ref}
 
 
 def host_cpu_model():
@@ -613,80 +613,113 @@ def scatter_main(args, name):
     print(json.dumps(line), flush=True)
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="asm24000_bf16")
-    ap.add_argument("--cpu-seconds", type=float, default=20.0)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--calibrate-bytes", type=int, default=1 << 31,
-                    help="bytes for the plain-copy calibration kernel (counter scaling)")
-    args = ap.parse_args()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print("bench.py measures a single GPU: the library has no multi-GPU path (no collectives or "
-              "sharding across GPUs); run with --gpus 1.", file=sys.stderr)
-        sys.exit(2)
+def flops_per_pair(wl):
+    """Algorithmic flops per valid (query, key) pair: LayerNorm statistics and
+    normalisation (3 c_z), bias projection (2 c_z H), QK^T and PV (4 H d), the
+    bias add and the softmax (2 H + 6 H)."""
+    return 3 * wl.c_z + 2 * wl.n_heads + 2 * wl.c_z * wl.n_heads + 4 * wl.n_heads * wl.head_dim + 6 * wl.n_heads
 
+
+class AttentionLayer:
+    """Device inputs and buffers of one token-attention workload, and its step."""
+
+    def __init__(self, wl, dev, sp):
+        import numpy as np
+        import torch
+        import paper_2607_05439_amd as dcp
+        import synth
+        self.wl, self.sp = wl, sp
+        n, cz = wl.n_tok, wl.c_z
+        zdt = torch.bfloat16 if wl.bf16 else torch.float32
+        self.z = torch.empty((n, n, cz), dtype=zdt, device=dev)
+        synth.z_fill_device(wl, self.z.data_ptr(), 0, n, sp)
+        self.s_host = synth.s_host(wl)
+        self.w_host = synth.weights(wl)
+        self.mask_host = synth.mask_host(wl)
+        if wl.bf16:
+            self.s = torch.from_numpy(self.s_host.view(np.int16)).view(torch.bfloat16).to(dev)
+        else:
+            self.s = torch.from_numpy(self.s_host).to(dev)
+        self.w = {k: (None if v is None else torch.from_numpy(v).to(dev)) for k, v in self.w_host.items()}
+        self.mask = None if self.mask_host is None else torch.from_numpy(self.mask_host).to(dev)
+        out_dtype = dcp.DCP_BF16 if wl.bf16 else dcp.DCP_F32
+        act = dcp.DCP_BF16 if wl.bf16 else dcp.DCP_F32
+        self.shape = dcp.make_shape(n, wl.c_s, cz, wl.n_heads, wl.head_dim, act, out_dtype, 1e-5)
+        w = self.w
+        self.weights = dcp.make_weights(w["w_q"], w["w_k"], w["w_v"], w["w_g"], w["w_b"], w["b_b"], w["ln_gamma"],
+                                        w["ln_beta"])
+        hd = wl.n_heads * wl.head_dim
+        self.ws_bytes = max(dcp.dcp_workspace_size(self.shape, nq, wl.n_key_blocks) for _, nq in wl.stripes)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)
+        self.outs = [torch.empty((nq, hd), dtype=zdt, device=dev) for _, nq in wl.stripes]
+        self.n_valid = n if self.mask_host is None else int(self.mask_host.sum())
+        self.bytes_per_launch = [nq * self.n_valid * cz * wl.elem_bytes for _, nq in wl.stripes]
+        self.bytes_per_step = sum(self.bytes_per_launch)
+        # algorithmic flops: the pairs of every stripe, plus q, g of the query rows and k, v of the keys once
+        self.pair_flops_per_launch = [nq * self.n_valid * flops_per_pair(wl) for _, nq in wl.stripes]
+        n_q_total = sum(nq for _, nq in wl.stripes)
+        self.flops_per_step = (sum(self.pair_flops_per_launch) + 2 * wl.c_s * hd * 2 * (n_q_total + n))
+
+    def step(self, evs=None):
+        import paper_2607_05439_amd as dcp
+        wl = self.wl
+        n, cz = wl.n_tok, wl.c_z
+        for i, (q0, nq) in enumerate(wl.stripes):
+            if evs is not None:
+                dcp.dcp_set_timing_events(*evs[i])
+            dcp.dcp_pair_bias_attention(self.shape, self.weights, self.s,
+                                        self.z.data_ptr() + q0 * n * cz * wl.elem_bytes, self.mask, q0, nq,
+                                        wl.n_key_blocks, self.outs[i], self.ws, self.ws_bytes, self.sp)
+        if evs is not None:
+            dcp.dcp_set_timing_events(None, None)
+
+    def time(self, hip, stream, steps, warmup):
+        """ms per step (torch events around the steps) and the attention
+        kernel's time of every launch (HIP events on the library's stream)."""
+        import torch
+        for _ in range(warmup):
+            self.step()
+        torch.cuda.synchronize()
+        kernel_evs = [[(hip.event(), hip.event()) for _ in self.wl.stripes] for _ in range(steps)]
+        t_start, t_stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t_start.record(stream)
+        for k in range(steps):
+            self.step(kernel_evs[k])
+        t_stop.record(stream)
+        torch.cuda.synchronize()
+        ms_per_step = t_start.elapsed_time(t_stop) / steps
+        k_ms = [hip.elapsed_ms(a, b) for evs in kernel_evs for (a, b) in evs]
+        for evs in kernel_evs:
+            for a, b in evs:
+                hip.destroy(a)
+                hip.destroy(b)
+        return ms_per_step, k_ms
+
+
+def launch_stats(k_ms):
+    k_sorted = sorted(k_ms)
+    return {"median": round(k_sorted[len(k_sorted) // 2], 4), "min": round(k_sorted[0], 4),
+            "max": round(k_sorted[-1], 4), "launches": len(k_ms)}
+
+
+def attention_main(args, wl):
     import numpy as np
     import torch
     import paper_2607_05439_amd as dcp
     import synth
 
-    if args.workload in synth.ATOM_WORKLOADS:
-        return sparse_main(args, synth.ATOM_WORKLOADS[args.workload])
-    if args.workload in synth.KNN_WORKLOADS:
-        return knn_main(args, synth.KNN_WORKLOADS[args.workload])
-    if args.workload in synth.TRANSITION_WORKLOADS:
-        return transition_main(args, args.workload)
-    if args.workload in synth.SCATTER_WORKLOADS:
-        return scatter_main(args, args.workload)
-    wl = synth.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
     n, cz = wl.n_tok, wl.c_z
     progress(f"workload {wl.name}: N={n} c_z={cz} H={wl.n_heads} d={wl.head_dim} n_kb={wl.n_key_blocks} "
              f"z={n * n * cz * wl.elem_bytes / 1e9:.1f} GB")
-    zdt = torch.bfloat16 if wl.bf16 else torch.float32
-    z = torch.empty((n, n, cz), dtype=zdt, device=dev)
-    synth.z_fill_device(wl, z.data_ptr(), 0, n, sp)
-    s_host = synth.s_host(wl)
-    w_host = synth.weights(wl)
-    mask_host = synth.mask_host(wl)
-    if wl.bf16:
-        s = torch.from_numpy(s_host.view(np.int16)).view(torch.bfloat16).to(dev)
-    else:
-        s = torch.from_numpy(s_host).to(dev)
-    w = {k: (None if v is None else torch.from_numpy(v).to(dev)) for k, v in w_host.items()}
-    mask = None if mask_host is None else torch.from_numpy(mask_host).to(dev)
-    out_dtype = dcp.DCP_BF16 if wl.bf16 else dcp.DCP_F32
-    shape = dcp.make_shape(n, wl.c_s, cz, wl.n_heads, wl.head_dim, dcp.DCP_BF16 if wl.bf16 else dcp.DCP_F32,
-                           out_dtype, 1e-5)
-    weights = dcp.make_weights(w["w_q"], w["w_k"], w["w_v"], w["w_g"], w["w_b"], w["b_b"], w["ln_gamma"],
-                               w["ln_beta"])
-    hd = wl.n_heads * wl.head_dim
-    ws_bytes = max(dcp.dcp_workspace_size(shape, nq, wl.n_key_blocks) for _, nq in wl.stripes)
-    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
-    outs = [torch.empty((nq, hd), dtype=torch.bfloat16 if wl.bf16 else torch.float32, device=dev)
-            for _, nq in wl.stripes]
-    n_valid = n if mask_host is None else int(mask_host.sum())
-    bytes_per_launch = [nq * n_valid * cz * wl.elem_bytes for _, nq in wl.stripes]
-    bytes_per_step = sum(bytes_per_launch)
+    layer = AttentionLayer(wl, dev, sp)
+    z = layer.z
+    weights = layer.weights
     torch.cuda.synchronize()
-
     hip = Hip()
-
-    def step(evs=None):
-        for i, (q0, nq) in enumerate(wl.stripes):
-            if evs is not None:
-                dcp.dcp_set_timing_events(*evs[i])
-            dcp.dcp_pair_bias_attention(shape, weights, s, z.data_ptr() + q0 * n * cz * wl.elem_bytes, mask, q0,
-                                        nq, wl.n_key_blocks, outs[i], ws, ws_bytes, sp)
-        if evs is not None:
-            dcp.dcp_set_timing_events(None, None)
 
     # calibration kernels (outside the timed region): a plain copy of known size
     # for counter scaling, and a plain streaming read of z for achievable bandwidth
@@ -717,29 +750,18 @@ def main():
     progress(f"streaming read of z: {read_gbps:.0f} GB/s; attention access pattern, no arithmetic: "
              f"{pattern_gbps or 0:.0f} GB/s")
 
-    progress(f"warmup {args.warmup} steps")
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    kernel_evs = [[(hip.event(), hip.event()) for _ in wl.stripes] for _ in range(args.steps)]
-    progress(f"timing {args.steps} steps")
-    t_start, t_stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record(stream)
-    for k in range(args.steps):
-        step(kernel_evs[k])
-    t_stop.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = t_start.elapsed_time(t_stop) / args.steps
-    k_ms = [hip.elapsed_ms(a, b) for evs in kernel_evs for (a, b) in evs]
+    progress(f"warmup {args.warmup} steps, timing {args.steps} steps")
+    ms_per_step, k_ms = layer.time(hip, stream, args.steps, args.warmup)
     avg_kernel_ms = sum(k_ms) / len(k_ms)
-    k_sorted = sorted(k_ms)
-    launch_stats = {"median": round(k_sorted[len(k_sorted) // 2], 4), "min": round(k_sorted[0], 4),
-                    "max": round(k_sorted[-1], 4), "launches": len(k_ms)}
+    bytes_per_step = layer.bytes_per_step
+    n_valid, bytes_launch0, flops_step = layer.n_valid, layer.bytes_per_launch[0], layer.flops_per_step
     achieved = (bytes_per_step / len(wl.stripes)) / (avg_kernel_ms * 1e-3) / 1e9
     value = bytes_per_step / (ms_per_step * 1e-3) / 1e9
+    kernel_tflops = (sum(layer.pair_flops_per_launch) / len(wl.stripes)) / (avg_kernel_ms * 1e-3) / 1e12
+    layer_tflops = flops_step / (ms_per_step * 1e-3) / 1e12
     progress(f"{ms_per_step:.3f} ms/layer, attention kernel {avg_kernel_ms:.3f} ms/launch, "
-             f"{achieved:.0f} GB/s in the kernel ({achieved / PEAK_HBM_GBPS:.1%} of peak)")
+             f"{achieved:.0f} GB/s in the kernel ({achieved / PEAK_HBM_GBPS:.1%} of peak), "
+             f"{kernel_tflops:.1f} TFLOP/s in the kernel ({kernel_tflops / PEAK_BF16_TFLOPS:.1%} of bf16 peak)")
 
     # the materialised bias alone (dcp_bias_project) on a stripe of rows: the z
     # stream with LayerNorm and the c_z -> H projection but no attention, as a
@@ -765,9 +787,10 @@ def main():
         progress(f"dcp_bias_project on {nr} rows: {b_med:.3f} ms, z read at {bias_ref['z_read_GBps']:.0f} GB/s")
 
     cpu = None
+    err = None
     if not args.no_cpu_baseline:
         progress(f"cpu baseline: oracle on sampled rows (~{args.cpu_seconds:.0f} s)")
-        cb = cpu_baseline(wl, s_host, w_host, mask_host, args.cpu_seconds)
+        cb = cpu_baseline(wl, layer.s_host, layer.w_host, layer.mask_host, args.cpu_seconds)
         cpu = {"value": round(bytes_per_step / cb["t_layer_s"] / 1e9, 6), "unit": "GB/s", "cores": cb["threads"],
                "kind": "oracle",
                "sample": f"{cb['rows']} of {sum(nq for _, nq in wl.stripes)} query rows in {cb['t_run_s']:.1f} s "
@@ -779,6 +802,49 @@ def main():
                "one_thread": {"value": round(bytes_per_step / cb["t_layer_1thread_s"] / 1e9, 6), "unit": "GB/s",
                               "sample": f"{cb['rows_1thread']} of the sampled rows on one host thread",
                               "ms_per_layer_extrapolated": round(cb["t_layer_1thread_s"] * 1e3, 1)}}
+        # the error of the timed layer's output on the same sampled rows
+        got = np.empty_like(cb["ref"])
+        for r_i, r in enumerate(cb["row_ids"]):
+            for s_i, (q0, nq) in enumerate(wl.stripes):
+                if q0 <= r < q0 + nq:
+                    got[r_i] = layer.outs[s_i][r - q0].float().cpu().numpy()
+                    break
+        den = float(np.max(np.abs(cb["ref"])))
+        e = float(np.max(np.abs(got - cb["ref"]))) / (den if den > 0 else 1.0)
+        err = {"max_rel_err": float(f"{e:.4g}"), "rows": cb["rows"],
+               "tolerance": 1e-2 if wl.bf16 else 1e-5,
+               "definition": "max|out_gpu - out_oracle| / max|out_oracle| over the sampled query rows, "
+                             "output of the last timed step"}
+        progress(f"max rel err on {cb['rows']} sampled rows: {e:.3e}")
+
+    # the other attention workloads, each timed after the previous one's tensors are freed
+    extras = None
+    if not args.no_extra_configs and wl.name == "asm24000_bf16":
+        extras = {}
+        del z, layer
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        for name in ("grid12000_bf16", "ico4800_bf16", "pad1024_bf16"):
+            xw = synth.WORKLOADS[name]
+            progress(f"extra workload {name}")
+            xl = AttentionLayer(xw, dev, sp)
+            x_ms, x_k = xl.time(hip, stream, args.extra_steps, 3)
+            x_avg = sum(x_k) / len(x_k)
+            x_gbps = (xl.bytes_per_step / len(xw.stripes)) / (x_avg * 1e-3) / 1e9
+            x_tf = (sum(xl.pair_flops_per_launch) / len(xw.stripes)) / (x_avg * 1e-3) / 1e12
+            extras[name] = {
+                "ms_per_layer": round(x_ms, 4), "layer_GBps": round(xl.bytes_per_step / (x_ms * 1e-3) / 1e9, 1),
+                "kernel_ms": round(x_avg, 4), "kernel_launch_ms": launch_stats(x_k),
+                "kernel_GBps": round(x_gbps, 1), "frac": round(x_gbps / PEAK_HBM_GBPS, 4),
+                "kernel_TFLOPs": round(x_tf, 1), "layer_TFLOPs": round(xl.flops_per_step / (x_ms * 1e-3) / 1e12, 1),
+                "per_tile_ms": round(x_avg / xw.n_key_blocks, 4), "n_key_blocks": xw.n_key_blocks,
+                "stripes": [list(x) for x in xw.stripes], "algorithmic_bytes_per_step": xl.bytes_per_step,
+                "steps": args.extra_steps}
+            progress(f"  {x_ms:.3f} ms/layer, kernel {x_avg:.3f} ms/launch, {x_gbps:.0f} GB/s "
+                     f"({x_gbps / PEAK_HBM_GBPS:.1%}), {x_tf:.1f} TFLOP/s")
+            del xl
+            torch.cuda.synchronize()
+            torch.cuda.empty_cache()
 
     traffic = stored_traffic(wl.name)
     line = {
@@ -801,17 +867,59 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic,
                      "kernel": "attn_kernel", "kernel_ms": round(avg_kernel_ms, 4),
-                     "algorithmic_bytes_per_launch": bytes_per_launch[0]},
-        "attn_launch_ms": launch_stats,
+                     "algorithmic_bytes_per_launch": bytes_launch0},
+        "tflops": {"kernel": round(kernel_tflops, 1), "layer": round(layer_tflops, 1), "peak": PEAK_BF16_TFLOPS,
+                   "kernel_frac_of_bf16_peak": round(kernel_tflops / PEAK_BF16_TFLOPS, 4),
+                   "flops_per_valid_pair": flops_per_pair(wl), "flops_per_step": flops_step,
+                   "note": "algorithmic flops (pairs x per-pair flops; projections once per token) over HIP-event "
+                           "kernel time and the layer's step time; the path is HBM-bound"},
+        "max_rel_err": err,
+        "attn_launch_ms": launch_stats(k_ms),
         # one launch covers a stripe of query rows against n_key_blocks key blocks:
         # the time of one (stripe, key block) tile of a grid schedule
         "per_tile_ms": round(avg_kernel_ms / wl.n_key_blocks, 4),
         "bias_project_stripe": bias_ref,
         "streaming_read_GBps": round(read_gbps, 1),
         "pattern_read_GBps": None if pattern_gbps is None else round(pattern_gbps, 1),
+        "other_configs": extras,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="asm24000_bf16")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra-configs", action="store_true",
+                    help="skip timing the smaller attention workloads after the default one")
+    ap.add_argument("--extra-steps", type=int, default=20)
+    ap.add_argument("--calibrate-bytes", type=int, default=1 << 31,
+                    help="bytes for the plain-copy calibration kernel (counter scaling)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures a single GPU: the library has no multi-GPU path (no collectives or "
+              "sharding across GPUs); run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2607_05439_amd as dcp
+    import synth
+
+    if args.workload in synth.ATOM_WORKLOADS:
+        return sparse_main(args, synth.ATOM_WORKLOADS[args.workload])
+    if args.workload in synth.KNN_WORKLOADS:
+        return knn_main(args, synth.KNN_WORKLOADS[args.workload])
+    if args.workload in synth.TRANSITION_WORKLOADS:
+        return transition_main(args, args.workload)
+    if args.workload in synth.SCATTER_WORKLOADS:
+        return scatter_main(args, args.workload)
+    return attention_main(args, synth.WORKLOADS[args.workload])
 
 
 if __name__ == "__main__":

@@ -176,9 +176,9 @@ int dcp_block_merge(int32_t n_parts, int64_t n_rows, int32_t n_heads, int32_t he
  * Sparse (kNN) pair-biased gated attention over atoms.
  *
  * Paper, Methods, "RFDiffusion 3 preliminaries and notation": atoms carry a
- * single track A[L, c_atom] and a pair track P[L, L, c_ap]; atom attention is
- * sparse, each query atom attending to a budget of k neighbours, and the slice
- * of P at those neighbours is gathered and projected to the per-head bias.
+ * single track A[L, c_atom] and a pair track P[L, L, c_ap]; the atom-level
+ * attention is not dense: every query atom sees only k neighbour atoms, whose
+ * entries of P are gathered and projected per head into the bias.
  * Appendix "Distributed kNN for sparse atom attention": per ring step the
  * neighbour indices are filtered to the visited column block, K, V and the
  * bias are gathered there, and the logits are merged into the running softmax.

@@ -330,10 +330,10 @@ int oracle_attention(int64_t n_tok, int c_s, int c_z, int n_heads, int d, const 
 /* ---------------------------------------------------------------------------
  * Sparse (kNN) pair-biased atom attention.
  *
- * Paper, Methods, "RFDiffusion 3 preliminaries and notation": atom attention
- * is sparse: each query atom attends to a budget of k neighbours, and the
- * slice of the atom pair track P at those k indices is gathered and projected
- * to the per-head bias. Appendix "Distributed kNN for sparse atom attention":
+ * Paper, Methods, "RFDiffusion 3 preliminaries and notation": the atom-level
+ * attention is not dense; every query atom looks at a fixed number k of
+ * neighbour atoms only, and the bias for those k keys comes from the matching
+ * entries of the atom pair track P, gathered and projected per head. Appendix "Distributed kNN for sparse atom attention":
  * at each ring step the indices are filtered to the visited column block, K, V
  * and B are gathered there, and the logits are merged into the running
  * softmax. Readings as for the token path (LayerNorm over the c_ap channels of
