@@ -121,6 +121,26 @@ int dcp_pair_bias_attention(const dcp_shape* shape, const dcp_weights* weights, 
                             int32_t n_key_blocks, void* out, void* workspace, size_t workspace_bytes,
                             void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * call as dcp_pair_bias_attention, with the same arguments, kernels and
+ * results, but its scratch comes from a library-owned device array of
+ * DCP_NOALLOC_SCRATCH_BYTES on each GPU (held from the first call on that GPU
+ * until the process ends) instead of a workspace argument. It allocates and
+ * frees nothing and calls no allocating routine. A call whose
+ * dcp_workspace_size() exceeds DCP_NOALLOC_SCRATCH_BYTES returns
+ * DCP_ERR_WORKSPACE before anything is launched (split the query rows into
+ * stripes). The array used is the current device's; `stream` must belong to
+ * the current device (DCP_ERR_INVALID_ARGUMENT otherwise). Every call on one
+ * GPU shares that array: calls that overlap in time on one GPU (different
+ * streams, or host threads) race and give undefined results; calls ordered on
+ * one stream do not. Nothing in the array needs clearing: every byte a call
+ * reads is first written by the same call. */
+#define DCP_NOALLOC_SCRATCH_BYTES (128u << 20) /* 128 MiB */
+int dcp_pair_bias_attention_noalloc(const dcp_shape* shape, const dcp_weights* weights, const void* s,
+                                    const void* z_rows, const uint8_t* key_mask, int64_t q_row0, int64_t n_q,
+                                    int32_t n_key_blocks, void* out, void* stream);
+
 /* One ring step (Appendix "Q/K/V layout and the ring loop": a query stripe
  * against the key block visiting this rank; the 2D scheme's inner loop): the
  * partial attention state of query rows [q_row0, q_row0 + n_q) over the keys

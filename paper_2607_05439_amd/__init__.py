@@ -2,7 +2,7 @@
 
 Every step of the computation runs in the library's HIP kernels; PyTorch is
 used for device memory and streams. The functions carry the C names
-(``dcp_pair_bias_attention``, ``dcp_pair_bias_attention_partial``, ``dcp_bias_project``, ``dcp_block_merge``,
+(``dcp_pair_bias_attention``, ``dcp_pair_bias_attention_noalloc``, ``dcp_pair_bias_attention_partial``, ``dcp_bias_project``, ``dcp_block_merge``,
 ``dcp_workspace_size``, ``dcp_workspace_bytes``, ``dcp_sparse_pair_bias_attention``,
 ``dcp_sparse_workspace_size``, ``dcp_knn_topk``, ``dcp_topk_merge``,
 ``dcp_pair_transition``, ``dcp_transition_workspace_size``, ``dcp_scatter_mean``,
@@ -21,7 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libdcp.so")
 
 DCP_F32, DCP_BF16 = 0, 1
 DCP_OK, DCP_ERR_INVALID_ARGUMENT, DCP_ERR_UNSUPPORTED, DCP_ERR_WORKSPACE, DCP_ERR_HIP = 0, -1, -2, -3, -4
-EXPORTS = ("dcp_workspace_size", "dcp_workspace_bytes", "dcp_pair_bias_attention", "dcp_pair_bias_attention_partial", "dcp_bias_project",
+EXPORTS = ("dcp_workspace_size", "dcp_workspace_bytes", "dcp_pair_bias_attention", "dcp_pair_bias_attention_noalloc", "dcp_pair_bias_attention_partial", "dcp_bias_project",
            "dcp_block_merge",
            "dcp_sparse_workspace_size", "dcp_sparse_pair_bias_attention", "dcp_knn_topk", "dcp_topk_merge",
            "dcp_transition_workspace_size", "dcp_pair_transition", "dcp_scatter_mean_workspace_size",
@@ -67,6 +67,7 @@ def lib() -> ctypes.CDLL:
         L.dcp_workspace_bytes.argtypes = [P(DcpShape), i64, i32]
         L.dcp_workspace_bytes.restype = sz
         L.dcp_pair_bias_attention.argtypes = [P(DcpShape), P(DcpWeights), vp, vp, vp, i64, i64, i32, vp, vp, sz, vp]
+        L.dcp_pair_bias_attention_noalloc.argtypes = [P(DcpShape), P(DcpWeights), vp, vp, vp, i64, i64, i32, vp, vp]
         L.dcp_pair_bias_attention_partial.argtypes = [P(DcpShape), P(DcpWeights), vp, vp, vp, i64, i64, i64, i64, vp,
                                                       vp, vp, vp, vp, sz, vp]
         L.dcp_bias_project.argtypes = [P(DcpShape), P(DcpWeights), vp, i64, i64, i64, vp, vp]
@@ -81,7 +82,8 @@ def lib() -> ctypes.CDLL:
         L.dcp_scatter_mean_workspace_size.argtypes = [i64, i32, P(sz)]
         L.dcp_scatter_mean.argtypes = [i64, i64, i32, i32, i32, vp, vp, vp, vp, sz, vp]
         L.dcp_set_timing_events.argtypes = [vp, vp]
-        for f in (L.dcp_workspace_size, L.dcp_pair_bias_attention, L.dcp_pair_bias_attention_partial,
+        for f in (L.dcp_workspace_size, L.dcp_pair_bias_attention, L.dcp_pair_bias_attention_noalloc,
+                  L.dcp_pair_bias_attention_partial,
                   L.dcp_bias_project, L.dcp_block_merge,
                   L.dcp_sparse_workspace_size, L.dcp_sparse_pair_bias_attention, L.dcp_knn_topk, L.dcp_topk_merge,
                   L.dcp_transition_workspace_size, L.dcp_pair_transition, L.dcp_scatter_mean_workspace_size,
@@ -147,6 +149,16 @@ def dcp_pair_bias_attention(shape: DcpShape, weights: DcpWeights, s: Ptr, z_rows
     _check(lib().dcp_pair_bias_attention(ctypes.byref(shape), ctypes.byref(weights), _ptr(s), _ptr(z_rows),
                                          _ptr(key_mask), q_row0, n_q, n_key_blocks, _ptr(out), _ptr(workspace),
                                          workspace_bytes, _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20  # DCP_NOALLOC_SCRATCH_BYTES
+
+
+def dcp_pair_bias_attention_noalloc(shape: DcpShape, weights: DcpWeights, s: Ptr, z_rows: Ptr, key_mask: Ptr,
+                                    q_row0: int, n_q: int, n_key_blocks: int, out: Ptr, stream=None) -> None:
+    _check(lib().dcp_pair_bias_attention_noalloc(ctypes.byref(shape), ctypes.byref(weights), _ptr(s), _ptr(z_rows),
+                                                 _ptr(key_mask), q_row0, n_q, n_key_blocks, _ptr(out),
+                                                 _stream(stream)))
 
 
 def dcp_pair_bias_attention_partial(shape: DcpShape, weights: DcpWeights, s: Ptr, z_rows: Ptr, key_mask: Ptr,

@@ -8,6 +8,8 @@
 #include <stdint.h>
 #include <stdio.h>
 
+#include <mutex>
+
 #include "dcp.h"
 #include "dcp_internal.h"
 
@@ -333,6 +335,38 @@ static int run_attention(const dcp_shape* shape, const dcp_weights* w, const voi
   return ok();
 }
 
+// ---- scratch of the entry point that allocates nothing
+// One array per GPU the library runs on, held until the process ends. In host
+// code `scratch` names a host-side stand-in, never the device memory: host
+// code uses only the address hipGetSymbolAddress returns for each device.
+static __device__ __align__(256) unsigned char scratch[DCP_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The scratch address on the current device, looked up once per device.
+int scratch_on_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(DCP_ERR_HIP, "hipGetDevice failed: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(DCP_ERR_UNSUPPORTED, "device %d beyond the %d supported", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(DCP_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d failed: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return DCP_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* dcp_last_error(void) { return g_err; }
@@ -383,6 +417,35 @@ int dcp_pair_bias_attention(const dcp_shape* shape, const dcp_weights* w, const 
                             void* workspace, size_t workspace_bytes, void* stream) {
   return run_attention(shape, w, s, z_rows, key_mask, q_row0, n_q, n_key_blocks, 0, shape ? shape->n_tokens : 0, out,
                        nullptr, workspace, workspace_bytes, stream);
+}
+
+int dcp_pair_bias_attention_noalloc(const dcp_shape* shape, const dcp_weights* w, const void* s, const void* z_rows,
+                                    const uint8_t* key_mask, int64_t q_row0, int64_t n_q, int32_t n_key_blocks,
+                                    void* out, void* stream) {
+  // every size check first: an oversized call touches neither the GPU nor the runtime
+  size_t need = 0;
+  int rc = dcp_workspace_size(shape, n_q, n_key_blocks, &need);
+  if (rc) return rc;
+  if (need > (size_t)DCP_NOALLOC_SCRATCH_BYTES)
+    return fail(DCP_ERR_WORKSPACE,
+                "the call needs %zu bytes of scratch, beyond the %zu-byte maximum of "
+                "dcp_pair_bias_attention_noalloc; split the query rows into smaller stripes or use "
+                "dcp_pair_bias_attention with a workspace",
+                need, (size_t)DCP_NOALLOC_SCRATCH_BYTES);
+  if (n_q == 0) return run_attention(shape, w, s, z_rows, key_mask, q_row0, n_q, n_key_blocks, 0,
+                                     shape->n_tokens, out, nullptr, nullptr, 0, stream);
+  if (stream) {
+    int sdev = -1, cdev = -1;
+    hipError_t e = hipStreamGetDevice(static_cast<hipStream_t>(stream), &sdev);
+    if (e == hipSuccess) e = hipGetDevice(&cdev);
+    if (e != hipSuccess) return fail(DCP_ERR_HIP, "stream device query failed: %s", hipGetErrorString(e));
+    if (sdev != cdev)
+      return fail(DCP_ERR_INVALID_ARGUMENT, "the stream belongs to device %d, the current device is %d", sdev, cdev);
+  }
+  void* ptr = nullptr;
+  if ((rc = scratch_on_current_device(&ptr)) != DCP_OK) return rc;
+  return run_attention(shape, w, s, z_rows, key_mask, q_row0, n_q, n_key_blocks, 0, shape->n_tokens, out, nullptr,
+                       ptr, (size_t)DCP_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int dcp_pair_bias_attention_partial(const dcp_shape* shape, const dcp_weights* w, const void* s, const void* z_rows,

@@ -332,3 +332,26 @@ def test_scatter_mean_arguments():
     assert ok(wsb=100) == W
     assert ok(nt=0, out=None, ws=None) == dcp.DCP_OK
 
+
+def test_noalloc_rejects_beyond_its_scratch():
+    """dcp_pair_bias_attention_noalloc checks sizes before anything else: a
+    call needing more than DCP_NOALLOC_SCRATCH_BYTES is refused on the host
+    (here without a GPU), bad arguments get their usual codes."""
+    assert dcp.NOALLOC_SCRATCH_BYTES == 128 << 20
+    lib = dcp.lib()
+
+    def call(sh, n_q, n_kb, q_row0=0):
+        return lib.dcp_pair_bias_attention_noalloc(ctypes.byref(sh), ctypes.byref(weights()), FAKE, FAKE, None,
+                                                   q_row0, n_q, n_kb, FAKE, None)
+
+    need = dcp.dcp_workspace_size(shape(), 24000, 6)
+    assert need > dcp.NOALLOC_SCRATCH_BYTES
+    assert call(shape(), 24000, 6) == dcp.DCP_ERR_WORKSPACE
+    msg = dcp.dcp_last_error()
+    assert "maximum" in msg and str(need) in msg
+    assert call(shape(n_tokens=0), 10, 1) == dcp.DCP_ERR_INVALID_ARGUMENT
+    assert call(shape(), 100, 0) == dcp.DCP_ERR_INVALID_ARGUMENT
+    assert call(shape(c_z=512), 10, 1) == dcp.DCP_ERR_UNSUPPORTED
+    # the workloads it is meant for fit: a 1024-token layer, a 3000-row stripe of 12000 tokens
+    assert dcp.dcp_workspace_size(shape(n_tokens=1024), 1024, 4) <= dcp.NOALLOC_SCRATCH_BYTES
+    assert dcp.dcp_workspace_size(shape(n_tokens=12000), 3000, 4) <= dcp.NOALLOC_SCRATCH_BYTES
