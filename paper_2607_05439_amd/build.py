@@ -5,7 +5,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SOURCES = ["dcp_api.hip", "fast.hip", "generic.hip", "merge.hip", "sparse.hip", "knn.hip", "transition.hip", "scatter.hip"]
+SOURCES = ["dcp_api.hip", "fast.hip", "proj.hip", "generic.hip", "merge.hip", "sparse.hip", "knn.hip", "transition.hip", "scatter.hip"]
 FLAGS = ["-O3", "--offload-arch=gfx950", "-fPIC", "-shared", "-std=c++17",
          # hipcc's host pass warns that it does not know this feature; harmless
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -1,9 +1,6 @@
 // Fused bf16 path for c_z = 128, H = 16, d = 24 on gfx950 (CDNA4).
 //
-// Three kernels:
-//   proj_kernel  q, k, v, g projections of the single track (MFMA, fp32 weights
-//                split into a bf16 hi+lo pair), written in the layouts the
-//                attention kernel's matrix-core operands want.
+// Two kernels (the q, k, v, g projections that feed them are in proj.hip):
 //   attn_kernel  the hot loop: one wave owns 16 query rows and one key range
 //                (a ring step of the paper's 2D scheme, or a slice of one). Per
 //                key it reads the 16 rows' pair vectors z[i, j, :] once from
@@ -131,139 +128,6 @@ __device__ __forceinline__ f32x4 bias_weight_sums(const bf16x8 (&whi)[4], const 
     r = mfma32(wlo[s], ones, r);
   }
   return r;
-}
-
-// ----------------------------------------------------------------------------- projections
-constexpr int kProjTiles = 4;  // 16-token tiles per projection wave (share the weight operands)
-
-// grid (groups of 4 tiles of 16 tokens, H, 4 projections {q, k, v, g}); one
-// wave each. Per 32-channel k-step the wave converts its head's weight rows to
-// bf16 hi + lo once and applies them to its 4 token tiles.
-__global__ void __launch_bounds__(64) proj_kernel(FastProjArgs a) {
-  const int lane = threadIdx.x, n = lane & 15, g = lane >> 4;
-  const int h = blockIdx.y, which = blockIdx.z;  // 0 q, 1 k, 2 v, 3 g
-  const bool is_query = (which == 0 || which == 3);
-  const int64_t limit = is_query ? a.nq_pad : a.n_pad;
-  const int64_t tile0 = (int64_t)blockIdx.x * kProjTiles;
-  if (tile0 * 16 >= limit) return;
-  const int64_t n_valid = is_query ? a.n_q : a.n_tok;
-  const int64_t base_tok = is_query ? a.q_row0 : 0;
-  const float* w = which == 0 ? a.w_q : which == 1 ? a.w_k : which == 2 ? a.w_v : a.w_g;
-  const bool swap_ab = (which == 2);  // v: accumulator [token][e]; others [e][token]
-
-  const uint16_t* srow[kProjTiles];
-#pragma unroll
-  for (int u = 0; u < kProjTiles; ++u) {
-    const int64_t my_tok = base_tok + min((tile0 + u) * 16 + n, n_valid - 1);  // padded rows are zeroed on output
-    srow[u] = a.s + my_tok * a.c_s + 8 * g;
-  }
-  f32x4 acc[kProjTiles][2];
-#pragma unroll
-  for (int u = 0; u < kProjTiles; ++u) acc[u][0] = acc[u][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int k0 = 0; k0 < a.c_s; k0 += 32) {
-    bf16x8 whi[2], wlo[2];
-#pragma unroll
-    for (int et = 0; et < 2; ++et) {
-      const int e = 16 * et + n;  // weight row e of head h (zero for e >= 24)
-      if (e < kD) {
-        const float4* wp = reinterpret_cast<const float4*>(w + (int64_t)(h * kD + e) * a.c_s + k0 + 8 * g);
-        const float4 x0 = wp[0], x1 = wp[1];
-        const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const __bf16 hv = (__bf16)xs[i];
-          whi[et][i] = hv;
-          wlo[et][i] = (__bf16)(xs[i] - (float)hv);
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) whi[et][i] = wlo[et][i] = (__bf16)0.0f;
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < kProjTiles; ++u) {
-      const bf16x8 sv = as_bf16x8(*reinterpret_cast<const u32x4*>(srow[u] + k0));
-#pragma unroll
-      for (int et = 0; et < 2; ++et) {
-        if (swap_ab) {
-          acc[u][et] = mfma32(sv, whi[et], acc[u][et]);
-          acc[u][et] = mfma32(sv, wlo[et], acc[u][et]);
-        } else {
-          acc[u][et] = mfma32(whi[et], sv, acc[u][et]);
-          acc[u][et] = mfma32(wlo[et], sv, acc[u][et]);
-        }
-      }
-    }
-  }
-
-#pragma unroll
-  for (int u = 0; u < kProjTiles; ++u) {
-    const int64_t tile = tile0 + u;
-    if (tile * 16 >= limit) break;
-    const int64_t t0 = tile * 16;
-    if (which == 2) {
-      // acc[u][et][i] = v[token t0 + 4g + i][e = 16 et + n]: exactly the V^T tile
-      // operand (lane L, slot i) of rows e = 16 et + n, keys 4g + i.
-#pragma unroll
-      for (int et = 0; et < 2; ++et) {
-        const int e = 16 * et + n;
-        bf16x4 o;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int64_t tok = t0 + 4 * g + i;
-          const bool valid = tok < a.n_tok && (a.mask == nullptr || a.mask[tok] != 0);
-          float val = valid ? acc[u][et][i] : 0.0f;
-          if (e == kD) val = valid ? 1.0f : 0.0f;  // row of ones: the softmax denominator
-          o[i] = (__bf16)val;
-        }
-        u32x2* dst = reinterpret_cast<u32x2*>(a.vt) + ((((int64_t)h * (a.n_pad / 16) + tile) * 64 + lane) * 2 + et);
-        *dst = __builtin_bit_cast(u32x2, o);
-      }
-      continue;
-    }
-    // acc[u][et][i] = proj[e = 16 et + 4g + i][token t0 + n]
-    const int64_t tok = t0 + n;
-    if (which == 3) {
-      if (tok >= a.n_q) continue;
-#pragma unroll
-      for (int et = 0; et < 2; ++et) {
-        const int e0 = 16 * et + 4 * g;
-        if (e0 >= kD) continue;
-        float4 o;
-        o.x = 1.0f / (1.0f + __expf(-acc[u][et][0]));
-        o.y = 1.0f / (1.0f + __expf(-acc[u][et][1]));
-        o.z = 1.0f / (1.0f + __expf(-acc[u][et][2]));
-        o.w = 1.0f / (1.0f + __expf(-acc[u][et][3]));
-        *reinterpret_cast<float4*>(a.g + tok * (kH * kD) + h * kD + e0) = o;
-      }
-      continue;
-    }
-    if (which == 1 && h == 0) {
-      // per-tile key mask: bit i = token t0 + i exists and attends
-      const bool kv_valid = tok < a.n_tok && (a.mask == nullptr || a.mask[tok] != 0);
-      const uint32_t bits = (uint32_t)(__ballot(kv_valid) & 0xFFFFull);
-      if (lane == 0) a.tile_valid[tile] = bits;
-    }
-    bool valid;
-    float scale;
-    uint16_t* dst;
-    if (which == 0) {
-      valid = tok < a.n_q;
-      scale = kLog2e * 0.20412414523193150818f;  // log2(e) / sqrt(24)
-      dst = a.q + ((int64_t)h * a.nq_pad + tok) * kDp;
-    } else {
-      valid = tok < a.n_tok && (a.mask == nullptr || a.mask[tok] != 0);
-      scale = 1.0f;
-      dst = a.k + ((int64_t)h * a.n_pad + tok) * kDp;
-    }
-#pragma unroll
-    for (int et = 0; et < 2; ++et) {
-      bf16x4 o;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) o[i] = (__bf16)(valid ? acc[u][et][i] * scale : 0.0f);  // rows >= 24 are 0
-      *reinterpret_cast<u32x2*>(dst + 16 * et + 4 * g) = __builtin_bit_cast(u32x2, o);
-    }
-  }
 }
 
 // ----------------------------------------------------------------------------- attention
@@ -538,13 +402,6 @@ __global__ void __launch_bounds__(64) bias_kernel(FastBiasArgs a) {
 }
 
 }  // namespace
-
-hipError_t launch_fast_proj(const FastProjArgs& a, hipStream_t st) {
-  const int64_t tiles = (a.n_pad > a.nq_pad ? a.n_pad : a.nq_pad) / 16;
-  hipLaunchKernelGGL(proj_kernel, dim3((unsigned)((tiles + kProjTiles - 1) / kProjTiles), kH, 4), dim3(64), 0, st,
-                     a);
-  return hipGetLastError();
-}
 
 hipError_t launch_fast_attn(const FastAttnArgs& a, hipStream_t st) {
   const int64_t n_qt = a.nq_pad / kTileQ;

@@ -14,7 +14,11 @@
 // 8 waves; tiles are visited starting at the one that holds the queries
 // themselves when they are candidates (their sequence neighbours are close in
 // space, which makes the thresholds tight early; the result does not depend on
-// the order). A lane takes one candidate per 64-candidate step and tests it
+// the order). Per tile, the bounding box of every 128 candidates is formed in
+// LDS, and a wave skips the candidates of a box whose distance (computed in
+// the definition's rounded operations, which bound every member's distance
+// from below) exceeds the current k-th distance of all 4 of its queries: an
+// exact exclusion, not a heuristic. A lane takes one candidate per 64-candidate step and tests it
 // against the 4 queries with a cheap conservative bound (|c|^2 - 2 c.q by
 // three multiply-adds, |c|^2 staged with the tile, against a per-query limit
 // derived from the current k-th distance with a proven rounding margin): no
@@ -204,6 +208,7 @@ template <int KS, int MODE>
 __global__ void __launch_bounds__(64 * kKnnWaves) __attribute__((amdgpu_waves_per_eu(KS == 2 ? 6 : 1))) knn_kernel(KnnArgs a) {
   __shared__ float4 s_c[kTile];  // x, y, z, then |c|^2 (MODE 0) or the group bits
   __shared__ uint64_t s_buf[kKnnWaves][kKnnQ][64];
+  __shared__ float4 s_box[kTile / 128][2];  // bounding box (low, high corner) of each 128-candidate step
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -248,6 +253,88 @@ __global__ void __launch_bounds__(64 * kKnnWaves) __attribute__((amdgpu_waves_pe
       s_c[i] = v;
     }
     __syncthreads();
+    // Bounding box of each 128-candidate step: wave w takes steps 2w and
+    // 2w + 1, lane l step 2w + l / 32 and its candidates l % 32 + 32 m.
+    // Padding entries (NaN x) drop out of the minima and maxima.
+    {
+      const int st = 2 * wave + (lane >> 5);
+      float lx = __builtin_inff(), ly = lx, lz = lx, hx = -lx, hy = -lx, hz = -lx;
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const float4 c = s_c[128 * st + (lane & 31) + 32 * m];
+        lx = fminf(lx, c.x); ly = fminf(ly, c.y); lz = fminf(lz, c.z);
+        hx = fmaxf(hx, c.x); hy = fmaxf(hy, c.y); hz = fmaxf(hz, c.z);
+      }
+      lx = fminf(lx, __uint_as_float(xor_lane<1>(__float_as_uint(lx))));
+      lx = fminf(lx, __uint_as_float(xor_lane<2>(__float_as_uint(lx))));
+      lx = fminf(lx, __uint_as_float(xor_lane<4>(__float_as_uint(lx))));
+      lx = fminf(lx, __uint_as_float(xor_lane<8>(__float_as_uint(lx))));
+      lx = fminf(lx, __uint_as_float(xor_lane<16>(__float_as_uint(lx))));
+      ly = fminf(ly, __uint_as_float(xor_lane<1>(__float_as_uint(ly))));
+      ly = fminf(ly, __uint_as_float(xor_lane<2>(__float_as_uint(ly))));
+      ly = fminf(ly, __uint_as_float(xor_lane<4>(__float_as_uint(ly))));
+      ly = fminf(ly, __uint_as_float(xor_lane<8>(__float_as_uint(ly))));
+      ly = fminf(ly, __uint_as_float(xor_lane<16>(__float_as_uint(ly))));
+      lz = fminf(lz, __uint_as_float(xor_lane<1>(__float_as_uint(lz))));
+      lz = fminf(lz, __uint_as_float(xor_lane<2>(__float_as_uint(lz))));
+      lz = fminf(lz, __uint_as_float(xor_lane<4>(__float_as_uint(lz))));
+      lz = fminf(lz, __uint_as_float(xor_lane<8>(__float_as_uint(lz))));
+      lz = fminf(lz, __uint_as_float(xor_lane<16>(__float_as_uint(lz))));
+      hx = fmaxf(hx, __uint_as_float(xor_lane<1>(__float_as_uint(hx))));
+      hx = fmaxf(hx, __uint_as_float(xor_lane<2>(__float_as_uint(hx))));
+      hx = fmaxf(hx, __uint_as_float(xor_lane<4>(__float_as_uint(hx))));
+      hx = fmaxf(hx, __uint_as_float(xor_lane<8>(__float_as_uint(hx))));
+      hx = fmaxf(hx, __uint_as_float(xor_lane<16>(__float_as_uint(hx))));
+      hy = fmaxf(hy, __uint_as_float(xor_lane<1>(__float_as_uint(hy))));
+      hy = fmaxf(hy, __uint_as_float(xor_lane<2>(__float_as_uint(hy))));
+      hy = fmaxf(hy, __uint_as_float(xor_lane<4>(__float_as_uint(hy))));
+      hy = fmaxf(hy, __uint_as_float(xor_lane<8>(__float_as_uint(hy))));
+      hy = fmaxf(hy, __uint_as_float(xor_lane<16>(__float_as_uint(hy))));
+      hz = fmaxf(hz, __uint_as_float(xor_lane<1>(__float_as_uint(hz))));
+      hz = fmaxf(hz, __uint_as_float(xor_lane<2>(__float_as_uint(hz))));
+      hz = fmaxf(hz, __uint_as_float(xor_lane<4>(__float_as_uint(hz))));
+      hz = fmaxf(hz, __uint_as_float(xor_lane<8>(__float_as_uint(hz))));
+      hz = fmaxf(hz, __uint_as_float(xor_lane<16>(__float_as_uint(hz))));
+      if ((lane & 31) == 0) {
+        s_box[st][0] = make_float4(lx, ly, lz, 0.f);
+        s_box[st][1] = make_float4(hx, hy, hz, 0.f);
+      }
+    }
+    __syncthreads();
+    // Steps no candidate of which can enter any of the wave's 4 top-k lists:
+    // lane l tests step l % 16 against query l / 16. For a candidate c in the
+    // box, |x_q - x_c| >= the box distance bx per axis, and the definition's
+    // rounded operations are monotone, so with bx, by, bz computed as rounded
+    // differences and d = ((bx*bx) + (by*by)) + (bz*bz) in the definition's
+    // order, the candidate's distance is at least d. A candidate enters only
+    // with distance <= the current k-th distance T, so d > T excludes the
+    // whole step. (T only decreases, so the test stays valid for the tile; with
+    // fewer than k entries T is NaN and nothing is excluded; an all-padding
+    // step has a NaN box and is not excluded.)
+    uint32_t skip;
+    {
+      const int st = lane & 15, jq = lane >> 4;
+      const float4 lo = s_box[st][0], hi = s_box[st][1];
+      float qx = q[0].x, qy = q[0].y, qz = q[0].z, T = __uint_as_float((uint32_t)(q[0].tau >> 32));
+#pragma unroll
+      for (int j = 1; j < kKnnQ; ++j)
+        if (jq == j) {
+          qx = q[j].x;
+          qy = q[j].y;
+          qz = q[j].z;
+          T = __uint_as_float((uint32_t)(q[j].tau >> 32));
+        }
+      float d;
+      {
+#pragma clang fp contract(off)
+        const float bx = fmaxf(fmaxf(lo.x - qx, qx - hi.x), 0.0f);
+        const float by = fmaxf(fmaxf(lo.y - qy, qy - hi.y), 0.0f);
+        const float bz = fmaxf(fmaxf(lo.z - qz, qz - hi.z), 0.0f);
+        d = (bx * bx + by * by) + bz * bz;
+      }
+      const uint64_t far = __ballot(d > T);
+      skip = (uint32_t)(far & (far >> 16) & (far >> 32) & (far >> 48) & 0xFFFFull);
+    }
     const uint32_t index0 = (uint32_t)(a.c_index0 + c0);
     // two steps of 64 candidates at a time; entries past n_here are padding
     // (NaN distance) that the exact test rejects. In the tile that holds the
@@ -260,6 +347,7 @@ __global__ void __launch_bounds__(64 * kKnnWaves) __attribute__((amdgpu_waves_pe
       if (self >= 0 && self < n_here) pr = max(0, (int)(self >> 7) - 1);
     }
     for (int t = 0; t < n_pairs; ++t, pr = pr + 1 == n_pairs ? 0 : pr + 1) {
+      if ((skip >> pr) & 1u) continue;
       const int s = pr << 7;
       const float4 ca = s_c[s + lane], cb = s_c[s + 64 + lane];
       const float cca = MODE ? norm2(ca) : ca.w, ccb = MODE ? norm2(cb) : cb.w;

@@ -149,6 +149,10 @@ __global__ void __launch_bounds__(64 * kWaves) trans_kernel(TransArgs a) {
     // LayerNorm of the staged z (two passes over the pair's 128 channels: 32
     // per lane, 4 lanes), then gamma and beta (from global memory: small and
     // cached)
+    // The output accumulators start at z itself (the residual): accumulator
+    // (ct = 2 ks + s, register i) is channel 32 ks + 8g + 4s + i, element
+    // 4s + i of the lane's staged chunk ks, so z never has to be read again.
+    f32x4 acc[8][2];  // out^T: output tile ct, pair tile p
     bf16x8 nv[2][4];
     {
       float x[2][4][8], rstd[2];
@@ -162,6 +166,7 @@ __global__ void __launch_bounds__(64 * kWaves) trans_kernel(TransArgs a) {
           for (int i = 0; i < 8; ++i) {
             const uint32_t w = zz[i >> 1];
             x[p][ks][i] = __uint_as_float((i & 1) ? (w & 0xFFFF0000u) : (w << 16));
+            acc[2 * ks + (i >> 2)][p][i & 3] = x[p][ks][i];
             s += x[p][ks][i];
           }
         }
@@ -192,11 +197,6 @@ __global__ void __launch_bounds__(64 * kWaves) trans_kernel(TransArgs a) {
       }
     }
     const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
-    f32x4 acc[8][2];  // out^T: output tile ct, pair tile p
-#pragma unroll
-    for (int ct = 0; ct < 8; ++ct)
-#pragma unroll
-      for (int p = 0; p < 2; ++p) acc[ct][p] = zero;
 
     bf16x8 hv[2];
     // h' = A' B / (1 + 2^A') of one tile pair, as the B operand over its 32
@@ -209,18 +209,6 @@ __global__ void __launch_bounds__(64 * kWaves) trans_kernel(TransArgs a) {
           const float x = ha[j >> 2][p][j & 3];
           hv[p][j] = (__bf16)(x * hb[j >> 2][p][j & 3] * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x)));
         }
-    };
-    // the residual's z: global memory again (recently staged, so mostly from
-    // L2), issued in the last chunk once the normalised z is dead
-    u32x4 zres[2][4];
-    auto load_zres = [&]() {
-#pragma unroll
-      for (int p = 0; p < 2; ++p) {
-        const int64_t pr = min(pair0 + 16 * p + n, a.n_pairs - 1);
-        const u32x4* src = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.z_in) + pr * kCz + 8 * g);
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) zres[p][ks] = src[4 * ks];
-      }
     };
     const bool stage_next = !last_group;
     const __amdgpu_buffer_rsrc_t znext = z_rsrc(stage_next ? grp + gridDim.x : grp);
@@ -273,10 +261,7 @@ __global__ void __launch_bounds__(64 * kWaves) trans_kernel(TransArgs a) {
 #pragma unroll
           for (int p = 0; p < 2; ++p) h[m][tt][p] = mfma32(w, nv[p][ks], ks == 0 ? zero : h[m][tt][p]);
         } else {
-          if (r == 16) {
-            silu(h[0], h[1]);
-            if (c == kChunks - 1 && f == 40) load_zres();  // the residual's z, once the normalised z is dead
-          }
+          if (r == 16) silu(h[0], h[1]);
           // out^T += W3'' h'^T
 #pragma unroll
           for (int p = 0; p < 2; ++p) acc[r - 16][p] = mfma32(w, hv[p], acc[r - 16][p]);
@@ -287,24 +272,47 @@ __global__ void __launch_bounds__(64 * kWaves) trans_kernel(TransArgs a) {
       }
       ++seq;
     }
-    // residual and store: accumulator (ct = 2 ks + s, register i) is channel
-    // 32 ks + 8g + 4s + i, element 4s + i of the lane's loaded chunk ks
+    // store. Accumulator (ct = 2 ks + s, register i) is channel 32 ks + 8g +
+    // 4s + i of pair 16p + n: lane (n, g) holds bytes 64 ks + 16 g .. +15 of
+    // the pair's 256-byte row for each ks. Those are regrouped across lanes so
+    // that each store instruction writes 8 pairs x one whole 128-byte line
+    // (lane L: pair 8 half + L / 8, bytes 128 line + 16 (L % 8)); half lines
+    // written by separate streaming stores were each sent to memory on their own.
+    {
+      uint32_t o[2][4][4];  // [pair tile][ks][dword]: bf16 pairs of the lane's chunk
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
-      const int64_t pr = pair0 + 16 * p + n;
-      if (pr >= a.n_pairs) continue;
-      u32x4* dst = reinterpret_cast<u32x4*>(static_cast<uint16_t*>(a.z_out) + pr * kCz + 8 * g);
+      for (int p = 0; p < 2; ++p)
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        bf16x8 o;
+        for (int ks = 0; ks < 4; ++ks) {
+          bf16x8 v;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const uint32_t w = zres[p][ks][e >> 1];
-          const float zin = __uint_as_float((e & 1) ? (w & 0xFFFF0000u) : (w << 16));
-          o[e] = (__bf16)(zin + acc[2 * ks + (e >> 2)][p][e & 3]);
+          for (int e = 0; e < 8; ++e) v[e] = (__bf16)acc[2 * ks + (e >> 2)][p][e & 3];  // z + W3'' h'
+          const u32x4 w = __builtin_bit_cast(u32x4, v);
+#pragma unroll
+          for (int d = 0; d < 4; ++d) o[p][ks][d] = w[d];
         }
-        __builtin_nontemporal_store(__builtin_bit_cast(u32x4, o), dst + 4 * ks);
-      }
+      const bool upper = (lane & 4) != 0;  // chunk L % 8 >= 4: the second 64 bytes of the line
+#pragma unroll
+      for (int p = 0; p < 2; ++p)
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const int src = 8 * half + (lane >> 3) + 16 * (lane & 3);  // lane (n, g) holding the bytes
+#pragma unroll
+          for (int line = 0; line < 2; ++line) {
+            u32x4 v;
+#pragma unroll
+            for (int d = 0; d < 4; ++d) {
+              const uint32_t lo = (uint32_t)__builtin_amdgcn_ds_bpermute(4 * src, (int)o[p][2 * line][d]);
+              const uint32_t hi = (uint32_t)__builtin_amdgcn_ds_bpermute(4 * src, (int)o[p][2 * line + 1][d]);
+              v[d] = upper ? hi : lo;
+            }
+            const int64_t pr = pair0 + 16 * p + 8 * half + (lane >> 3);
+            if (pr < a.n_pairs) {
+              u32x4* dst = reinterpret_cast<u32x4*>(static_cast<uint16_t*>(a.z_out) + pr * kCz) + 8 * line + (lane & 7);
+              __builtin_nontemporal_store(v, dst);
+            }
+          }
+        }
     }
   }
   wait_vm<0>();
