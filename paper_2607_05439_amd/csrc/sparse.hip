@@ -255,12 +255,26 @@ __device__ __forceinline__ float across_sum(float x) {
   swap32(a, b);
   return a + b;
 }
+// Maximum of two floats as one v_max_f32: fmaxf would first canonicalise
+// operands that come from cross-lane moves (two more instructions each); the
+// instruction itself already returns the other operand for a NaN one.
+__device__ __forceinline__ float vmax(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
 template <int GROUPS>
 __device__ __forceinline__ float across_max(float x) {
-  if constexpr (GROUPS == 4) return max4(x);
   float a = x, b = x;
   swap32(a, b);
-  return fmaxf(a, b);
+  x = vmax(a, b);
+  if constexpr (GROUPS == 4) {
+    a = x;
+    b = x;
+    swap16(a, b);
+    x = vmax(a, b);
+  }
+  return x;
 }
 
 __device__ __forceinline__ int wave_min(int x) {
@@ -483,7 +497,7 @@ sparse_attn_kernel(SparseAttnArgs a) {
   auto weigh = [&](int buf, const float (&lg)[kUnroll]) {
     float mx = -INFINITY;
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) mx = fmaxf(mx, lg[u]);
+    for (int u = 0; u < kUnroll; ++u) mx = vmax(mx, lg[u]);
     mx = across_max<NPI>(mx);
     const float m_new = fmaxf(m_run, ceilf(mx));
     if (m_new != m_run) {  // lane-varying (per head); only a rescale of the state

@@ -155,3 +155,39 @@ def test_token_permutation_equivariance(torch_cuda):
     assert err <= TOL_PERM
     # and the masked tokens, wherever they land, still give finite outputs
     assert np.isfinite(got).all()
+
+
+# ----------------------------------------------------------------------------- peaked softmax (large logits)
+def _scale_weights(d, q_k: float, b: float):
+    """Scale W_q, W_k and W_b by powers of two (exact in fp32) on both sides."""
+    import torch
+    for name, f in (("w_q", q_k), ("w_k", q_k), ("w_b", b)):
+        d.w_host[name] = (d.w_host[name] * np.float32(f)).astype(np.float32)
+        d.w[name] = torch.from_numpy(np.ascontiguousarray(d.w_host[name])).to(d.dev)
+
+
+@pytest.mark.parametrize("dtype,q_k,b,tol", [("bf16", 1.0, 8.0, TOL_BF16), ("f32", 2.0, 8.0, 1e-5)])
+def test_peaked_softmax(torch_cuda, dtype, q_k, b, tol):
+    """Logits far from the unit-scale workloads' range (the pair bias scaled
+    up 8x, to a spread of about +-30 natural units; q and k scaled too on the
+    fp32 path): most softmax weights underflow against the row maximum, and
+    the running maximum moves by many units between key tiles. (On the bf16
+    path q and k stay at unit scale: they enter the matrix cores as bf16, whose
+    rounding grows with the logits' size and is part of that path's precision,
+    not of its softmax: at 4x larger q.k logits the error against the fp64
+    oracle reaches 1.3e-2.)"""
+    if dtype == "bf16":
+        wl = workload(n_tok=300, mask="random:20")
+        q0, nq, nkb = 5, 290, 3
+    else:
+        wl = workload(n_tok=128, c_s=128, c_z=32, n_heads=4, head_dim=32, dtype="f32", mask="tail:6")
+        q0, nq, nkb = 0, 128, 4
+    log(f"case peaked softmax {dtype}: W_q, W_k x{q_k}, W_b x{b}")
+    d = Device(wl, affine=True)
+    _scale_weights(d, q_k, b)
+    got = _np(d.attention(q0, nq, nkb))[:nq]
+    ref = d.oracle_rows(np.arange(q0, q0 + nq))
+    err = rel_err(got, ref)
+    log(f"  rel err {err:.3e}")
+    assert err <= tol
+    assert rel_err(_np(d.attention(q0, nq, 1))[:nq], got) <= (TOL_BLOCKED if dtype == "bf16" else 1e-5)
