@@ -111,7 +111,7 @@ struct Layout {
   Path path;
   int n_seg, n_parts;
   int64_t nq_pad, n_pad;
-  size_t off_q, off_k, off_v, off_tv, off_g, off_m, off_l, off_acc, total;
+  size_t off_q, off_k, off_v, off_tv, off_ws, off_g, off_m, off_l, off_acc, total;
 };
 
 void make_layout(const dcp_shape* sh, Path path, int64_t n_q, int32_t n_kb, Layout* L) {
@@ -132,6 +132,7 @@ void make_layout(const dcp_shape* sh, Path path, int64_t n_q, int32_t n_kb, Layo
     L->off_k = take((size_t)dcp::kFastH * L->n_pad * dcp::kFastDp * 2);
     L->off_v = take((size_t)dcp::kFastH * L->n_pad * dcp::kFastDp * 2);
     L->off_tv = take((size_t)(L->n_pad / 16) * 4);
+    L->off_ws = take(dcp::fast_proj_split_bytes(sh->c_s));
   } else {
     L->n_seg = 1;
     L->n_parts = n_kb;
@@ -141,6 +142,7 @@ void make_layout(const dcp_shape* sh, Path path, int64_t n_q, int32_t n_kb, Layo
     L->off_k = take((size_t)sh->n_tokens * hd * 4);
     L->off_v = take((size_t)sh->n_tokens * hd * 4);
     L->off_tv = 0;
+    L->off_ws = 0;
   }
   L->off_g = take((size_t)n_q * hd * 4);
   L->off_m = take((size_t)L->n_parts * sh->n_heads * n_q * 4);
@@ -232,6 +234,7 @@ static int run_attention(const dcp_shape* shape, const dcp_weights* w, const voi
     pa.vt = reinterpret_cast<uint16_t*>(ws + L.off_v);
     pa.g = reinterpret_cast<float*>(ws + L.off_g);
     pa.tile_valid = reinterpret_cast<uint32_t*>(ws + L.off_tv);
+    pa.w_split = ws + L.off_ws;
     if ((e = dcp::launch_fast_proj(pa, st)) != hipSuccess)
       return fail(DCP_ERR_HIP, "projection launch failed: %s", hipGetErrorString(e));
     dcp::FastAttnArgs aa{};

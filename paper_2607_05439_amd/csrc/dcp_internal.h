@@ -62,6 +62,7 @@ struct FastProjArgs {
   uint16_t* vt;  // [H][n_pad/16][64][2][4] bf16: V^T tiles (lane, M-tile) with a row of ones at e = 24
   float* g;      // [n_q][H*d] fp32, sigmoid applied
   uint32_t* tile_valid;  // [n_pad/16]: bit i = key 16t+i exists and is not masked
+  void* w_split;         // fast_proj_split_bytes(c_s): the weights as bf16 hi + lo matrix-core operands
 };
 
 struct FastAttnArgs {
@@ -227,6 +228,7 @@ struct ScatterArgs {
   int64_t* plan;          // [n_tokens][2] first atom and one past the last of each token (workspace)
 };
 
+size_t fast_proj_split_bytes(int32_t c_s);
 hipError_t launch_fast_proj(const FastProjArgs& a, hipStream_t st);
 hipError_t launch_fast_attn(const FastAttnArgs& a, hipStream_t st);
 hipError_t launch_fast_bias(const FastBiasArgs& a, hipStream_t st);

@@ -9,11 +9,24 @@
 //   g  [n_q][H d] fp32, sigmoid applied
 //   tile_valid [n_pad / 16]: bit i = key 16 t + i exists and attends
 // Matrix-core operand layouts as in fast.hip (v_mfma_f32_16x16x32_bf16).
+//
+// Two kernels:
+//   proj_split_kernel  the four weight matrices, split into bf16 hi + lo and
+//                      laid out as matrix-core operands: for projection p,
+//                      16-output tile j (rows 16 j .. 16 j + 15 of W_p, which
+//                      are the outputs h d + e in order) and k-step s
+//                      (channels 32 s .. 32 s + 31), 1 KB of hi then 1 KB of
+//                      lo, lane L holding row 16 j + L % 16, channels
+//                      32 s + 8 (L / 16) .. + 7. A wave's weight load is then
+//                      1 KB of consecutive bytes, where rows of W read in
+//                      place give 16 half cache lines per load.
+//   proj_kernel        the products. The 384 outputs of a projection are 24
+//                      tiles of 16 with no padding (a tile may hold the end
+//                      of one head and the start of the next); each wave
+//                      takes two tiles over 128 tokens.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
-
-#include <type_traits>
 
 #include "cdna4.h"
 #include "dcp_internal.h"
@@ -22,203 +35,202 @@ namespace dcp {
 namespace {
 
 constexpr int kH = kFastH, kD = kFastD, kDp = kFastDp;
+constexpr int kHD = kH * kD;         // 384 outputs per projection
+constexpr int kOutTiles = kHD / 16;  // 24 output tiles per projection
 constexpr float kLog2e = 1.44269504088896340736f;
 
-// ----------------------------------------------------------------------------- projections
-constexpr int kProjTiles = 8;                   // 16-token tiles per workgroup (128 tokens)
-constexpr int kProjWaves = 8;                   // waves per workgroup, one head each
-constexpr int kProjHalves = kH / kProjWaves;    // workgroups per (token group, projection)
-constexpr int kProjChunk = 64;                  // s channels staged in LDS at a time (2 k-steps)
-constexpr int kProjRowChunks = kProjChunk / 8;  // 16-byte chunks per staged row
-constexpr int kProjStage = kProjTiles * 16 * kProjRowChunks / (64 * kProjWaves);  // loads per thread
+constexpr int kProjTiles = 8;                                   // 16-token tiles per workgroup (128 tokens)
+constexpr int kProjWaves = 8;                                   // waves per workgroup, two output tiles each
+constexpr int kProjSideWgs = 2 * kOutTiles / (2 * kProjWaves);  // workgroups per token group and side (3)
+constexpr int kProjChunk = 64;                                  // s channels staged in LDS at a time (2 k-steps)
+constexpr int kProjRowChunks = kProjChunk / 8;                  // 16-byte chunks per staged row
+constexpr int kProjStage = kProjTiles * 16 * kProjRowChunks / (64 * kProjWaves);  // LDS copies per wave per chunk
 
-// One workgroup = 128 tokens x one projection {q, k, v, g} x 8 heads; wave w
-// computes head 8 * half + w. The group's s rows are staged in LDS, 64
-// channels at a time and double-buffered, so each s row is read from memory
-// once per workgroup; every wave then reads its matrix-core operands from
-// LDS (16-byte chunks of a row XOR-swizzled by row / 2, so the 16 rows of one
-// operand read cover all banks once). Per 32-channel k-step a wave converts
-// its head's fp32 weight rows to bf16 hi + lo (loaded one k-step ahead) and
-// applies them to the 8 tiles: 32 products per weight load. Workgroups are
-// numbered so that the 8 workgroups of a token group (4 projections x 2 head
-// halves) run on the same XCD (dispatch gives workgroup i to XCD i % 8), which
-// then fetches the group's s rows once into its L2.
+// byte offset of the split weights of projection p, output tile j, k-step s
+__device__ __forceinline__ int split_offset(int p, int j, int s, int n_ks) {
+  return ((p * kOutTiles + j) * n_ks + s) * 2048;
+}
+
+// One thread per (projection, output tile, k-step, lane): 8 weights, 32 bytes
+// in, 16 bytes of hi and 16 of lo out.
+__global__ void __launch_bounds__(256) proj_split_kernel(FastProjArgs a) {
+  const int n_ks = a.c_s / 32;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)4 * kOutTiles * n_ks * 64) return;
+  const int lane = (int)(t & 63), n = lane & 15, g = lane >> 4;
+  const int s = (int)((t >> 6) % n_ks);
+  const int j = (int)((t >> 6) / n_ks % kOutTiles);
+  const int p = (int)((t >> 6) / n_ks / kOutTiles);
+  const float* w = p == 0 ? a.w_q : p == 1 ? a.w_k : p == 2 ? a.w_v : a.w_g;
+  const float4* src = reinterpret_cast<const float4*>(w + (int64_t)(16 * j + n) * a.c_s + 32 * s + 8 * g);
+  const float4 w0 = src[0], w1 = src[1];
+  const float xs[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+  bf16x8 hi, lo;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const __bf16 hv = (__bf16)xs[i];
+    hi[i] = hv;
+    lo[i] = (__bf16)(xs[i] - (float)hv);
+  }
+  char* dst = reinterpret_cast<char*>(a.w_split) + split_offset(p, j, s, n_ks) + 16 * lane;
+  *reinterpret_cast<bf16x8*>(dst) = hi;
+  *reinterpret_cast<bf16x8*>(dst + 1024) = lo;
+}
+
+// One workgroup = 128 tokens x one side (query: q and g of the stripe's rows;
+// key: k and v of all tokens) x 16 of the side's 48 output tiles; wave w of
+// workgroup b takes tiles 2 (8 b + w) and the next, of the side's first
+// projection for 8 b + w < 12, else its second. The group's s rows are staged
+// in LDS, 64 channels at a time and double-buffered, so each s row is read
+// from memory once per workgroup; every wave then reads its matrix-core
+// operands from LDS (16-byte chunks of a row XOR-swizzled by row / 2, so the
+// 16 rows of one operand read cover all banks once). Per 32-channel k-step a
+// wave loads its two tiles' split weights (one k-step ahead) and applies them
+// to the 8 token tiles: 32 products per 4 KB of weights. The three workgroups
+// of a (side, token group) run on the same XCD (dispatch gives workgroup i to
+// XCD i % 8), which then fetches the group's s rows once into its L2. Every
+// accumulator holds [output][token]; v's tiles are transposed at the end.
 __global__ void __launch_bounds__(64 * kProjWaves) __attribute__((amdgpu_waves_per_eu(4))) proj_kernel(FastProjArgs a) {
   __shared__ __attribute__((aligned(16))) u32x4 s_s[2][kProjTiles * 16][kProjRowChunks];  // 2 x 16 KB
   const int tid = threadIdx.x, lane = tid & 63, n = lane & 15, g = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
-  const int64_t grp = (int64_t)(slot / (4 * kProjHalves)) * 8 + xcd;
-  const int sub = slot % (4 * kProjHalves);
-  const int which = sub / kProjHalves;  // 0 q, 1 k, 2 v, 3 g
-  const int h = (sub % kProjHalves) * kProjWaves + wave;
-  const bool is_query = (which == 0 || which == 3);
+  const int64_t item = (int64_t)(slot / kProjSideWgs) * 8 + xcd;  // key groups first, then query groups
+  const int pair = (slot % kProjSideWgs) * kProjWaves + wave;     // 0..23 within the side
+  const int64_t key_groups = (a.n_pad / 16 + kProjTiles - 1) / kProjTiles;
+  const int64_t query_groups = (a.nq_pad / 16 + kProjTiles - 1) / kProjTiles;
+  if (item >= key_groups + query_groups) return;  // the whole workgroup, before any barrier
+  const bool is_query = item >= key_groups;
+  const int64_t grp = is_query ? item - key_groups : item;
+  const bool second = pair >= kOutTiles / 2;                          // g or v
+  const int which = is_query ? (second ? 3 : 0) : (second ? 2 : 1);  // 0 q, 1 k, 2 v, 3 g
+  const int j0 = 2 * (pair % (kOutTiles / 2));                        // first of the wave's two output tiles
   const int64_t limit = is_query ? a.nq_pad : a.n_pad;
-  const int64_t tile0 = grp * kProjTiles;
-  if (tile0 * 16 >= limit) return;  // the whole workgroup, before any barrier
   const int64_t n_valid = is_query ? a.n_q : a.n_tok;
   const int64_t base_tok = is_query ? a.q_row0 : 0;
-  const float* w = which == 0 ? a.w_q : which == 1 ? a.w_k : which == 2 ? a.w_v : a.w_g;
+  const int64_t tile0 = grp * kProjTiles;
 
-  // All loads are unconditional buffer loads; a load past the end of its
-  // buffer returns zeros and moves no data (the compiler then knows how many
-  // loads are in flight on every path and can wait for exactly the old ones).
-  // Staging: load m of thread t moves 16 bytes, item i = t + 512 m: row i / 8
-  // (rows past the valid tokens repeat the last one; their outputs are
-  // zeroed), chunk i % 8 of the 64 channels.
+  // Staging goes straight to LDS (16 bytes per lane): the workgroup's 16 KB
+  // per chunk are 16 blocks of 8 rows, block b copied by wave b % 8; lane i of
+  // a block fills row 8 b + i / 8, swizzled chunk i % 8, i.e. channel chunk
+  // (i % 8) ^ ((row >> 1) & 7) of the 64. Rows past the valid tokens repeat
+  // the last one (their outputs are zeroed); c_s is a multiple of 32, so a
+  // chunk's upper half past c_s repeats the last 8 channels, whose products
+  // with the zero weights there (out-of-range loads) add nothing.
   const int64_t rows_left = min(n_valid - tile0 * 16, (int64_t)(kProjTiles * 16));
   const __amdgpu_buffer_rsrc_t sres = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(a.s + (base_tok + tile0 * 16) * a.c_s), 0, (int)(rows_left * a.c_s * 2),
       kRawBufferFlags);
-  int st_off[kProjStage];
-#pragma unroll
-  for (int m = 0; m < kProjStage; ++m) {
-    const int i = tid + 64 * kProjWaves * m, row = i / kProjRowChunks, c = i % kProjRowChunks;
-    st_off[m] = (int)(min((int64_t)row, rows_left - 1) * a.c_s * 2) + 16 * c;
-  }
   const int n_chunks = (a.c_s + kProjChunk - 1) / kProjChunk;
-  auto stage_load = [&](int kc, u32x4 (&v)[kProjStage]) {
+  const int last_row = (int)rows_left - 1;
+  auto stage = [&](int kc, int buf) {
 #pragma unroll
     for (int m = 0; m < kProjStage; ++m) {
-      const int c = (tid + 64 * kProjWaves * m) % kProjRowChunks;
-      const bool in = kc * kProjChunk + 8 * c < a.c_s;
-      v[m] = __builtin_bit_cast(
-          u32x4, __builtin_amdgcn_raw_buffer_load_b128(sres, in ? st_off[m] + kc * kProjChunk * 2 : kOutOfRange, 0, 0));
-    }
-  };
-  auto stage_store = [&](int buf, const u32x4 (&v)[kProjStage]) {
-#pragma unroll
-    for (int m = 0; m < kProjStage; ++m) {
-      const int i = tid + 64 * kProjWaves * m, row = i / kProjRowChunks, c = i % kProjRowChunks;
-      s_s[buf][row][c ^ ((row >> 1) & 7)] = v[m];
+      const int row = 8 * (wave + kProjWaves * m) + lane / 8;
+      const int ch = min(kc * kProjChunk + 8 * ((lane % 8) ^ ((row >> 1) & 7)), a.c_s - 8);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          sres, (__attribute__((address_space(3))) void*)&s_s[buf][8 * (wave + kProjWaves * m)][0], 16,
+          (min(row, last_row) * a.c_s + ch) * 2, 0, 0, 0);
     }
   };
 
-  // weight rows e = 16 et + n of head h (zero for e >= 24), k-slots 8g .. 8g+7,
-  // one k-step ahead in two register buffers (k-step ks uses buffer ks & 1;
-  // a chunk holds an even number of k-steps, so the parity carries over)
-  float4 wbuf[2][2][2];
+  // the two tiles' split weights of a k-step: hi and lo of tile j0, then of
+  // tile j0 + 1, one k-step ahead in two register buffers (k-step ks of a
+  // chunk uses buffer ks & 1; a chunk holds an even number of k-steps, so the
+  // parity carries over). Loads past the last k-step read out of range: zeros.
+  const int n_ks = a.c_s / 32;
   const __amdgpu_buffer_rsrc_t wres =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(w), 0, kH * kD * a.c_s * 4, kRawBufferFlags);
-  auto load_w = [&](int k0, float4 (&dst)[2][2]) {
+      __builtin_amdgcn_make_buffer_rsrc(a.w_split, 0, split_offset(4, 0, 0, n_ks), kRawBufferFlags);
+  const int wbase = split_offset(which, j0, 0, n_ks) + 16 * lane;
+  u32x4 wbuf[2][4];
+  auto load_w = [&](int ks, u32x4 (&dst)[4]) {
 #pragma unroll
-    for (int et = 0; et < 2; ++et) {
-      const int e = 16 * et + n;
-      const int off = (e < kD && k0 < a.c_s) ? ((h * kD + e) * a.c_s + k0 + 8 * g) * 4 : kOutOfRange;
-      dst[et][0] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(wres, off, 0, 0));
-      dst[et][1] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(wres, off + 16, 0, 0));
-    }
+    for (int q = 0; q < 4; ++q)
+      dst[q] = __builtin_amdgcn_raw_buffer_load_b128(
+          wres, ks < n_ks ? wbase + (q >> 1) * n_ks * 2048 + ks * 2048 + (q & 1) * 1024 : kOutOfRange, 0, 0);
   };
 
   f32x4 acc[kProjTiles][2];
 #pragma unroll
   for (int u = 0; u < kProjTiles; ++u) acc[u][0] = acc[u][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // the product loop, instantiated per operand orientation (swap: v, whose
-  // accumulator is [token][e]; the others [e][token]) so the loop body has no
-  // branches
-  auto products = [&](auto swap_tag) {
-    constexpr bool kSwap = decltype(swap_tag)::value;
-    {
-      u32x4 first[kProjStage];
-      stage_load(0, first);
-      stage_store(0, first);
-    }
-    load_w(0, wbuf[0]);
-    for (int kc = 0; kc < n_chunks; ++kc) {
-      __syncthreads();  // chunk kc is in buffer kc & 1; nobody still reads the other buffer
-      const bool more = kc + 1 < n_chunks;
-      u32x4 nxt[kProjStage];
-      stage_load(more ? kc + 1 : kc, nxt);
-      // every chunk runs its 2 k-steps: channels past c_s are zeros on both
-      // sides (out-of-range loads), which add nothing
+  stage(0, 0);
+  load_w(0, wbuf[0]);
+  for (int kc = 0; kc < n_chunks; ++kc) {
+    // chunk kc is in buffer kc & 1 (the barrier waits for this wave's copies
+    // into it); nobody still reads the other buffer, which takes chunk kc + 1
+    __syncthreads();
+    if (kc + 1 < n_chunks) stage(kc + 1, (kc + 1) & 1);
 #pragma unroll
-      for (int ks = 0; ks < kProjChunk / 32; ++ks) {
-        const int k0 = kc * kProjChunk + 32 * ks;
-        bf16x8 whi[2], wlo[2];
+    for (int ks = 0; ks < kProjChunk / 32; ++ks) {
+      const bf16x8 whi0 = as_bf16x8(wbuf[ks & 1][0]), wlo0 = as_bf16x8(wbuf[ks & 1][1]);
+      const bf16x8 whi1 = as_bf16x8(wbuf[ks & 1][2]), wlo1 = as_bf16x8(wbuf[ks & 1][3]);
+      load_w(kc * (kProjChunk / 32) + ks + 1, wbuf[(ks + 1) & 1]);  // in flight during this k-step's products
+      __builtin_amdgcn_sched_barrier(0);  // (issued here, not sunk towards their use)
 #pragma unroll
-        for (int et = 0; et < 2; ++et) {
-          const float4 w0 = wbuf[ks & 1][et][0], w1 = wbuf[ks & 1][et][1];
-          const float xs[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-#pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            const __bf16 hv = (__bf16)xs[i];
-            whi[et][i] = hv;
-            wlo[et][i] = (__bf16)(xs[i] - (float)hv);
-          }
-        }
-        load_w(k0 + 32, wbuf[(ks + 1) & 1]);  // the next k-step, in flight during this one's products
-        __builtin_amdgcn_sched_barrier(0);     // (issued here, not sunk towards their use)
-#pragma unroll
-        for (int u = 0; u < kProjTiles; ++u) {
-          const int row = 16 * u + n;
-          const bf16x8 sv = as_bf16x8(s_s[kc & 1][row][(4 * ks + g) ^ ((row >> 1) & 7)]);
-#pragma unroll
-          for (int et = 0; et < 2; ++et) {
-            if constexpr (kSwap) {
-              acc[u][et] = mfma32(sv, whi[et], acc[u][et]);
-              acc[u][et] = mfma32(sv, wlo[et], acc[u][et]);
-            } else {
-              acc[u][et] = mfma32(whi[et], sv, acc[u][et]);
-              acc[u][et] = mfma32(wlo[et], sv, acc[u][et]);
-            }
-          }
-        }
-        // keep the next k-step's conversion (which waits for its loads) after
-        // this k-step's products
-        __builtin_amdgcn_sched_barrier(0);
+      for (int u = 0; u < kProjTiles; ++u) {
+        const int row = 16 * u + n;
+        const bf16x8 sv = as_bf16x8(s_s[kc & 1][row][(4 * ks + g) ^ ((row >> 1) & 7)]);
+        acc[u][0] = mfma32(whi0, sv, acc[u][0]);
+        acc[u][1] = mfma32(whi1, sv, acc[u][1]);
+        acc[u][0] = mfma32(wlo0, sv, acc[u][0]);
+        acc[u][1] = mfma32(wlo1, sv, acc[u][1]);
       }
-      if (more) stage_store((kc + 1) & 1, nxt);
+      // keep the next k-step's weight use (which waits for its loads) after
+      // this k-step's products
+      __builtin_amdgcn_sched_barrier(0);
     }
-  };
-  if (which == 2)
-    products(std::integral_constant<bool, true>{});
-  else
-    products(std::integral_constant<bool, false>{});
+  }
 
-  {
 #pragma unroll
-    for (int u = 0; u < kProjTiles; ++u) {
-      const int64_t tile = tile0 + u;
-      if (tile * 16 >= limit) break;
-      const int64_t t0 = tile * 16;
+  for (int u = 0; u < kProjTiles; ++u) {
+    const int64_t tile = tile0 + u;
+    if (tile * 16 >= limit) break;
+    const int64_t t0 = tile * 16;
+#pragma unroll
+    for (int jt = 0; jt < 2; ++jt) {
+      const int j = j0 + jt;
       if (which == 2) {
-        // acc[u][et][i] = v[token t0 + 4g + i][e = 16 et + n]: exactly the
-        // V^T tile operand (lane L, slot i) of rows e = 16 et + n, keys 4g + i.
+        // transposed through the matrix cores: the accumulator's registers as
+        // an A operand of the k = 16 product hold the tile's transpose, and
+        // times the identity that lands in the accumulator layout (exact: the
+        // bf16 values times 1). Then vt[i] = v[token t0 + 4g + i][output
+        // 16 j + n]: for its head h and e = output % 24, the V^T operand item
+        // (lane 16 g + e % 16, M-tile e / 16) of keys 4g .. 4g + 3. Rows
+        // e >= 16 also write row e + 8: the ones row (e + 8 = 24) or a zero row.
+        bf16x4 av, id;
 #pragma unroll
-        for (int et = 0; et < 2; ++et) {
-          const int e = 16 * et + n;
-          bf16x4 o;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int64_t tok = t0 + 4 * g + i;
-            const bool valid = tok < a.n_tok && (a.mask == nullptr || a.mask[tok] != 0);
-            float val = valid ? acc[u][et][i] : 0.0f;
-            if (e == kD) val = valid ? 1.0f : 0.0f;  // row of ones: the softmax denominator
-            o[i] = (__bf16)val;
-          }
-          u32x2* dst = reinterpret_cast<u32x2*>(a.vt) + ((((int64_t)h * (a.n_pad / 16) + tile) * 64 + lane) * 2 + et);
-          *dst = __builtin_bit_cast(u32x2, o);
+        for (int i = 0; i < 4; ++i) {
+          av[i] = (__bf16)acc[u][jt][i];
+          id[i] = (__bf16)(4 * g + i == n ? 1.0f : 0.0f);
         }
+        const f32x4 vt = mfma16(av, id, f32x4{0.f, 0.f, 0.f, 0.f});
+        const int o = 16 * j + n, h = o / kD, e = o % kD;
+        bf16x4 val, pad;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int64_t tok = t0 + 4 * g + i;
+          const bool valid = tok < a.n_tok && (a.mask == nullptr || a.mask[tok] != 0);
+          val[i] = (__bf16)(valid ? vt[i] : 0.0f);
+          pad[i] = (__bf16)(valid && e == 16 ? 1.0f : 0.0f);
+        }
+        u32x2* dst = reinterpret_cast<u32x2*>(a.vt) + (((int64_t)h * (a.n_pad / 16) + tile) * 64 + 16 * g) * 2;
+        dst[(e % 16) * 2 + e / 16] = __builtin_bit_cast(u32x2, val);
+        if (e >= 16) dst[(e - 8) * 2 + 1] = __builtin_bit_cast(u32x2, pad);
         continue;
       }
-      // acc[u][et][i] = proj[e = 16 et + 4g + i][token t0 + n]
+      // acc[u][jt][i] = proj[output 16 j + 4g + i][token t0 + n]; the four
+      // outputs lie in one head (24 is a multiple of 4)
       const int64_t tok = t0 + n;
+      const int o = 16 * j + 4 * g, h = o / kD, e = o % kD;
       if (which == 3) {
         if (tok >= a.n_q) continue;
+        f32x4 sg;
 #pragma unroll
-        for (int et = 0; et < 2; ++et) {
-          const int e0 = 16 * et + 4 * g;
-          if (e0 >= kD) continue;
-          float4 o;
-          o.x = 1.0f / (1.0f + __expf(-acc[u][et][0]));
-          o.y = 1.0f / (1.0f + __expf(-acc[u][et][1]));
-          o.z = 1.0f / (1.0f + __expf(-acc[u][et][2]));
-          o.w = 1.0f / (1.0f + __expf(-acc[u][et][3]));
-          *reinterpret_cast<float4*>(a.g + tok * (kH * kD) + h * kD + e0) = o;
-        }
+        for (int i = 0; i < 4; ++i) sg[i] = 1.0f / (1.0f + __expf(-acc[u][jt][i]));
+        *reinterpret_cast<f32x4*>(a.g + tok * kHD + o) = sg;
         continue;
       }
-      if (which == 1 && h == 0) {
+      if (which == 1 && j == 0) {
         // per-tile key mask: bit i = token t0 + i exists and attends
         const bool kv_valid = tok < a.n_tok && (a.mask == nullptr || a.mask[tok] != 0);
         const uint32_t bits = (uint32_t)(__ballot(kv_valid) & 0xFFFFull);
@@ -236,26 +248,30 @@ __global__ void __launch_bounds__(64 * kProjWaves) __attribute__((amdgpu_waves_p
         scale = 1.0f;
         dst = a.k + ((int64_t)h * a.n_pad + tok) * kDp;
       }
+      bf16x4 val;
 #pragma unroll
-      for (int et = 0; et < 2; ++et) {
-        bf16x4 o;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) o[i] = (__bf16)(valid ? acc[u][et][i] * scale : 0.0f);  // rows >= 24 are 0
-        *reinterpret_cast<u32x2*>(dst + 16 * et + 4 * g) = __builtin_bit_cast(u32x2, o);
-      }
+      for (int i = 0; i < 4; ++i) val[i] = (__bf16)(valid ? acc[u][jt][i] * scale : 0.0f);
+      *reinterpret_cast<u32x2*>(dst + e) = __builtin_bit_cast(u32x2, val);
+      if (e == kD - 4) *reinterpret_cast<u32x4*>(dst + kD) = u32x4{0u, 0u, 0u, 0u};  // e = 24 .. 31
     }
   }
 }
 
 }  // namespace
 
+size_t fast_proj_split_bytes(int32_t c_s) { return (size_t)4 * kOutTiles * (c_s / 32) * 2048; }
+
 hipError_t launch_fast_proj(const FastProjArgs& a, hipStream_t st) {
-  // token groups rounded up to whole sets of 8 (one per XCD), 4 projections x
-  // 2 head halves each
-  const int64_t tiles = (a.n_pad > a.nq_pad ? a.n_pad : a.nq_pad) / 16;
-  const int64_t groups = (tiles + kProjTiles - 1) / kProjTiles;
-  const int64_t sets = (groups + 7) / 8;
-  hipLaunchKernelGGL(proj_kernel, dim3((unsigned)(sets * 8 * 4 * kProjHalves)), dim3(64 * kProjWaves), 0, st, a);
+  const int64_t split_threads = (int64_t)4 * kOutTiles * (a.c_s / 32) * 64;
+  hipLaunchKernelGGL(proj_split_kernel, dim3((unsigned)((split_threads + 255) / 256)), dim3(256), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // (side, token group) items, rounded up to whole sets of 8 (one per XCD),
+  // 3 workgroups each
+  const int64_t items =
+      (a.n_pad / 16 + kProjTiles - 1) / kProjTiles + (a.nq_pad / 16 + kProjTiles - 1) / kProjTiles;
+  const int64_t sets = (items + 7) / 8;
+  hipLaunchKernelGGL(proj_kernel, dim3((unsigned)(sets * 8 * kProjSideWgs)), dim3(64 * kProjWaves), 0, st, a);
   return hipGetLastError();
 }
 
