@@ -51,30 +51,29 @@ __device__ __forceinline__ int split_offset(int p, int j, int s, int n_ks) {
   return ((p * kOutTiles + j) * n_ks + s) * 2048;
 }
 
-// One thread per (projection, output tile, k-step, lane): 8 weights, 32 bytes
-// in, 16 bytes of hi and 16 of lo out.
+// One thread per 4 consecutive weights of a row of W_p (reads in row order,
+// 16 bytes per thread): element (o, c), o = 16 j + n, c = 32 s + 8 g + i,
+// goes to lane 16 g + n, slot i of (p, j, s); 8 bytes of hi and 8 of lo out.
 __global__ void __launch_bounds__(256) proj_split_kernel(FastProjArgs a) {
-  const int n_ks = a.c_s / 32;
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= (int64_t)4 * kOutTiles * n_ks * 64) return;
-  const int lane = (int)(t & 63), n = lane & 15, g = lane >> 4;
-  const int s = (int)((t >> 6) % n_ks);
-  const int j = (int)((t >> 6) / n_ks % kOutTiles);
-  const int p = (int)((t >> 6) / n_ks / kOutTiles);
+  const int q4 = a.c_s / 4;  // float4s per row
+  if (t >= (int64_t)4 * kHD * q4) return;
+  const int p = (int)(t / ((int64_t)kHD * q4));
+  const int o = (int)(t / q4 % kHD), c = 4 * (int)(t % q4);
   const float* w = p == 0 ? a.w_q : p == 1 ? a.w_k : p == 2 ? a.w_v : a.w_g;
-  const float4* src = reinterpret_cast<const float4*>(w + (int64_t)(16 * j + n) * a.c_s + 32 * s + 8 * g);
-  const float4 w0 = src[0], w1 = src[1];
-  const float xs[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-  bf16x8 hi, lo;
+  const float4 x = *reinterpret_cast<const float4*>(w + (int64_t)o * a.c_s + c);
+  const float xs[4] = {x.x, x.y, x.z, x.w};
+  bf16x4 hi, lo;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < 4; ++i) {
     const __bf16 hv = (__bf16)xs[i];
     hi[i] = hv;
     lo[i] = (__bf16)(xs[i] - (float)hv);
   }
-  char* dst = reinterpret_cast<char*>(a.w_split) + split_offset(p, j, s, n_ks) + 16 * lane;
-  *reinterpret_cast<bf16x8*>(dst) = hi;
-  *reinterpret_cast<bf16x8*>(dst + 1024) = lo;
+  const int j = o / 16, n = o % 16, s = c / 32, g = c % 32 / 8, i0 = c % 8;
+  char* dst = reinterpret_cast<char*>(a.w_split) + split_offset(p, j, s, a.c_s / 32) + 16 * (16 * g + n) + 2 * i0;
+  *reinterpret_cast<bf16x4*>(dst) = hi;
+  *reinterpret_cast<bf16x4*>(dst + 1024) = lo;
 }
 
 // One workgroup = 128 tokens x one side (query: q and g of the stripe's rows;
@@ -262,7 +261,7 @@ __global__ void __launch_bounds__(64 * kProjWaves) __attribute__((amdgpu_waves_p
 size_t fast_proj_split_bytes(int32_t c_s) { return (size_t)4 * kOutTiles * (c_s / 32) * 2048; }
 
 hipError_t launch_fast_proj(const FastProjArgs& a, hipStream_t st) {
-  const int64_t split_threads = (int64_t)4 * kOutTiles * (a.c_s / 32) * 64;
+  const int64_t split_threads = (int64_t)4 * kHD * (a.c_s / 4);
   hipLaunchKernelGGL(proj_split_kernel, dim3((unsigned)((split_threads + 255) / 256)), dim3(256), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
