@@ -69,7 +69,9 @@ __device__ __forceinline__ uint64_t bitonic_stage(uint64_t v, int lane) {
   const uint64_t p = xor_lane64<M>(v);
   const bool up = SIZE >= 64 || (lane & SIZE) == 0;
   const bool keep_min = ((lane & M) == 0) == up;
-  return keep_min ? (p < v ? p : v) : (p > v ? p : v);
+  // the partner's key where it is the one to keep: one comparison per stage
+  // (equal keys are the same either way)
+  return ((p < v) == keep_min) ? p : v;
 }
 
 // Merge pass of size SIZE: sorts every bitonic run of SIZE lanes (ascending
