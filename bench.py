@@ -387,12 +387,14 @@ def knn_main(args, wl):
     idx = torch.empty((n_q, k), dtype=torch.int32, device=dev)
     d2 = torch.empty((n_q, k), dtype=torch.float32, device=dev)
     pairs = n_q * L
+    ws_bytes = dcp.dcp_knn_workspace_size(L)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     hip = Hip()
 
     def step(evs=None):
         if evs is not None:
             dcp.dcp_set_timing_events(*evs)
-        dcp.dcp_knn_topk(xq, n_q, x, L, 0, wl.q_row0, None, None, 0, k, idx, d2, sp)
+        dcp.dcp_knn_topk(xq, n_q, x, L, 0, wl.q_row0, None, None, 0, k, idx, d2, ws, ws_bytes, sp)
         if evs is not None:
             dcp.dcp_set_timing_events(None, None)
 

@@ -290,10 +290,20 @@ int dcp_sparse_pair_bias_attention(const dcp_sparse_shape* shape, const dcp_weig
  *   idx_out    [n_q, k] int32 global indices, nearest first; -1 past the
  *              number of admissible candidates
  *   d2_out     [n_q, k] fp32 squared distances (+inf past the end), or NULL
- * Device pointers, 4-byte aligned. No workspace. n_q = 0 is a no-op. */
+ *   workspace  at least dcp_knn_workspace_size(n_c) bytes of device memory,
+ *              256-byte aligned (may be NULL when n_c = 0): the candidates
+ *              re-laid out and the bounding box of every 128 of them, written
+ *              by this call; owned by the caller, contents undefined after
+ * Device pointers, 4-byte aligned. n_q = 0 is a no-op. A workspace that is
+ * missing, misaligned or too small returns DCP_ERR_WORKSPACE. */
 int dcp_knn_topk(const float* x_q, int64_t n_q, const float* x_c, int64_t n_c, int64_t c_index0, int64_t q_self0,
                  const int32_t* group_q, const int32_t* group_c, int32_t group_mode, int32_t k, int32_t* idx_out,
-                 float* d2_out, void* stream);
+                 float* d2_out, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes that dcp_knn_topk needs for n_c candidates (written to
+ * *bytes): 16 per candidate plus 32 per 128 candidates. Host-only; launches
+ * nothing. */
+int dcp_knn_workspace_size(int64_t n_c, size_t* bytes);
 
 /* The ring top-k combine: per row, the k smallest entries of the union of two
  * lists sorted as dcp_knn_topk returns them ([n_rows, k] each; index -1 =

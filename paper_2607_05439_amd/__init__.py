@@ -4,7 +4,7 @@ Every step of the computation runs in the library's HIP kernels; PyTorch is
 used for device memory and streams. The functions carry the C names
 (``dcp_pair_bias_attention``, ``dcp_pair_bias_attention_noalloc``, ``dcp_pair_bias_attention_partial``, ``dcp_bias_project``, ``dcp_block_merge``,
 ``dcp_workspace_size``, ``dcp_workspace_bytes``, ``dcp_sparse_pair_bias_attention``,
-``dcp_sparse_workspace_size``, ``dcp_knn_topk``, ``dcp_topk_merge``,
+``dcp_sparse_workspace_size``, ``dcp_knn_topk``, ``dcp_knn_workspace_size``, ``dcp_topk_merge``,
 ``dcp_pair_transition``, ``dcp_transition_workspace_size``, ``dcp_scatter_mean``,
 ``dcp_scatter_mean_workspace_size``) and accept torch tensors (device pointers are taken
 from ``data_ptr()``) or plain integer addresses. Loading fails loudly when the
@@ -23,7 +23,7 @@ DCP_F32, DCP_BF16 = 0, 1
 DCP_OK, DCP_ERR_INVALID_ARGUMENT, DCP_ERR_UNSUPPORTED, DCP_ERR_WORKSPACE, DCP_ERR_HIP = 0, -1, -2, -3, -4
 EXPORTS = ("dcp_workspace_size", "dcp_workspace_bytes", "dcp_pair_bias_attention", "dcp_pair_bias_attention_noalloc", "dcp_pair_bias_attention_partial", "dcp_bias_project",
            "dcp_block_merge",
-           "dcp_sparse_workspace_size", "dcp_sparse_pair_bias_attention", "dcp_knn_topk", "dcp_topk_merge",
+           "dcp_sparse_workspace_size", "dcp_sparse_pair_bias_attention", "dcp_knn_topk", "dcp_knn_workspace_size", "dcp_topk_merge",
            "dcp_transition_workspace_size", "dcp_pair_transition", "dcp_scatter_mean_workspace_size",
            "dcp_scatter_mean", "dcp_set_timing_events",
            "dcp_last_error", "dcp_version")
@@ -75,7 +75,8 @@ def lib() -> ctypes.CDLL:
         L.dcp_sparse_workspace_size.argtypes = [P(DcpSparseShape), i64, P(sz)]
         L.dcp_sparse_pair_bias_attention.argtypes = [P(DcpSparseShape), P(DcpWeights), vp, vp, vp, i64, i64, i32, vp,
                                                      vp, sz, vp]
-        L.dcp_knn_topk.argtypes = [vp, i64, vp, i64, i64, i64, vp, vp, i32, i32, vp, vp, vp]
+        L.dcp_knn_topk.argtypes = [vp, i64, vp, i64, i64, i64, vp, vp, i32, i32, vp, vp, vp, ctypes.c_size_t, vp]
+        L.dcp_knn_workspace_size.argtypes = [i64, ctypes.POINTER(ctypes.c_size_t)]
         L.dcp_topk_merge.argtypes = [i64, i32, vp, vp, vp, vp, vp, vp, vp]
         L.dcp_transition_workspace_size.argtypes = [i32, i32, i32, P(sz)]
         L.dcp_pair_transition.argtypes = [i64, i32, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
@@ -85,7 +86,7 @@ def lib() -> ctypes.CDLL:
         for f in (L.dcp_workspace_size, L.dcp_pair_bias_attention, L.dcp_pair_bias_attention_noalloc,
                   L.dcp_pair_bias_attention_partial,
                   L.dcp_bias_project, L.dcp_block_merge,
-                  L.dcp_sparse_workspace_size, L.dcp_sparse_pair_bias_attention, L.dcp_knn_topk, L.dcp_topk_merge,
+                  L.dcp_sparse_workspace_size, L.dcp_sparse_pair_bias_attention, L.dcp_knn_topk, L.dcp_knn_workspace_size, L.dcp_topk_merge,
                   L.dcp_transition_workspace_size, L.dcp_pair_transition, L.dcp_scatter_mean_workspace_size,
                   L.dcp_scatter_mean, L.dcp_set_timing_events):
             f.restype = ctypes.c_int
@@ -203,10 +204,18 @@ def dcp_sparse_pair_bias_attention(shape: DcpSparseShape, weights: DcpWeights, a
                                                 workspace_bytes, _stream(stream)))
 
 
+def dcp_knn_workspace_size(n_c: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().dcp_knn_workspace_size(n_c, ctypes.byref(n)))
+    return n.value
+
+
 def dcp_knn_topk(x_q: Ptr, n_q: int, x_c: Ptr, n_c: int, c_index0: int, q_self0: int, group_q: Ptr, group_c: Ptr,
-                 group_mode: int, k: int, idx_out: Ptr, d2_out: Ptr, stream=None) -> None:
+                 group_mode: int, k: int, idx_out: Ptr, d2_out: Ptr, workspace: Ptr, workspace_bytes: int,
+                 stream=None) -> None:
     _check(lib().dcp_knn_topk(_ptr(x_q), n_q, _ptr(x_c), n_c, c_index0, q_self0, _ptr(group_q), _ptr(group_c),
-                              group_mode, k, _ptr(idx_out), _ptr(d2_out), _stream(stream)))
+                              group_mode, k, _ptr(idx_out), _ptr(d2_out), _ptr(workspace), workspace_bytes,
+                              _stream(stream)))
 
 
 def dcp_topk_merge(n_rows: int, k: int, idx_a: Ptr, d2_a: Ptr, idx_b: Ptr, d2_b: Ptr, idx_out: Ptr, d2_out: Ptr,

@@ -709,9 +709,16 @@ int dcp_sparse_pair_bias_attention(const dcp_sparse_shape* shape, const dcp_weig
 }
 
 // ----------------------------------------------------------------------------- k nearest neighbours
+int dcp_knn_workspace_size(int64_t n_c, size_t* bytes) {
+  if (!bytes) return fail(DCP_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  if (n_c < 0) return fail(DCP_ERR_INVALID_ARGUMENT, "n_c must be >= 0");
+  *bytes = dcp::knn_workspace_bytes(n_c, nullptr);
+  return ok();
+}
+
 int dcp_knn_topk(const float* x_q, int64_t n_q, const float* x_c, int64_t n_c, int64_t c_index0, int64_t q_self0,
                  const int32_t* group_q, const int32_t* group_c, int32_t group_mode, int32_t k, int32_t* idx_out,
-                 float* d2_out, void* stream) {
+                 float* d2_out, void* workspace, size_t workspace_bytes, void* stream) {
   if (n_q < 0 || n_c < 0) return fail(DCP_ERR_INVALID_ARGUMENT, "n_q and n_c must be >= 0");
   if (k < 1) return fail(DCP_ERR_INVALID_ARGUMENT, "k must be >= 1 (got %d)", k);
   if (k > dcp::kKnnMaxK) return fail(DCP_ERR_UNSUPPORTED, "k must be <= %d (got %d)", dcp::kKnnMaxK, k);
@@ -725,7 +732,12 @@ int dcp_knn_topk(const float* x_q, int64_t n_q, const float* x_c, int64_t n_c, i
     return fail(DCP_ERR_INVALID_ARGUMENT, "x_q, x_c (when n_c > 0) and idx_out are required");
   if (!aligned(x_q, 4) || !aligned(x_c, 4) || !aligned(idx_out, 4) || (d2_out && !aligned(d2_out, 4)))
     return fail(DCP_ERR_INVALID_ARGUMENT, "x_q, x_c, idx_out and d2_out must be 4-byte aligned");
-  if (n_q == 0) return ok();
+  size_t box_offset = 0;
+  const size_t need = dcp::knn_workspace_bytes(n_c, &box_offset);
+  if (n_c > 0 && (!workspace || !aligned(workspace, 256)))
+    return fail(DCP_ERR_WORKSPACE, "workspace must be a 256-byte aligned device pointer");
+  if (n_c > 0 && workspace_bytes < need)
+    return fail(DCP_ERR_WORKSPACE, "workspace too small: %zu bytes given, %zu needed", workspace_bytes, need);
   dcp::KnnArgs a{};
   a.x_q = x_q;
   a.x_c = x_c;
@@ -739,6 +751,8 @@ int dcp_knn_topk(const float* x_q, int64_t n_q, const float* x_c, int64_t n_c, i
   a.group_mode = group_mode;
   a.idx_out = idx_out;
   a.d2_out = d2_out;
+  a.cand = workspace;
+  a.box = static_cast<char*>(workspace) + box_offset;
   hipError_t e;
   if (g_ev_start && (e = hipEventRecord(static_cast<hipEvent_t>(g_ev_start), static_cast<hipStream_t>(stream))) != hipSuccess)
     return fail(DCP_ERR_HIP, "hipEventRecord failed: %s", hipGetErrorString(e));

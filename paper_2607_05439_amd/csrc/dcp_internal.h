@@ -173,6 +173,7 @@ struct KnnArgs {
   int32_t k, group_mode;
   int32_t* idx_out;       // [n_q][k]
   float* d2_out;          // [n_q][k] or null
+  void *cand, *box;       // workspace: [n_c] float4 candidates, [ceil(n_c / 128)][2] float4 boxes
 };
 
 struct TopkMergeArgs {
@@ -238,6 +239,7 @@ hipError_t launch_gen_bias(const GenBiasArgs& a, hipStream_t st);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t st);
 hipError_t launch_sparse_proj(const SparseProjArgs& a, hipStream_t st);
 hipError_t launch_sparse_attn(const SparseAttnArgs& a, bool bf16, hipStream_t st);
+size_t knn_workspace_bytes(int64_t n_c, size_t* box_offset);
 hipError_t launch_knn(const KnnArgs& a, hipStream_t st);
 hipError_t launch_topk_merge(const TopkMergeArgs& a, hipStream_t st);
 hipError_t launch_transition(const TransArgs& a, hipStream_t st);

@@ -8,23 +8,28 @@
 // smaller candidate index. The 64-bit key (d2 bits << 32) | index orders
 // exactly that way (d2 >= 0).
 //
-// knn_kernel: a workgroup of 8 waves serves 32 consecutive query rows, 4 per
-// wave (their coordinates and thresholds are wave-uniform scalars). Candidates
-// are staged through LDS in tiles of 2048 as (x, y, z, group) and shared by the
-// 8 waves; tiles are visited starting at the one that holds the queries
-// themselves when they are candidates (their sequence neighbours are close in
-// space, which makes the thresholds tight early; the result does not depend on
-// the order). Per tile, the bounding box of every 128 candidates is formed in
-// LDS, and a wave skips the candidates of a box whose distance (computed in
+// knn_prep_kernel: one pass over the candidates writes each as a 16-byte
+// entry (x, y, z, then |c|^2, or the group in the group modes) and, for every
+// step of 128 consecutive candidates, its bounding box (low and high corner),
+// into the caller's workspace.
+// knn_kernel: a workgroup of 8 independent waves serves 32 consecutive query
+// rows, 4 per wave (their coordinates and thresholds are wave-uniform
+// scalars). A wave visits the candidates in groups of 16 steps (2048
+// candidates), starting at the group that holds the queries themselves when
+// they are candidates (their sequence neighbours are close in space, which
+// makes the thresholds tight early; the result does not depend on the order).
+// Per group it tests the 16 boxes against its 4 queries (the next group's
+// boxes are loaded meanwhile) and skips a step whose box distance (computed in
 // the definition's rounded operations, which bound every member's distance
-// from below) exceeds the current k-th distance of all 4 of its queries: an
-// exact exclusion, not a heuristic. A lane takes one candidate per 64-candidate step and tests it
-// against the 4 queries with a cheap conservative bound (|c|^2 - 2 c.q by
-// three multiply-adds, |c|^2 staged with the tile, against a per-query limit
-// derived from the current k-th distance with a proven rounding margin): no
-// candidate that could enter is rejected. Only where some lane passes does the
-// step compute the distances of the definition; the exact 64-bit key test then
-// picks the candidates that enter the query's 64-entry LDS buffer. The sorted top-k
+// from below) exceeds the current k-th distance of all 4 queries: an exact
+// exclusion, not a heuristic. Only the candidates of the remaining steps are
+// read, straight from the workspace (L2-resident): a lane takes two per step
+// and tests them against the 4 queries with a cheap conservative bound (|c|^2
+// - 2 c.q by three multiply-adds against a per-query limit derived from the
+// current k-th distance with a proven rounding margin): no candidate that
+// could enter is rejected. Only where some lane passes does the step compute
+// the distances of the definition; the exact 64-bit key test then picks the
+// candidates that enter the query's 64-entry LDS buffer. The sorted top-k
 // lives in registers (entry 64s + lane in slot s); a full buffer is sorted
 // (bitonic network across lanes) and merged slot by slot: the lane-wise
 // minimum of a sorted slot and the reversed sorted carry is a bitonic sequence
@@ -42,7 +47,6 @@ namespace {
 constexpr int kKnnWaves = 8;
 constexpr int kKnnQ = 4;                          // query rows per wave
 constexpr int kKnnRows = kKnnWaves * kKnnQ;       // query rows per workgroup
-constexpr int kTile = 2048;                       // candidates per LDS tile
 constexpr uint64_t kNoKey = ~0ULL;
 
 // Value of lane (lane ^ M).
@@ -206,18 +210,54 @@ __device__ __forceinline__ float dist2(float qx, float qy, float qz, float4 c) {
   return (dx * dx + dy * dy) + dz * dz;
 }
 
+constexpr int kStep = 128;   // candidates per bounding box
+constexpr int kGroup = 2048;  // candidates per group of 16 steps (one skip test per lane)
+
+// one wave per step of 128 candidates, two per lane
+template <int MODE>
+__global__ void __launch_bounds__(256) knn_prep_kernel(KnnArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t st = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (st * kStep >= a.n_c) return;
+  float4* c4 = static_cast<float4*>(a.cand);
+  float4* box = static_cast<float4*>(a.box);
+  float lx = __builtin_inff(), ly = lx, lz = lx, hx = -lx, hy = -lx, hz = -lx;
+  for (int h = 0; h < 2; ++h) {
+    const int64_t i = st * kStep + 64 * h + lane;
+    if (i < a.n_c) {
+      const float* p = a.x_c + 3 * i;
+      float4 v = make_float4(p[0], p[1], p[2], 0.f);
+      v.w = MODE ? __int_as_float(a.group_c[i]) : norm2(v);
+      c4[i] = v;
+      lx = fminf(lx, v.x); ly = fminf(ly, v.y); lz = fminf(lz, v.z);
+      hx = fmaxf(hx, v.x); hy = fmaxf(hy, v.y); hz = fmaxf(hz, v.z);
+    }
+  }
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) {
+    lx = fminf(lx, __shfl_xor(lx, m));
+    ly = fminf(ly, __shfl_xor(ly, m));
+    lz = fminf(lz, __shfl_xor(lz, m));
+    hx = fmaxf(hx, __shfl_xor(hx, m));
+    hy = fmaxf(hy, __shfl_xor(hy, m));
+    hz = fmaxf(hz, __shfl_xor(hz, m));
+  }
+  if (lane == 0) {
+    box[2 * st] = make_float4(lx, ly, lz, 0.f);
+    box[2 * st + 1] = make_float4(hx, hy, hz, 0.f);
+  }
+}
+
 template <int KS, int MODE>
 __global__ void __launch_bounds__(64 * kKnnWaves) __attribute__((amdgpu_waves_per_eu(KS == 2 ? 6 : 1))) knn_kernel(KnnArgs a) {
-  __shared__ float4 s_c[kTile];  // x, y, z, then |c|^2 (MODE 0) or the group bits
   __shared__ uint64_t s_buf[kKnnWaves][kKnnQ][64];
-  __shared__ float4 s_box[kTile / 128][2];  // bounding box (low, high corner) of each 128-candidate step
-
+  const float4* c4 = static_cast<const float4*>(a.cand);
+  const float4* box = static_cast<const float4*>(a.box);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int64_t r0 = (int64_t)blockIdx.x * kKnnRows;
   const int64_t rw = r0 + wave * kKnnQ;
   const int k = a.k;
-
   QueryTopk<KS> q[kKnnQ];
 #pragma unroll
   for (int j = 0; j < kKnnQ; ++j) {
@@ -234,75 +274,26 @@ __global__ void __launch_bounds__(64 * kKnnWaves) __attribute__((amdgpu_waves_pe
     q[j].qn = uniform(__builtin_sqrtf(q[j].qq));
     q[j].set_limit();
   }
-
-  const int64_t n_tiles = (a.n_c + kTile - 1) / kTile;
+  const int64_t n_steps = (a.n_c + kStep - 1) / kStep;
+  const int64_t n_groups = (a.n_c + kGroup - 1) / kGroup;
   int64_t t0 = 0;
-  if (a.q_self0 >= 0 && n_tiles > 0) t0 = ((a.q_self0 + r0) / kTile) % n_tiles;
-  for (int64_t tt = 0; tt < n_tiles; ++tt) {
-    const int64_t tile = (t0 + tt) % n_tiles;
-    const int64_t c0 = tile * kTile;
-    const int n_here = (int)min((int64_t)kTile, a.n_c - c0);
-    __syncthreads();  // the previous tile has been read by every wave
-    for (int i = threadIdx.x; i < kTile; i += 64 * kKnnWaves) {
-      float4 v;
-      if (i < n_here) {
-        const float* p = a.x_c + 3 * (c0 + i);
-        v = make_float4(p[0], p[1], p[2], 0.f);
-        v.w = MODE ? __int_as_float(a.group_c[c0 + i]) : norm2(v);
-      } else {
-        v = make_float4(__builtin_nanf(""), 0.f, 0.f, 0.f);  // never passes the prefilter of a full top-k
-      }
-      s_c[i] = v;
-    }
-    __syncthreads();
-    // Bounding box of each 128-candidate step: wave w takes steps 2w and
-    // 2w + 1, lane l step 2w + l / 32 and its candidates l % 32 + 32 m.
-    // Padding entries (NaN x) drop out of the minima and maxima.
-    {
-      const int st = 2 * wave + (lane >> 5);
-      float lx = __builtin_inff(), ly = lx, lz = lx, hx = -lx, hy = -lx, hz = -lx;
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const float4 c = s_c[128 * st + (lane & 31) + 32 * m];
-        lx = fminf(lx, c.x); ly = fminf(ly, c.y); lz = fminf(lz, c.z);
-        hx = fmaxf(hx, c.x); hy = fmaxf(hy, c.y); hz = fmaxf(hz, c.z);
-      }
-      lx = fminf(lx, __uint_as_float(xor_lane<1>(__float_as_uint(lx))));
-      lx = fminf(lx, __uint_as_float(xor_lane<2>(__float_as_uint(lx))));
-      lx = fminf(lx, __uint_as_float(xor_lane<4>(__float_as_uint(lx))));
-      lx = fminf(lx, __uint_as_float(xor_lane<8>(__float_as_uint(lx))));
-      lx = fminf(lx, __uint_as_float(xor_lane<16>(__float_as_uint(lx))));
-      ly = fminf(ly, __uint_as_float(xor_lane<1>(__float_as_uint(ly))));
-      ly = fminf(ly, __uint_as_float(xor_lane<2>(__float_as_uint(ly))));
-      ly = fminf(ly, __uint_as_float(xor_lane<4>(__float_as_uint(ly))));
-      ly = fminf(ly, __uint_as_float(xor_lane<8>(__float_as_uint(ly))));
-      ly = fminf(ly, __uint_as_float(xor_lane<16>(__float_as_uint(ly))));
-      lz = fminf(lz, __uint_as_float(xor_lane<1>(__float_as_uint(lz))));
-      lz = fminf(lz, __uint_as_float(xor_lane<2>(__float_as_uint(lz))));
-      lz = fminf(lz, __uint_as_float(xor_lane<4>(__float_as_uint(lz))));
-      lz = fminf(lz, __uint_as_float(xor_lane<8>(__float_as_uint(lz))));
-      lz = fminf(lz, __uint_as_float(xor_lane<16>(__float_as_uint(lz))));
-      hx = fmaxf(hx, __uint_as_float(xor_lane<1>(__float_as_uint(hx))));
-      hx = fmaxf(hx, __uint_as_float(xor_lane<2>(__float_as_uint(hx))));
-      hx = fmaxf(hx, __uint_as_float(xor_lane<4>(__float_as_uint(hx))));
-      hx = fmaxf(hx, __uint_as_float(xor_lane<8>(__float_as_uint(hx))));
-      hx = fmaxf(hx, __uint_as_float(xor_lane<16>(__float_as_uint(hx))));
-      hy = fmaxf(hy, __uint_as_float(xor_lane<1>(__float_as_uint(hy))));
-      hy = fmaxf(hy, __uint_as_float(xor_lane<2>(__float_as_uint(hy))));
-      hy = fmaxf(hy, __uint_as_float(xor_lane<4>(__float_as_uint(hy))));
-      hy = fmaxf(hy, __uint_as_float(xor_lane<8>(__float_as_uint(hy))));
-      hy = fmaxf(hy, __uint_as_float(xor_lane<16>(__float_as_uint(hy))));
-      hz = fmaxf(hz, __uint_as_float(xor_lane<1>(__float_as_uint(hz))));
-      hz = fmaxf(hz, __uint_as_float(xor_lane<2>(__float_as_uint(hz))));
-      hz = fmaxf(hz, __uint_as_float(xor_lane<4>(__float_as_uint(hz))));
-      hz = fmaxf(hz, __uint_as_float(xor_lane<8>(__float_as_uint(hz))));
-      hz = fmaxf(hz, __uint_as_float(xor_lane<16>(__float_as_uint(hz))));
-      if ((lane & 31) == 0) {
-        s_box[st][0] = make_float4(lx, ly, lz, 0.f);
-        s_box[st][1] = make_float4(hx, hy, hz, 0.f);
-      }
-    }
-    __syncthreads();
+  if (a.q_self0 >= 0 && n_groups > 0) t0 = ((a.q_self0 + r0) / kGroup) % n_groups;
+  const int jq = lane >> 4;
+  // lane l holds the box of step l % 16 of a group (the group's last step
+  // where it has fewer: those bits are never used)
+  auto box_of = [&](int64_t grp, float4& lo, float4& hi) {
+    const int64_t st = min(grp * (kGroup / kStep) + (lane & 15), n_steps - 1);
+    lo = box[2 * st];
+    hi = box[2 * st + 1];
+  };
+  float4 blo, bhi;
+  if (n_groups > 0) box_of(t0, blo, bhi);
+  for (int64_t tt = 0; tt < n_groups; ++tt) {
+    const int64_t grp = (t0 + tt) % n_groups;
+    const int64_t c0 = grp * kGroup;
+    const int n_here = (int)min((int64_t)kGroup, a.n_c - c0);
+    const float4 lo = blo, hi = bhi;
+    if (tt + 1 < n_groups) box_of((t0 + tt + 1) % n_groups, blo, bhi);  // in flight during this group
     // Steps no candidate of which can enter any of the wave's 4 top-k lists:
     // lane l tests step l % 16 against query l / 16. For a candidate c in the
     // box, |x_q - x_c| >= the box distance bx per axis, and the definition's
@@ -310,20 +301,15 @@ __global__ void __launch_bounds__(64 * kKnnWaves) __attribute__((amdgpu_waves_pe
     // differences and d = ((bx*bx) + (by*by)) + (bz*bz) in the definition's
     // order, the candidate's distance is at least d. A candidate enters only
     // with distance <= the current k-th distance T, so d > T excludes the
-    // whole step. (T only decreases, so the test stays valid for the tile; with
-    // fewer than k entries T is NaN and nothing is excluded; an all-padding
-    // step has a NaN box and is not excluded.)
+    // whole step. (T only decreases, so the test stays valid for the group;
+    // with fewer than k entries T is NaN and nothing is excluded.)
     uint32_t skip;
     {
-      const int st = lane & 15, jq = lane >> 4;
-      const float4 lo = s_box[st][0], hi = s_box[st][1];
       float qx = q[0].x, qy = q[0].y, qz = q[0].z, T = __uint_as_float((uint32_t)(q[0].tau >> 32));
 #pragma unroll
       for (int j = 1; j < kKnnQ; ++j)
         if (jq == j) {
-          qx = q[j].x;
-          qy = q[j].y;
-          qz = q[j].z;
+          qx = q[j].x; qy = q[j].y; qz = q[j].z;
           T = __uint_as_float((uint32_t)(q[j].tau >> 32));
         }
       float d;
@@ -338,11 +324,11 @@ __global__ void __launch_bounds__(64 * kKnnWaves) __attribute__((amdgpu_waves_pe
       skip = (uint32_t)(far & (far >> 16) & (far >> 32) & (far >> 48) & 0xFFFFull);
     }
     const uint32_t index0 = (uint32_t)(a.c_index0 + c0);
-    // two steps of 64 candidates at a time; entries past n_here are padding
-    // (NaN distance) that the exact test rejects. In the tile that holds the
-    // wave's own queries the steps start just before them and wrap around, so
-    // their sequence neighbours come first.
-    const int n_pairs = (n_here + 127) >> 7;
+    // steps of 128 candidates, two per lane; entries past n_here take no
+    // part. In the group that holds the wave's own queries the steps start
+    // just before them and wrap around, so their sequence neighbours come
+    // first.
+    const int n_pairs = (n_here + kStep - 1) / kStep;
     int pr = 0;
     if (a.q_self0 >= 0) {
       const int64_t self = a.q_self0 + rw - c0;
@@ -351,15 +337,16 @@ __global__ void __launch_bounds__(64 * kKnnWaves) __attribute__((amdgpu_waves_pe
     for (int t = 0; t < n_pairs; ++t, pr = pr + 1 == n_pairs ? 0 : pr + 1) {
       if ((skip >> pr) & 1u) continue;
       const int s = pr << 7;
-      const float4 ca = s_c[s + lane], cb = s_c[s + 64 + lane];
+      const bool va = s + lane < n_here, vb = s + 64 + lane < n_here;
+      const float4 ca = c4[c0 + (va ? s + lane : 0)], cb = c4[c0 + (vb ? s + 64 + lane : 0)];
       const float cca = MODE ? norm2(ca) : ca.w, ccb = MODE ? norm2(cb) : cb.w;
       uint64_t ma[kKnnQ], mb[kKnnQ], any = 0;
 #pragma unroll
       for (int j = 0; j < kKnnQ; ++j) {
         const float ea = fmaf(ca.x, q[j].mx, fmaf(ca.y, q[j].my, fmaf(ca.z, q[j].mz, cca)));
         const float eb = fmaf(cb.x, q[j].mx, fmaf(cb.y, q[j].my, fmaf(cb.z, q[j].mz, ccb)));
-        ma[j] = __ballot(!(ea > q[j].lim));
-        mb[j] = __ballot(!(eb > q[j].lim));
+        ma[j] = __ballot(va && !(ea > q[j].lim));
+        mb[j] = __ballot(vb && !(eb > q[j].lim));
         any |= ma[j] | mb[j];
       }
       if (any == 0) continue;
@@ -368,11 +355,11 @@ __global__ void __launch_bounds__(64 * kKnnWaves) __attribute__((amdgpu_waves_pe
 #pragma unroll
       for (int j = 0; j < kKnnQ; ++j) {
         if (ma[j])
-          q[j].template offer<MODE>(__float_as_uint(dist2(q[j].x, q[j].y, q[j].z, ca)), index0 + s + lane,
-                                    s + lane < n_here, __float_as_int(ca.w), lane, k);
+          q[j].template offer<MODE>(__float_as_uint(dist2(q[j].x, q[j].y, q[j].z, ca)), index0 + s + lane, va,
+                                    __float_as_int(ca.w), lane, k);
         if (mb[j])
-          q[j].template offer<MODE>(__float_as_uint(dist2(q[j].x, q[j].y, q[j].z, cb)), index0 + s + 64 + lane,
-                                    s + 64 + lane < n_here, __float_as_int(cb.w), lane, k);
+          q[j].template offer<MODE>(__float_as_uint(dist2(q[j].x, q[j].y, q[j].z, cb)), index0 + s + 64 + lane, vb,
+                                    __float_as_int(cb.w), lane, k);
       }
     }
   }
@@ -442,6 +429,11 @@ __global__ void __launch_bounds__(256) topk_merge_kernel(TopkMergeArgs a) {
 
 template <int KS>
 hipError_t launch_knn_k(const KnnArgs& a, hipStream_t st) {
+  if (a.n_c > 0) {
+    const dim3 pg((unsigned)(((a.n_c + kStep - 1) / kStep + 3) / 4)), pb(256);
+    if (a.group_mode) hipLaunchKernelGGL((knn_prep_kernel<1>), pg, pb, 0, st, a);
+    else hipLaunchKernelGGL((knn_prep_kernel<0>), pg, pb, 0, st, a);
+  }
   const dim3 grid((unsigned)((a.n_q + kKnnRows - 1) / kKnnRows)), block(64 * kKnnWaves);
   if (a.group_mode == 1)
     hipLaunchKernelGGL((knn_kernel<KS, 1>), grid, block, 0, st, a);
@@ -453,6 +445,12 @@ hipError_t launch_knn_k(const KnnArgs& a, hipStream_t st) {
 }
 
 }  // namespace
+
+size_t knn_workspace_bytes(int64_t n_c, size_t* box_offset) {
+  const size_t cand = ((size_t)n_c * 16 + 255) / 256 * 256;
+  if (box_offset) *box_offset = cand;
+  return cand + (size_t)((n_c + kStep - 1) / kStep) * 32;
+}
 
 hipError_t launch_knn(const KnnArgs& a, hipStream_t st) {
   return a.k <= 128 ? launch_knn_k<2>(a, st) : launch_knn_k<4>(a, st);

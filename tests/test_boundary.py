@@ -252,8 +252,9 @@ def test_sparse_bad_arguments():
 
 
 # ----------------------------------------------------------------------------- k nearest neighbours
-def knn(x_q=FAKE, n_q=100, x_c=FAKE, n_c=1000, c0=0, self0=-1, gq=None, gc=None, mode=0, k=128, idx=FAKE, d2=FAKE):
-    return dcp.lib().dcp_knn_topk(x_q, n_q, x_c, n_c, c0, self0, gq, gc, mode, k, idx, d2, None)
+def knn(x_q=FAKE, n_q=100, x_c=FAKE, n_c=1000, c0=0, self0=-1, gq=None, gc=None, mode=0, k=128, idx=FAKE, d2=FAKE,
+        ws=FAKE, ws_bytes=1 << 20):
+    return dcp.lib().dcp_knn_topk(x_q, n_q, x_c, n_c, c0, self0, gq, gc, mode, k, idx, d2, ws, ws_bytes, None)
 
 
 def test_knn_bad_arguments():
@@ -270,8 +271,23 @@ def test_knn_bad_arguments():
     assert knn(x_c=None) == E
     assert knn(idx=None) == E
     assert knn(x_q=FAKE + 2) == E                  # misaligned
+    W = dcp.DCP_ERR_WORKSPACE
+    assert knn(ws=None) == W
+    assert knn(ws=FAKE + 16) == W                  # not 256-byte aligned
+    assert knn(ws_bytes=dcp.dcp_knn_workspace_size(1000) - 1) == W
     assert knn(n_q=0) == dcp.DCP_OK                # no-op
     assert len(dcp.dcp_last_error()) == 0
+
+
+def test_knn_workspace_size():
+    # 16 bytes per candidate (rounded to 256) plus 32 per started 128
+    assert dcp.dcp_knn_workspace_size(0) == 0
+    assert dcp.dcp_knn_workspace_size(1) == 256 + 32
+    assert dcp.dcp_knn_workspace_size(128) == 2048 + 32
+    assert dcp.dcp_knn_workspace_size(129) == 2304 + 64
+    assert dcp.dcp_knn_workspace_size(96000) == 96000 * 16 + 750 * 32
+    rc = dcp.lib().dcp_knn_workspace_size(-1, ctypes.byref(ctypes.c_size_t()))
+    assert rc == dcp.DCP_ERR_INVALID_ARGUMENT
 
 
 def test_topk_merge_bad_arguments():

@@ -24,7 +24,9 @@ def gpu_knn(x_q, x_c, k, c_index0=0, q_self0=-1, group_q=None, group_c=None, mod
     n_q = len(x_q)
     idx = torch.full((max(n_q, 1), k), -7, dtype=torch.int32, device="cuda:0")
     d2 = torch.full((max(n_q, 1), k), -7.0, dtype=torch.float32, device="cuda:0") if with_d2 else None
-    dcp.dcp_knn_topk(xq, n_q, xc, len(x_c), c_index0, q_self0, gq, gc, mode, k, idx, d2)
+    ws_bytes = dcp.dcp_knn_workspace_size(len(x_c))
+    ws = torch.full((max(ws_bytes, 1),), 0xA5, dtype=torch.uint8, device="cuda:0")  # stale contents
+    dcp.dcp_knn_topk(xq, n_q, xc, len(x_c), c_index0, q_self0, gq, gc, mode, k, idx, d2, ws, ws_bytes)
     return idx.cpu().numpy()[:n_q], (d2.cpu().numpy()[:n_q] if with_d2 else None)
 
 
