@@ -47,12 +47,17 @@ int main(void) {
   expect(dcp_sparse_workspace_size(&ss, 24000, &bytes), DCP_OK, "sparse workspace size");
   ss.k = 0;
   expect(dcp_sparse_workspace_size(&ss, 24000, &bytes), DCP_ERR_INVALID_ARGUMENT, "sparse k = 0");
-  expect(dcp_knn_topk(NULL, 10, fake_f, 10, 0, -1, NULL, NULL, 0, 4, fake_i, fake_f, NULL), DCP_ERR_INVALID_ARGUMENT,
+  expect(dcp_knn_topk(NULL, 10, fake_f, 10, 0, -1, NULL, NULL, 0, 4, fake_i, fake_f, NULL, 0, NULL), DCP_ERR_INVALID_ARGUMENT,
          "knn, null queries");
-  expect(dcp_knn_topk(fake_f, 10, fake_f, 10, 0, -1, NULL, NULL, 0, 0, fake_i, fake_f, NULL),
+  expect(dcp_knn_topk(fake_f, 10, fake_f, 10, 0, -1, NULL, NULL, 0, 0, fake_i, fake_f, NULL, 0, NULL),
          DCP_ERR_INVALID_ARGUMENT, "knn, k = 0");
-  expect(dcp_knn_topk(fake_f, 10, fake_f, 10, 0, -1, NULL, NULL, 1, 4, fake_i, fake_f, NULL),
+  expect(dcp_knn_topk(fake_f, 10, fake_f, 10, 0, -1, NULL, NULL, 1, 4, fake_i, fake_f, NULL, 0, NULL),
          DCP_ERR_INVALID_ARGUMENT, "knn, group mode without groups");
+  expect(dcp_knn_topk(fake_f, 10, fake_f, 10, 0, -1, NULL, NULL, 0, 4, fake_i, fake_f, NULL, 0, NULL),
+         DCP_ERR_WORKSPACE, "knn, no workspace");
+  expect(dcp_knn_workspace_size(96000, &bytes), DCP_OK, "knn workspace size");
+  expect(bytes == 96000 * 16 + 750 * 32 ? DCP_OK : -99, DCP_OK, "knn workspace size value");
+  expect(dcp_knn_workspace_size(-1, &bytes), DCP_ERR_INVALID_ARGUMENT, "knn workspace size, n_c < 0");
   expect(dcp_topk_merge(4, 0, fake_i, fake_f, fake_i, fake_f, fake_i, fake_f, NULL), DCP_ERR_INVALID_ARGUMENT,
          "topk merge, k = 0");
   expect(dcp_transition_workspace_size(128, 512, DCP_BF16, &bytes), DCP_OK, "transition workspace size");
