@@ -212,6 +212,7 @@ __device__ __forceinline__ float dist2(float qx, float qy, float qz, float4 c) {
 
 constexpr int kStep = 128;   // candidates per bounding box
 constexpr int kGroup = 2048;  // candidates per group of 16 steps (one skip test per lane)
+constexpr int kSeedWords = 64;  // steps whose seed bit a wave keeps: 64 x 64
 
 // one wave per step of 128 candidates, two per lane
 template <int MODE>
@@ -251,6 +252,7 @@ __global__ void __launch_bounds__(256) knn_prep_kernel(KnnArgs a) {
 template <int KS, int MODE>
 __global__ void __launch_bounds__(64 * kKnnWaves) __attribute__((amdgpu_waves_per_eu(KS == 2 ? 6 : 1))) knn_kernel(KnnArgs a) {
   __shared__ uint64_t s_buf[kKnnWaves][kKnnQ][64];
+  __shared__ uint64_t s_seed[kKnnWaves][kSeedWords];
   const float4* c4 = static_cast<const float4*>(a.cand);
   const float4* box = static_cast<const float4*>(a.box);
   const int lane = threadIdx.x & 63;
@@ -286,6 +288,78 @@ __global__ void __launch_bounds__(64 * kKnnWaves) __attribute__((amdgpu_waves_pe
     lo = box[2 * st];
     hi = box[2 * st + 1];
   };
+  // One step: 128 candidates from c0s, two per lane (entries past the n_s
+  // candidates take no part), the prefilter against the 4 queries, and the
+  // exact test and append where some lane passes it.
+  auto visit = [&](int64_t c0s, int n_s) {
+    const bool va = lane < n_s, vb = 64 + lane < n_s;
+    const float4 ca = c4[c0s + (va ? lane : 0)], cb = c4[c0s + (vb ? 64 + lane : 0)];
+    const float cca = MODE ? norm2(ca) : ca.w, ccb = MODE ? norm2(cb) : cb.w;
+    uint64_t ma[kKnnQ], mb[kKnnQ], any = 0;
+#pragma unroll
+    for (int j = 0; j < kKnnQ; ++j) {
+      const float ea = fmaf(ca.x, q[j].mx, fmaf(ca.y, q[j].my, fmaf(ca.z, q[j].mz, cca)));
+      const float eb = fmaf(cb.x, q[j].mx, fmaf(cb.y, q[j].my, fmaf(cb.z, q[j].mz, ccb)));
+      ma[j] = __ballot(va && !(ea > q[j].lim));
+      mb[j] = __ballot(vb && !(eb > q[j].lim));
+      any |= ma[j] | mb[j];
+    }
+    if (any == 0) return;
+    // the exact distances and keys decide; a flush lowers tau after the
+    // prefilter, so the masks stay a superset
+    const uint32_t index0 = (uint32_t)(a.c_index0 + c0s);
+#pragma unroll
+    for (int j = 0; j < kKnnQ; ++j) {
+      if (ma[j])
+        q[j].template offer<MODE>(__float_as_uint(dist2(q[j].x, q[j].y, q[j].z, ca)), index0 + lane, va,
+                                  __float_as_int(ca.w), lane, k);
+      if (mb[j])
+        q[j].template offer<MODE>(__float_as_uint(dist2(q[j].x, q[j].y, q[j].z, cb)), index0 + 64 + lane, vb,
+                                  __float_as_int(cb.w), lane, k);
+    }
+  };
+
+  // Seeds: the steps (among the first 64 x 64) whose box holds one of the
+  // wave's queries. They are visited first, the one that holds the queries
+  // themselves (as candidates) before the others, so that the k-th distances
+  // are small before the bulk of the candidates is tested; the full pass below
+  // then leaves them out. Only the visiting order changes, never the result.
+  const int64_t seed_steps = min(n_steps, (int64_t)kSeedWords * 64);
+  for (int64_t w0 = 0; w0 < seed_steps; w0 += 64) {
+    const int64_t st = w0 + lane;
+    bool in = false;
+    if (st < seed_steps) {
+      const float4 lo = box[2 * st], hi = box[2 * st + 1];
+#pragma unroll
+      for (int j = 0; j < kKnnQ; ++j)
+        in = in || (q[j].x >= lo.x && q[j].x <= hi.x && q[j].y >= lo.y && q[j].y <= hi.y && q[j].z >= lo.z &&
+                    q[j].z <= hi.z);
+    }
+    const uint64_t m = __ballot(in);
+    if (lane == 0) s_seed[wave][w0 >> 6] = m;
+  }
+  wave_lds_sync();
+  {
+    int64_t own = -1;
+    if (a.q_self0 >= 0) {
+      own = (a.q_self0 + rw) / kStep;
+      if (own < seed_steps && ((s_seed[wave][own >> 6] >> (own & 63)) & 1u))
+        visit(own * kStep, (int)min((int64_t)kStep, a.n_c - own * kStep));
+      else
+        own = -1;
+    }
+    for (int wd = 0; wd < (int)((seed_steps + 63) >> 6); ++wd) {
+      uint64_t m = s_seed[wave][wd];
+      m = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(m >> 32)) << 32) |
+          (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)m);
+      while (m) {
+        const int64_t st = ((int64_t)wd << 6) + __builtin_ctzll(m);
+        m &= m - 1;
+        if (st != own) visit(st * kStep, (int)min((int64_t)kStep, a.n_c - st * kStep));
+      }
+    }
+  }
+
   float4 blo, bhi;
   if (n_groups > 0) box_of(t0, blo, bhi);
   for (int64_t tt = 0; tt < n_groups; ++tt) {
@@ -302,7 +376,8 @@ __global__ void __launch_bounds__(64 * kKnnWaves) __attribute__((amdgpu_waves_pe
     // order, the candidate's distance is at least d. A candidate enters only
     // with distance <= the current k-th distance T, so d > T excludes the
     // whole step. (T only decreases, so the test stays valid for the group;
-    // with fewer than k entries T is NaN and nothing is excluded.)
+    // with fewer than k entries T is NaN and nothing is excluded.) Seeds,
+    // already visited, are left out too.
     uint32_t skip;
     {
       float qx = q[0].x, qy = q[0].y, qz = q[0].z, T = __uint_as_float((uint32_t)(q[0].tau >> 32));
@@ -322,12 +397,14 @@ __global__ void __launch_bounds__(64 * kKnnWaves) __attribute__((amdgpu_waves_pe
       }
       const uint64_t far = __ballot(d > T);
       skip = (uint32_t)(far & (far >> 16) & (far >> 32) & (far >> 48) & 0xFFFFull);
+      const int64_t st0 = grp * (kGroup / kStep);  // a multiple of 16: its seeds are 16 bits of one word
+      if (st0 < seed_steps) {
+        const uint64_t sw = s_seed[wave][st0 >> 6];
+        skip |= (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)((sw >> (st0 & 63)) & 0xFFFFull));
+      }
     }
-    const uint32_t index0 = (uint32_t)(a.c_index0 + c0);
-    // steps of 128 candidates, two per lane; entries past n_here take no
-    // part. In the group that holds the wave's own queries the steps start
-    // just before them and wrap around, so their sequence neighbours come
-    // first.
+    // In the group that holds the wave's own queries the steps start just
+    // before them and wrap around, so their sequence neighbours come first.
     const int n_pairs = (n_here + kStep - 1) / kStep;
     int pr = 0;
     if (a.q_self0 >= 0) {
@@ -336,31 +413,7 @@ __global__ void __launch_bounds__(64 * kKnnWaves) __attribute__((amdgpu_waves_pe
     }
     for (int t = 0; t < n_pairs; ++t, pr = pr + 1 == n_pairs ? 0 : pr + 1) {
       if ((skip >> pr) & 1u) continue;
-      const int s = pr << 7;
-      const bool va = s + lane < n_here, vb = s + 64 + lane < n_here;
-      const float4 ca = c4[c0 + (va ? s + lane : 0)], cb = c4[c0 + (vb ? s + 64 + lane : 0)];
-      const float cca = MODE ? norm2(ca) : ca.w, ccb = MODE ? norm2(cb) : cb.w;
-      uint64_t ma[kKnnQ], mb[kKnnQ], any = 0;
-#pragma unroll
-      for (int j = 0; j < kKnnQ; ++j) {
-        const float ea = fmaf(ca.x, q[j].mx, fmaf(ca.y, q[j].my, fmaf(ca.z, q[j].mz, cca)));
-        const float eb = fmaf(cb.x, q[j].mx, fmaf(cb.y, q[j].my, fmaf(cb.z, q[j].mz, ccb)));
-        ma[j] = __ballot(va && !(ea > q[j].lim));
-        mb[j] = __ballot(vb && !(eb > q[j].lim));
-        any |= ma[j] | mb[j];
-      }
-      if (any == 0) continue;
-      // the exact distances and keys decide; a flush lowers tau after the
-      // prefilter, so the masks stay a superset
-#pragma unroll
-      for (int j = 0; j < kKnnQ; ++j) {
-        if (ma[j])
-          q[j].template offer<MODE>(__float_as_uint(dist2(q[j].x, q[j].y, q[j].z, ca)), index0 + s + lane, va,
-                                    __float_as_int(ca.w), lane, k);
-        if (mb[j])
-          q[j].template offer<MODE>(__float_as_uint(dist2(q[j].x, q[j].y, q[j].z, cb)), index0 + s + 64 + lane, vb,
-                                    __float_as_int(cb.w), lane, k);
-      }
+      visit(c0 + pr * kStep, min(kStep, n_here - pr * kStep));
     }
   }
 #pragma unroll
