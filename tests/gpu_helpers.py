@@ -43,13 +43,13 @@ class Device:
     """Device-resident inputs of one workload."""
 
     def __init__(self, wl: synth.Workload, affine: bool = False, mask: Optional[np.ndarray] = "default",
-                 z_override: Optional[np.ndarray] = None):
+                 z_override: Optional[np.ndarray] = None, s_override: Optional[np.ndarray] = None):
         import torch
         self.torch = torch
         self.wl = wl
         self.dev = torch.device("cuda:0")
         self.w_host = synth.weights(wl, affine=affine)
-        self.s_host = synth.s_host(wl)
+        self.s_host = synth.s_host(wl) if s_override is None else np.ascontiguousarray(s_override)
         self.mask_host = synth.mask_host(wl) if isinstance(mask, str) else mask
         self.s = self._to_dev(self.s_host)
         self.w = {k: (None if v is None else torch.from_numpy(np.ascontiguousarray(v)).to(self.dev))
