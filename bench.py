@@ -777,7 +777,8 @@ def attention_main(args, wl):
     synth.device_read(z.data_ptr(), read_bytes, sink.data_ptr(), sp)
     hip.record(e1, sp)
     read_gbps = read_bytes / (hip.elapsed_ms(e0, e1) * 1e-3) / 1e9
-    # the attention kernel's own access pattern over the first stripe, no arithmetic
+    # the attention kernel's own z stream over the first stripe (same grid, loads
+    # and ring), no arithmetic
     pattern_gbps = None
     if wl.bf16 and cz == 128:
         q0, nq = wl.stripes[0]
@@ -787,7 +788,7 @@ def attention_main(args, wl):
         synth.device_read_pattern(zp, n, nq, wl.n_key_blocks, sink.data_ptr(), sp)
         hip.record(e1, sp)
         pattern_gbps = nq * n * cz * wl.elem_bytes / (hip.elapsed_ms(e0, e1) * 1e-3) / 1e9
-    progress(f"streaming read of z: {read_gbps:.0f} GB/s; attention access pattern, no arithmetic: "
+    progress(f"streaming read of z: {read_gbps:.0f} GB/s; the attention's z stream, no arithmetic: "
              f"{pattern_gbps or 0:.0f} GB/s")
 
     progress(f"warmup {args.warmup} steps, timing {args.steps} steps")

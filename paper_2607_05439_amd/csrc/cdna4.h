@@ -82,7 +82,6 @@ __device__ __forceinline__ void transpose_bias(float (&b)[16][4]) {
       for (int i = 0; i < 4; ++i) swap16(b[4 * c + r][i], b[4 * (c + 1) + r][i]);
 }
 
-
 // ---- direct-to-LDS loads and explicit waits
 // The DMA loads below are issued from inline asm, so the compiler neither
 // counts them nor inserts waits for them: every wait on their data is an
@@ -109,18 +108,26 @@ __device__ __forceinline__ void dma_b128(__amdgpu_buffer_rsrc_t r, int voff, uin
       : "memory");
 }
 
-// The same with the non-temporal hint, for data read exactly once (the pair
-// tensor stream), so it does not displace reused data (K/V tiles) in the caches.
-__device__ __forceinline__ void dma_b128_stream(__amdgpu_buffer_rsrc_t r, int voff, uint32_t lds_base) {
+// The four loads of one key of the pair tensor stream, 4 x 1 KB into LDS at
+// lds_base, non-temporal (data read exactly once, so it does not displace the
+// reused K/V tiles in the caches), under one M0: the instruction offset (1024 i
+// for load i) is added to the LDS and to the global address alike, so voff_i
+// is load i's global offset minus 1024 i. Waits for this wave's LDS reads
+// first, like dma_b128.
+__device__ __forceinline__ void dma_key_stream(__amdgpu_buffer_rsrc_t r, int v0, int v1, int v2, int v3,
+                                               uint32_t lds_base) {
   uint32_t saved;
   asm volatile(
       "s_waitcnt lgkmcnt(0)\n\t"
       "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %3\n\t"
-      "buffer_load_dwordx4 %1, %2, 0 offen nt lds\n\t"
+      "s_mov_b32 m0, %6\n\t"
+      "buffer_load_dwordx4 %1, %5, 0 offen nt lds\n\t"
+      "buffer_load_dwordx4 %2, %5, 0 offen offset:1024 nt lds\n\t"
+      "buffer_load_dwordx4 %3, %5, 0 offen offset:2048 nt lds\n\t"
+      "buffer_load_dwordx4 %4, %5, 0 offen offset:3072 nt lds\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
-      : "v"(voff), "s"(r), "s"(lds_base)
+      : "v"(v0), "v"(v1), "v"(v2), "v"(v3), "s"(r), "s"(lds_base)
       : "memory");
 }
 

@@ -225,11 +225,16 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
     zoff[i] = row * row_bytes + 16 * ((lane & 15) ^ row);
   }
   const uint32_t ring_base = lds_addr(&zring[wave][0]);
-  auto z_dma = [&](int64_t j, bool valid, int slot) {
+  // one M0 per key: the instruction offset 1024 i, which moves the LDS and the
+  // global address alike, selects load i's quarter of the slot, so its vector
+  // offset is that of its rows minus 1024 i
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      dma_b128_stream(zres, valid ? zoff[i] + (int)j * (kCz * 2) : kOutOfRange,
-               ring_base + (uint32_t)slot * (uint32_t)sizeof(ZSlot) + 1024u * i);
+  for (int i = 0; i < 4; ++i) zoff[i] -= 1024 * i;
+  auto z_dma = [&](int64_t j, bool valid, int slot) {
+    const int jo = (int)j * (kCz * 2);
+    dma_key_stream(zres, valid ? zoff[0] + jo : kOutOfRange, valid ? zoff[1] + jo : kOutOfRange,
+                   valid ? zoff[2] + jo : kOutOfRange, valid ? zoff[3] + jo : kOutOfRange,
+                   ring_base + (uint32_t)slot * (uint32_t)sizeof(ZSlot));
   };
   // K/V tiles: this wave fetches heads 4*wave .. 4*wave+3.
   const __amdgpu_buffer_rsrc_t kres = __builtin_amdgcn_make_buffer_rsrc(
@@ -297,29 +302,53 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
     const KvTile& cur = kv;
     transpose_bias(b);
 
+    // heads in pairs: two independent QK^T / softmax chains and one vote per
+    // pair on rescaling (a factor of exactly 1 leaves a head unchanged)
+    constexpr int kG = 2;
 #pragma unroll
-    for (int h = 0; h < kH; ++h) {
-      const int ha = h >> 2, hi = h & 3;
-      const f32x4 cin = {b[4 * ha + 0][hi], b[4 * ha + 1][hi], b[4 * ha + 2][hi], b[4 * ha + 3][hi]};
-      const u32x4 kt = cur.k[h][lane];
-      const u32x4 vv = cur.v[h][lane];
-      // x[r]: logit (base 2, + kShift) of row n, key 4g + r
-      const f32x4 x = mfma32(as_bf16x8(kt), qreg[h], cin);
-      const float tmax = max4(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
-      const float mnew = fmaxf(m[h], ceilf(tmax));
-      const float muse = (mnew == -INFINITY) ? 0.0f : mnew;
-      const float alpha = (m[h] == -INFINITY) ? 0.0f : ldexpf(1.0f, (int)(m[h] - muse));
-      bf16x4 p;
+    for (int h0 = 0; h0 < kH; h0 += kG) {
+      f32x4 x[kG];
+      float mnew[kG], muse[kG], alpha[kG];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) p[r] = (__bf16)__builtin_amdgcn_exp2f(x[r] - muse);
-      // the running maximum is an integer and rarely moves, so most tiles skip this
-      if (__any(alpha != 1.0f)) {
-        o[h][0] *= alpha;
-        o[h][1] *= alpha;
+      for (int j = 0; j < kG; ++j) {
+        const int h = h0 + j, ha = h >> 2, hi = h & 3;
+        const f32x4 cin = {b[4 * ha + 0][hi], b[4 * ha + 1][hi], b[4 * ha + 2][hi], b[4 * ha + 3][hi]};
+        const u32x4 kt = cur.k[h][lane];
+        // x[r]: logit (base 2, + kShift) of row n, key 4g + r
+        x[j] = mfma32(as_bf16x8(kt), qreg[h], cin);
       }
-      o[h][0] = mfma16(as_bf16x4(u32x2{vv[0], vv[1]}), p, o[h][0]);
-      o[h][1] = mfma16(as_bf16x4(u32x2{vv[2], vv[3]}), p, o[h][1]);
-      m[h] = mnew;
+#pragma unroll
+      for (int j = 0; j < kG; ++j) {
+        const int h = h0 + j;
+        const float tmax = max4(fmaxf(fmaxf(x[j][0], x[j][1]), fmaxf(x[j][2], x[j][3])));
+        mnew[j] = fmaxf(m[h], ceilf(tmax));
+        muse[j] = (mnew[j] == -INFINITY) ? 0.0f : mnew[j];
+        alpha[j] = (m[h] == -INFINITY) ? 0.0f : ldexpf(1.0f, (int)(m[h] - muse[j]));
+      }
+      bf16x4 p[kG];
+#pragma unroll
+      for (int j = 0; j < kG; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) p[j][r] = (__bf16)__builtin_amdgcn_exp2f(x[j][r] - muse[j]);
+      // the running maximum is an integer and rarely moves, so most pairs skip this
+      bool mv = false;
+#pragma unroll
+      for (int j = 0; j < kG; ++j) mv = mv || alpha[j] != 1.0f;
+      if (__any(mv)) {
+#pragma unroll
+        for (int j = 0; j < kG; ++j) {
+          o[h0 + j][0] *= alpha[j];
+          o[h0 + j][1] *= alpha[j];
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < kG; ++j) {
+        const int h = h0 + j;
+        const u32x4 vv = cur.v[h][lane];
+        o[h][0] = mfma16(as_bf16x4(u32x2{vv[0], vv[1]}), p[j], o[h][0]);
+        o[h][1] = mfma16(as_bf16x4(u32x2{vv[2], vv[3]}), p[j], o[h][1]);
+        m[h] = mnew[j];
+      }
     }
     // every wave is done with K/V tile t: load tile t+1 into the same buffer
     barrier_lds();

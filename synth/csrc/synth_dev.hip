@@ -112,28 +112,68 @@ __global__ void __launch_bounds__(256) read_kernel(const uint4* __restrict__ src
   if (acc == 0x9E3779B9u) sink[0] = acc;  // practically never taken; keeps the loads
 }
 
-// Reads 256-byte pair vectors of rows [0, n_rows) in the fused attention
-// kernel's visiting order (a wave walks 16 rows key by key, 16 rows x 64 B per
-// load; workgroups of 4 waves; key ranges split into n_parts), with no
-// arithmetic, non-temporal like the kernel's stream: the memory system's
-// ceiling for that access pattern.
-__global__ void __launch_bounds__(256) read_pattern_kernel(const uint4* __restrict__ z, int64_t n_tok, int64_t n_rows,
-                                                           int n_parts, uint32_t* __restrict__ sink) {
+// Reads 256-byte pair vectors of rows [0, n_rows) the way the fused attention
+// kernel streams them, with no arithmetic: the memory system's ceiling for that
+// stream. Same geometry and instructions: workgroups of 4 waves, each wave 16
+// rows over one of n_parts key ranges, one workgroup per CU (160 KB of LDS),
+// every key fetched as four non-temporal direct-to-LDS loads of 4 rows x 256 B
+// under one M0 into an 8-slot ring per wave, issued 7 keys ahead; each key is
+// read back from LDS once (folded into a word so the reads stay live).
+constexpr int kPatRing = 8;
+constexpr int kPatAhead = kPatRing - 1;
+
+__device__ __forceinline__ void pattern_key_loads(__amdgpu_buffer_rsrc_t r, int v0, int v1, int v2, int v3,
+                                                  uint32_t lds_base) {
+  uint32_t saved;
+  asm volatile(
+      "s_waitcnt lgkmcnt(0)\n\t"
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %6\n\t"
+      "buffer_load_dwordx4 %1, %5, 0 offen nt lds\n\t"
+      "buffer_load_dwordx4 %2, %5, 0 offen offset:1024 nt lds\n\t"
+      "buffer_load_dwordx4 %3, %5, 0 offen offset:2048 nt lds\n\t"
+      "buffer_load_dwordx4 %4, %5, 0 offen offset:3072 nt lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(v0), "v"(v1), "v"(v2), "v"(v3), "s"(r), "s"(lds_base)
+      : "memory");
+}
+
+__global__ void __launch_bounds__(256, 1) read_pattern_kernel(const uint16_t* __restrict__ z, int64_t n_tok,
+                                                              int64_t n_rows, int n_parts, uint32_t* __restrict__ sink) {
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __shared__ u32x4 ring[4][kPatRing][256];    // 128 KB: 4 KB per key and wave
+  __shared__ uint32_t fill[32 * 256 - 16];    // the rest of the CU's LDS
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int64_t r0 = ((int64_t)blockIdx.x * 4 + wave) * 16;
-  if (r0 + 16 > n_rows) return;  // whole 16-row tiles only
+  if (r0 + 16 > n_rows) return;  // whole 16-row tiles only; no barriers below
   const int64_t q = n_tok / n_parts, rem = n_tok % n_parts, p = blockIdx.y;
   const int64_t k0 = p * q + (p < rem ? p : rem), k1 = k0 + q + (p < rem ? 1 : 0);
-  const u32x4* base = reinterpret_cast<const u32x4*>(z) + r0 * n_tok * 16;
+  const int row_bytes = (int)(n_tok * 256);
+  const __amdgpu_buffer_rsrc_t zres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(z) + r0 * n_tok * 128, 0, 16 * row_bytes, 0x00020000);
+  int off[4];  // load i: rows 4i + lane/16, 16-byte chunk lane%16, minus the instruction offset
+#pragma unroll
+  for (int i = 0; i < 4; ++i) off[i] = (4 * i + (lane >> 4)) * row_bytes + 16 * (lane & 15) - 1024 * i;
+  const uint32_t base = (uint32_t)reinterpret_cast<uintptr_t>(&ring[wave][0][0]);
+  auto issue = [&](int64_t j) {
+    const bool in = j < k1;
+    const int jo = (int)j * 256;
+    const int none = 0x7FFFFF00;  // past every record: moves no data
+    pattern_key_loads(zres, in ? off[0] + jo : none, in ? off[1] + jo : none, in ? off[2] + jo : none,
+                      in ? off[3] + jo : none, base + (uint32_t)(j % kPatRing) * 4096u);
+  };
+  for (int a = 0; a < kPatAhead; ++a) issue(k0 + a);
   u32x4 acc = {0u, 0u, 0u, 0u};
   for (int64_t j = k0; j < k1; ++j) {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(4 * (kPatAhead - 1)) : "memory");
+    const u32x4* slot = &ring[wave][j % kPatRing][0];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int idx = i * 64 + lane;  // row idx / 16 of the tile, 16-byte chunk idx % 16
-      acc ^= __builtin_nontemporal_load(base + ((int64_t)(idx >> 4) * n_tok + j) * 16 + (idx & 15));
-    }
+    for (int i = 0; i < 4; ++i) acc ^= slot[64 * i + lane];
+    issue(j + kPatAhead);
   }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if (n_parts < 0) fill[threadIdx.x] = acc.x;  // never: keeps the LDS reservation
   if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9E3779B9u) sink[0] = 1;
 }
 
@@ -205,8 +245,9 @@ int synth_dev_copy(const void* src, void* dst, int64_t bytes, void* stream) {
 
 int synth_dev_read_pattern(const void* z, int64_t n_tok, int64_t n_rows, int32_t n_parts, void* sink, void* stream) {
   if (!z || !sink || n_tok <= 0 || n_rows <= 0 || n_parts < 1 || n_parts > n_tok) return -1;
+  if (n_tok * 256 * 16 + 4096 > INT32_MAX) return -1;  // 32-bit buffer offsets of 16 rows
   hipLaunchKernelGGL(read_pattern_kernel, dim3((unsigned)((n_rows + 63) / 64), (unsigned)n_parts), dim3(256), 0,
-                     (hipStream_t)stream, (const uint4*)z, n_tok, n_rows, n_parts, (uint32_t*)sink);
+                     (hipStream_t)stream, (const uint16_t*)z, n_tok, n_rows, n_parts, (uint32_t*)sink);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
