@@ -779,7 +779,7 @@ def attention_main(args, wl):
     read_gbps = read_bytes / (hip.elapsed_ms(e0, e1) * 1e-3) / 1e9
     # the attention kernel's own z stream over the first stripe (same grid, loads
     # and ring), no arithmetic
-    pattern_gbps = None
+    pattern_gbps = pattern_ms = None
     if wl.bf16 and cz == 128:
         q0, nq = wl.stripes[0]
         zp = z.data_ptr() + q0 * n * cz * wl.elem_bytes
@@ -787,7 +787,8 @@ def attention_main(args, wl):
         hip.record(e0, sp)
         synth.device_read_pattern(zp, n, nq, wl.n_key_blocks, sink.data_ptr(), sp)
         hip.record(e1, sp)
-        pattern_gbps = nq * n * cz * wl.elem_bytes / (hip.elapsed_ms(e0, e1) * 1e-3) / 1e9
+        pattern_ms = hip.elapsed_ms(e0, e1)
+        pattern_gbps = nq * n * cz * wl.elem_bytes / (pattern_ms * 1e-3) / 1e9
     progress(f"streaming read of z: {read_gbps:.0f} GB/s; the attention's z stream, no arithmetic: "
              f"{pattern_gbps or 0:.0f} GB/s")
 
@@ -921,7 +922,11 @@ def attention_main(args, wl):
         "per_tile_ms": round(avg_kernel_ms / wl.n_key_blocks, 4),
         "bias_project_stripe": bias_ref,
         "streaming_read_GBps": round(read_gbps, 1),
+        # the kernel's own z stream over the first stripe (same grid, loads and
+        # ring, all keys) with no arithmetic, and its time over the kernel's
         "pattern_read_GBps": None if pattern_gbps is None else round(pattern_gbps, 1),
+        "pattern_ms": None if pattern_ms is None else round(pattern_ms, 4),
+        "pattern_ms_over_kernel_ms": None if pattern_ms is None else round(pattern_ms / avg_kernel_ms, 4),
         "other_configs": extras,
         "cpu_baseline": cpu,
     }
