@@ -73,10 +73,16 @@ class Hip:
 
 
 def kernel_source_sha(sources=KERNEL_SOURCES):
+    """Hash of the kernel's sources and of the compiler flags each .hip among
+    them is built with (a flag changes the code as much as an edit does)."""
+    from paper_2607_05439_amd import build as dcp_build
     h = hashlib.sha256()
     for p in sources:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
+        if p.endswith(".hip"):
+            name = os.path.basename(p)
+            h.update(" ".join([*dcp_build.FLAGS, *dcp_build.EXTRA.get(name, [])]).replace(ROOT, "").encode())
     return h.hexdigest()[:16]
 
 
