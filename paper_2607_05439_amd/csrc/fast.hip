@@ -1,6 +1,6 @@
 // Fused bf16 path for c_z = 128, H = 16, d = 24 on gfx950 (CDNA4).
 //
-// Two kernels (the q, k, v, g projections that feed them are in proj.hip):
+// Kernels (the q, k, v, g projections that feed them are in proj.hip):
 //   attn_kernel  the hot loop: one wave owns 16 query rows and one key range
 //                (a ring step of the paper's 2D scheme, or a slice of one). Per
 //                key it reads the 16 rows' pair vectors z[i, j, :] once from
@@ -8,7 +8,10 @@
 //                projection on the matrix cores, then per 16-key tile runs
 //                QK^T and PV on the matrix cores with an fp32 online softmax.
 //                It writes one partial state (m, l, acc) per (row, head).
-//   bias_kernel  the pair bias alone, materialised (dcp_bias_project).
+//   bias_ring_kernel  the pair bias alone, materialised (dcp_bias_project):
+//                the same z stream, one column per step, whole-line stores
+//                (bias_kernel, with z loaded straight into registers, serves
+//                row strides too long for 32-bit offsets).
 //
 // Matrix-core operand layouts (v_mfma_f32_16x16x32_bf16, 64 lanes, lane L,
 // n = L % 16, g = L / 16): A holds row n with k-slots 8g..8g+7, B holds
@@ -377,17 +380,8 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
 }
 
 // ----------------------------------------------------------------------------- bias only
-// grid (tiles of 16 rows, column chunks); each wave walks its columns.
-__global__ void __launch_bounds__(64) bias_kernel(FastBiasArgs a) {
-  const int lane = threadIdx.x, n = lane & 15, g = lane >> 4;
-  const int64_t r0 = (int64_t)blockIdx.x * 16;
-  const int64_t c_begin = (int64_t)blockIdx.y * a.cols_per_wave;
-  const int64_t c_end = min(c_begin + (int64_t)a.cols_per_wave, a.n_cols);
-  bf16x8 whi[4], wlo[4];
-  bias_weights(a.w_b, a.gamma, 1.0f, lane, whi, wlo);
-  const f32x4 wsum = bias_weight_sums(whi, wlo);
-  // per-head constant sum_c W_b[h,c] beta_c + b_b[h] for heads 4g..4g+3
-  float cst[4];
+// Per-head constant sum_c W_b[h,c] beta_c + b_b[h] for heads 4g..4g+3.
+__device__ __forceinline__ void bias_constants(const FastBiasArgs& a, int g, float (&cst)[4]) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int h = 4 * g + i;
@@ -396,6 +390,112 @@ __global__ void __launch_bounds__(64) bias_kernel(FastBiasArgs a) {
       for (int c = 0; c < kCz; ++c) c0 = fmaf(a.w_b[h * kCz + c], a.beta[c], c0);
     cst[i] = c0;
   }
+}
+
+constexpr int kBiasRing = 8;               // z slots per wave: 128 KB per workgroup, one per CU
+constexpr int kBiasAhead = kBiasRing - 1;  // columns of z in flight ahead of the one being used
+
+// grid (groups of 64 rows, column chunks of an even length); 4 waves of 16
+// rows. Each wave streams its rows' z through an LDS ring by direct-to-LDS
+// loads, 4 rows x 256 B per load (the pair tensor's fast read pattern), and
+// computes the bias of one column per step on the matrix cores. Every two
+// columns the results are regrouped across lanes so that each non-temporal
+// store writes 8 rows x one whole 128-byte line (a row's two columns); half
+// lines written by separate streaming stores would each go to memory alone.
+__global__ void __launch_bounds__(64 * kWaves, 1) bias_ring_kernel(FastBiasArgs a) {
+  __shared__ ZSlot ring[kWaves][kBiasRing];
+  const int tid = threadIdx.x, lane = tid & 63, n = lane & 15, g = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t r0 = ((int64_t)blockIdx.x * kWaves + wave) * 16;
+  if (r0 >= a.n_rows) return;  // whole wave; nothing below synchronises waves
+  const int64_t c_begin = (int64_t)blockIdx.y * a.cols_per_wave;
+  const int64_t c_end = min(c_begin + (int64_t)a.cols_per_wave, a.n_cols);
+  bf16x8 whi[4], wlo[4];
+  bias_weights(a.w_b, a.gamma, 1.0f, lane, whi, wlo);
+  const f32x4 wsum = bias_weight_sums(whi, wlo);
+  float cst[4];
+  bias_constants(a, g, cst);
+
+  // rows r0 .. r0+15 (those past n_rows fall outside the record range: no data)
+  const int64_t rows_here = min((int64_t)16, a.n_rows - r0);
+  const int row_bytes = (int)(a.row_stride * 2);
+  const __amdgpu_buffer_rsrc_t zres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.z) + r0 * a.row_stride, 0, (int)((rows_here - 1) * row_bytes + a.n_cols * (kCz * 2)),
+      kRawBufferFlags);
+  // load i of a column fills slot rows 4i..4i+3 (lane L: row 4i + L/16, chunk
+  // (L%16) ^ row); the instruction offset 1024 i selects the slot quarter
+  int zoff[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 4 * i + (lane >> 4);
+    zoff[i] = row * row_bytes + 16 * ((lane & 15) ^ row) - 1024 * i;
+  }
+  const uint32_t ring_base = lds_addr(&ring[wave][0]);
+  auto z_dma = [&](int64_t c) {
+    const bool valid = c < c_end;
+    const int jo = (int)c * (kCz * 2);
+    dma_key_stream(zres, valid ? zoff[0] + jo : kOutOfRange, valid ? zoff[1] + jo : kOutOfRange,
+                   valid ? zoff[2] + jo : kOutOfRange, valid ? zoff[3] + jo : kOutOfRange,
+                   ring_base + (uint32_t)((c - c_begin) & (kBiasRing - 1)) * (uint32_t)sizeof(ZSlot));
+  };
+#pragma unroll
+  for (int p = 0; p < kBiasAhead; ++p) z_dma(c_begin + p);
+
+  // store lane L of store q: row 8q + L/8, bytes 16 (L%8) of the row's 128
+  // bytes for columns c0, c0+1, i.e. head chunk (L%8)%4 of column c0 + (L%8)/4,
+  // held by lane (row, group (L%8)%4)
+  const int orow = lane >> 3, ochunk = lane & 7;
+  for (int64_t c0 = c_begin; c0 < c_end; c0 += 2) {
+    float o[2][4];  // o[k][i]: column c0 + k, head 4g + i
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int64_t c = c0 + k;
+      // column c has landed: the loads issued after it are the next kBiasAhead - 1
+      // columns (loads complete in issue order; stores in between only make this stricter)
+      wait_vm<4 * (kBiasAhead - 1)>();
+      const ZSlot& zs = ring[wave][(c - c_begin) & (kBiasRing - 1)];
+      u32x4 zb[4];
+#pragma unroll
+      for (int st = 0; st < 4; ++st) zb[st] = zs.c[n][(4 * st + g) ^ n];
+      f32x4 acc;
+      float rstd;
+      pair_bias(zb, whi, wlo, wsum, a.eps, n, acc, rstd);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[k][i] = fmaf(acc[i], rstd, cst[i]);
+      z_dma(c + kBiasAhead);  // into column c-1's slot (the wait inside covers this step's reads too)
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int src = (8 * q + orow) + 16 * (ochunk & 3);
+      f32x4 v;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float lo = __int_as_float(__builtin_amdgcn_ds_bpermute(4 * src, __float_as_int(o[0][i])));
+        const float hi = __int_as_float(__builtin_amdgcn_ds_bpermute(4 * src, __float_as_int(o[1][i])));
+        v[i] = ochunk < 4 ? lo : hi;
+      }
+      const int64_t orw = r0 + 8 * q + orow;
+      const int64_t oc = c0 + (ochunk >> 2);
+      if (orw < a.n_rows && oc < c_end)
+        __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(a.out + (orw * a.n_cols + oc) * kH + 4 * (ochunk & 3)));
+    }
+  }
+  wait_vm<0>();  // the look-ahead loads past the chunk (no data) before exit
+}
+
+// The same for row strides too long for 32-bit buffer offsets over 16 rows:
+// grid (tiles of 16 rows, column chunks); one wave each, z loaded straight into
+// the operand registers.
+__global__ void __launch_bounds__(64) bias_kernel(FastBiasArgs a) {
+  const int lane = threadIdx.x, n = lane & 15, g = lane >> 4;
+  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  const int64_t c_begin = (int64_t)blockIdx.y * a.cols_per_wave;
+  const int64_t c_end = min(c_begin + (int64_t)a.cols_per_wave, a.n_cols);
+  bf16x8 whi[4], wlo[4];
+  bias_weights(a.w_b, a.gamma, 1.0f, lane, whi, wlo);
+  const f32x4 wsum = bias_weight_sums(whi, wlo);
+  float cst[4];
+  bias_constants(a, g, cst);
   const int64_t row = r0 + n;
   const int64_t rr = min(row, a.n_rows - 1);
   const u32x4* zrow = reinterpret_cast<const u32x4*>(a.z + rr * a.row_stride) + g;
@@ -440,6 +540,20 @@ hipError_t launch_fast_attn(const FastAttnArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_fast_bias(const FastBiasArgs& a, hipStream_t st) {
+  // 16 rows of the tile must be addressable with 32-bit offsets (plus one slot quarter)
+  if ((int64_t)16 * a.row_stride * 2 + 4096 <= INT32_MAX) {
+    FastBiasArgs b = a;
+    const int64_t groups = (a.n_rows + 16 * kWaves - 1) / (16 * kWaves);
+    // about 1024 workgroups (four rounds of one per CU), at least 16 columns each
+    int64_t chunks = (1024 + groups - 1) / groups;
+    chunks = max((int64_t)1, min(chunks, (a.n_cols + 15) / 16));
+    int64_t per = (a.n_cols + chunks - 1) / chunks;
+    per += per & 1;  // even: column pairs start on 128-byte lines when n_cols is even
+    b.cols_per_wave = (int32_t)per;
+    const int64_t ct = (a.n_cols + per - 1) / per;
+    hipLaunchKernelGGL(bias_ring_kernel, dim3((unsigned)groups, (unsigned)ct), dim3(64 * kWaves), 0, st, b);
+    return hipGetLastError();
+  }
   const int64_t rt = (a.n_rows + 15) / 16;
   const int64_t ct = (a.n_cols + a.cols_per_wave - 1) / a.cols_per_wave;
   hipLaunchKernelGGL(bias_kernel, dim3((unsigned)rt, (unsigned)ct), dim3(64), 0, st, a);

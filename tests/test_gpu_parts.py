@@ -36,13 +36,13 @@ def test_bias_project(torch_cuda, dtype, c_z, h, tol):
 
 
 def test_bias_project_column_chunks(torch_cuda):
-    """The fused bias kernel walks 64 columns per wave, two at a time: several
-    chunks and an odd last chunk (131 = 64 + 64 + 3 columns)."""
+    """The fused bias kernel: workgroups of 64 rows (here one full group and a
+    partial one) over column chunks (131 columns: 9 chunks, a short last one)."""
     import paper_2607_05439_amd as dcp
-    log("case bias_project bf16 c_z=128 H=16, 131 columns")
+    log("case bias_project bf16 c_z=128 H=16, 75 rows x 131 columns")
     wl = workload(n_tok=200, c_z=128, n_heads=16, head_dim=24, c_s=384, dtype="bf16")
     d = Device(wl, affine=True)
-    r0, c0, nr, nc = 7, 60, 21, 131
+    r0, c0, nr, nc = 7, 60, 75, 131
     tile = d.z[r0:r0 + nr, c0:c0 + nc]
     out = torch_cuda.empty((nr, nc, 16), dtype=torch_cuda.float32, device="cuda")
     dcp.dcp_bias_project(d.shape(), d.weights(), tile.data_ptr(), nr, nc, wl.n_tok * 128, out)
@@ -52,6 +52,28 @@ def test_bias_project_column_chunks(torch_cuda):
     err = rel_err(out.cpu().numpy(), ref)
     log(f"  rel err {err:.3e}")
     assert err <= 1e-4
+
+
+def test_bias_project_long_row_stride(torch_cuda):
+    """Row strides too long for 32-bit offsets over 16 rows take the
+    register-load kernel; it gives the same bits as the LDS-ring kernel on the
+    same pairs (17 rows 2^26 elements apart: a 2.3 GB allocation)."""
+    import paper_2607_05439_amd as dcp
+    log("case bias_project bf16, row stride 2^26 elements (fallback kernel) vs contiguous")
+    wl = workload(n_tok=40, c_z=128, n_heads=16, head_dim=24, c_s=384, dtype="bf16")
+    d = Device(wl, affine=True)
+    nr, nc = 17, 40
+    stride = 1 << 26
+    big = torch_cuda.empty(nr * stride, dtype=torch_cuda.bfloat16, device="cuda")
+    rows = big.view(nr, stride)[:, :nc * 128]
+    rows.copy_(d.z[:nr].reshape(nr, nc * 128))
+    got = torch_cuda.empty((nr, nc, 16), dtype=torch_cuda.float32, device="cuda")
+    ref = torch_cuda.empty((nr, nc, 16), dtype=torch_cuda.float32, device="cuda")
+    dcp.dcp_bias_project(d.shape(), d.weights(), big.data_ptr(), nr, nc, stride, got)
+    dcp.dcp_bias_project(d.shape(), d.weights(), d.z.data_ptr(), nr, nc, nc * 128, ref)
+    torch_cuda.cuda.synchronize()
+    del big, rows
+    assert torch_cuda.equal(got, ref)
 
 
 @pytest.mark.parametrize("D", [6, 8, 24])
