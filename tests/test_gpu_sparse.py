@@ -109,6 +109,34 @@ def test_edge_neighbour_lists(tiny):
     assert err <= 1e-5
 
 
+def test_edge_neighbour_lists_bf16():
+    """Edge lists on the bf16 path: empty, out-of-range and negative slots,
+    one atom in every slot, heavy repeats, 16 consecutive query atoms without
+    neighbours, two queries with the same list, every neighbour listed twice."""
+    import torch
+    wl = atom_workload("atoms5000_bf16", n_q=40, q_row0=300)
+    d = AtomDevice(wl, affine=True)
+    nb = d.nbr_host.copy()
+    nb[0, :] = -1
+    nb[1, :] = wl.n_atoms + 5
+    nb[2, :] = 17
+    nb[3, 5:] = -1
+    nb[4, :] = np.arange(wl.k) % 3
+    nb[5, :] = -1
+    nb[5, 0] = wl.n_atoms - 1
+    nb[6, ::2] = -7
+    nb[16:32, :] = -1
+    nb[33, :] = nb[34, :]
+    nb[35, wl.k // 2:] = nb[35, :wl.k // 2]
+    log(f"case atoms5000_bf16 edge lists, k={wl.k}, rows 300..339")
+    ref = d.oracle_rows(np.arange(wl.n_q), nbr=nb)
+    got = d.attention(4, nbr=torch.from_numpy(nb).to(d.dev)).cpu().numpy()
+    assert np.all(got[0] == 0) and np.all(got[1] == 0) and np.all(got[16:32] == 0)
+    err = rel_err(got, ref)
+    log(f"  edge lists rel err {err:.3e}")
+    assert err <= 1e-2
+
+
 @pytest.mark.parametrize("k", [1, 63, 100, 256])
 def test_slot_counts(k):
     """Budgets that are not a multiple of 64, a single slot, and the 256-slot
