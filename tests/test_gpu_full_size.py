@@ -45,3 +45,25 @@ def test_asm24000_blocked_and_deterministic(big):
     assert err <= 1e-6
     # padding (masked) query rows still produce outputs; masked keys are never used
     assert torch.isfinite(a).all()
+
+
+@pytest.mark.parametrize("r0", [0, 11990, 23980])
+def test_asm24000_bias_project_full_rows(big, r0):
+    """dcp_bias_project over whole rows of the 147 GB tensor (all 24000 columns,
+    the last rows masked padding tokens, which the bias does not skip) against
+    the oracle."""
+    import torch
+    import oracle
+    import paper_2607_05439_amd as dcp
+    import synth
+    wl = big.wl
+    nr, nc = 20, wl.n_tok
+    log(f"case asm24000_bf16 bias_project rows {r0}..{r0 + nr - 1} x {nc} columns")
+    out = torch.empty((nr, nc, wl.n_heads), dtype=torch.float32, device="cuda")
+    dcp.dcp_bias_project(big.shape(), big.weights(), big.z[r0].data_ptr(), nr, nc, nc * wl.c_z, out)
+    z_host = synth.z_host(wl, range(r0, r0 + nr))
+    w = big.w_host
+    ref = oracle.bias(np.ascontiguousarray(z_host), w["w_b"], w["b_b"], w["ln_gamma"], w["ln_beta"], 1e-5)
+    err = rel_err(out.cpu().numpy(), ref)
+    log(f"  rel err {err:.3e}")
+    assert err <= 1e-4
