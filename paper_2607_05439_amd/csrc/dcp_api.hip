@@ -192,8 +192,8 @@ static int run_attention(const dcp_shape* shape, const dcp_weights* w, const voi
                (part->gate && !aligned(part->gate, 4))))
     return fail(DCP_ERR_INVALID_ARGUMENT, "m_out, l_out, acc_out and gate_out must be 4-byte aligned");
   if (path == kPathFast && (!aligned(w->w_q, 16) || !aligned(w->w_k, 16) || !aligned(w->w_v, 16) ||
-                            !aligned(w->w_g, 16)))
-    return fail(DCP_ERR_INVALID_ARGUMENT, "w_q, w_k, w_v and w_g must be 16-byte aligned");
+                            !aligned(w->w_g, 16) || !aligned(w->w_b, 16) || !aligned(w->ln_gamma, 16)))
+    return fail(DCP_ERR_INVALID_ARGUMENT, "w_q, w_k, w_v, w_g, w_b and ln_gamma must be 16-byte aligned");
   Layout L;
   make_layout(shape, path, n_q, n_key_blocks, &L);
   // a key range shorter than N: its own segment count, never more parts than
@@ -485,6 +485,8 @@ int dcp_bias_project(const dcp_shape* shape, const dcp_weights* w, const void* z
   if (fast) {
     if (!aligned(z_tile, 16) || !aligned(bias_out, 16) || row_stride_elems % 8 != 0)
       return fail(DCP_ERR_INVALID_ARGUMENT, "z_tile and bias_out must be 16-byte aligned, row_stride_elems a multiple of 8");
+    if (!aligned(w->w_b, 16) || !aligned(w->ln_gamma, 16))
+      return fail(DCP_ERR_INVALID_ARGUMENT, "w_b and ln_gamma must be 16-byte aligned");
     dcp::FastBiasArgs a{};
     a.z = static_cast<const uint16_t*>(z_tile);
     a.w_b = w->w_b;

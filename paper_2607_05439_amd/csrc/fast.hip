@@ -46,17 +46,36 @@ constexpr float kShift = kFastShift;
 // (subtracting its mean over channels makes sum_c W''_hc z_c = sum_c W'_hc
 // (z_c - mean z)), then split into bf16 hi + lo so the pair carries about 16
 // significant bits.
+// w_b and gamma are 16-byte aligned (checked on the host): each lane reads its
+// 8 consecutive channels per k-step as two 16-byte loads, and the absence of
+// gamma is one wave-uniform branch, not one per element.
 __device__ void bias_weights(const float* __restrict__ w_b, const float* __restrict__ gamma, float scale, int lane,
                              bf16x8 (&hi)[4], bf16x8 (&lo)[4]) {
   const int h = lane & 15, g = lane >> 4;
   float w[4][8];
+  const float4* wr = reinterpret_cast<const float4*>(w_b + h * kCz + 8 * g);  // channel 32 s + 8 g + i: float4 8 s + i / 4
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const float4 a = wr[8 * s], b = wr[8 * s + 1];
+    w[s][0] = a.x, w[s][1] = a.y, w[s][2] = a.z, w[s][3] = a.w;
+    w[s][4] = b.x, w[s][5] = b.y, w[s][6] = b.z, w[s][7] = b.w;
+  }
+  if (gamma) {
+    const float4* gr = reinterpret_cast<const float4*>(gamma + 8 * g);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const float4 a = gr[8 * s], b = gr[8 * s + 1];
+      const float gm[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+      for (int i = 0; i < 8; ++i) w[s][i] *= gm[i];
+    }
+  }
   float rs = 0.f;
 #pragma unroll
   for (int s = 0; s < 4; ++s)
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int c = 32 * s + 8 * g + i;
-      w[s][i] = w_b[h * kCz + c] * (gamma ? gamma[c] : 1.0f) * scale;
+      w[s][i] *= scale;
       rs += w[s][i];
     }
   const float mean = sum4(rs) * (1.0f / kCz);

@@ -110,6 +110,10 @@ def test_bad_ranges():
     assert attention(sh, z=FAKE + 2) == E  # misaligned
     w = dcp.make_weights(FAKE, FAKE, 0, FAKE, FAKE)
     assert attention(sh, w=w) == E
+    # the fused path reads w_b and ln_gamma with 16-byte loads
+    assert attention(sh, w=dcp.make_weights(FAKE, FAKE, FAKE, FAKE, FAKE + 4)) == E
+    assert "w_b" in dcp.dcp_last_error()
+    assert attention(sh, w=dcp.make_weights(FAKE, FAKE, FAKE, FAKE, FAKE, ln_gamma=FAKE + 8)) == E
     assert dcp.lib().dcp_pair_bias_attention(None, ctypes.byref(weights()), FAKE, FAKE, None, 0, 1, 1, FAKE, FAKE,
                                              1 << 40, None) == E
 
@@ -157,6 +161,8 @@ def test_bias_project_rejections():
     assert L.dcp_bias_project(ctypes.byref(sh), ctypes.byref(w), 0, 4, 8, 1024, FAKE, None) == E
     assert L.dcp_bias_project(ctypes.byref(sh), ctypes.byref(w), FAKE, -1, 8, 1024, FAKE, None) == E
     assert L.dcp_bias_project(ctypes.byref(sh), ctypes.byref(w), FAKE, 0, 8, 1024, FAKE, None) == dcp.DCP_OK
+    for wb in (dcp.make_weights(FAKE, FAKE, FAKE, FAKE, FAKE + 4), dcp.make_weights(0, 0, 0, 0, FAKE, ln_gamma=FAKE + 4)):
+        assert L.dcp_bias_project(ctypes.byref(sh), ctypes.byref(wb), FAKE, 4, 8, 1024, FAKE, None) == E
     bad = shape(c_z=1000)
     assert L.dcp_bias_project(ctypes.byref(bad), ctypes.byref(w), FAKE, 4, 8, 8000, FAKE, None) == \
         dcp.DCP_ERR_UNSUPPORTED
