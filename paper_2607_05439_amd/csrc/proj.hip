@@ -23,7 +23,8 @@
 //   proj_kernel        the products. The 384 outputs of a projection are 24
 //                      tiles of 16 with no padding (a tile may hold the end
 //                      of one head and the start of the next); each wave
-//                      takes two tiles over 128 tokens.
+//                      takes two tiles over 128 tokens (64 or 32 on small
+//                      layers, so that the launch still fills the chip).
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -39,12 +40,10 @@ constexpr int kHD = kH * kD;         // 384 outputs per projection
 constexpr int kOutTiles = kHD / 16;  // 24 output tiles per projection
 constexpr float kLog2e = 1.44269504088896340736f;
 
-constexpr int kProjTiles = 8;                                   // 16-token tiles per workgroup (128 tokens)
 constexpr int kProjWaves = 8;                                   // waves per workgroup, two output tiles each
 constexpr int kProjSideWgs = 2 * kOutTiles / (2 * kProjWaves);  // workgroups per token group and side (3)
 constexpr int kProjChunk = 64;                                  // s channels staged in LDS at a time (2 k-steps)
 constexpr int kProjRowChunks = kProjChunk / 8;                  // 16-byte chunks per staged row
-constexpr int kProjStage = kProjTiles * 16 * kProjRowChunks / (64 * kProjWaves);  // LDS copies per wave per chunk
 
 // byte offset of the split weights of projection p, output tile j, k-step s
 __device__ __forceinline__ int split_offset(int p, int j, int s, int n_ks) {
@@ -76,7 +75,8 @@ __global__ void __launch_bounds__(256) proj_split_kernel(FastProjArgs a) {
   *reinterpret_cast<bf16x4*>(dst + 1024) = lo;
 }
 
-// One workgroup = 128 tokens x one side (query: q and g of the stripe's rows;
+// One workgroup = TILES x 16 tokens (128 when TILES = 8; fewer tiles per
+// workgroup, and so more workgroups, when the token count is small) x one side (query: q and g of the stripe's rows;
 // key: k and v of all tokens) x 16 of the side's 48 output tiles; wave w of
 // workgroup b takes tiles 2 (8 b + w) and the next, of the side's first
 // projection for 8 b + w < 12, else its second. The group's s rows are staged
@@ -85,12 +85,16 @@ __global__ void __launch_bounds__(256) proj_split_kernel(FastProjArgs a) {
 // operands from LDS (16-byte chunks of a row XOR-swizzled by row / 2, so the
 // 16 rows of one operand read cover all banks once). Per 32-channel k-step a
 // wave loads its two tiles' split weights (one k-step ahead) and applies them
-// to the 8 token tiles: 32 products per 4 KB of weights. The three workgroups
+// to the TILES token tiles: 4 TILES products per 4 KB of weights. The three workgroups
 // of a (side, token group) run on the same XCD (dispatch gives workgroup i to
 // XCD i % 8), which then fetches the group's s rows once into its L2. Every
 // accumulator holds [output][token]; v's tiles are transposed at the end.
+template <int TILES>
 __global__ void __launch_bounds__(64 * kProjWaves) __attribute__((amdgpu_waves_per_eu(4))) proj_kernel(FastProjArgs a) {
-  __shared__ __attribute__((aligned(16))) u32x4 s_s[2][kProjTiles * 16][kProjRowChunks];  // 2 x 16 KB
+  constexpr int kProjTiles = TILES;                           // 16-token tiles per workgroup
+  constexpr int kBlocks = kProjTiles * 2;                     // blocks of 8 staged rows
+  constexpr int kProjStage = (kBlocks + kProjWaves - 1) / kProjWaves;  // LDS copies per wave per chunk
+  __shared__ __attribute__((aligned(16))) u32x4 s_s[2][kProjTiles * 16][kProjRowChunks];  // 2 x 2 TILES KB
   const int tid = threadIdx.x, lane = tid & 63, n = lane & 15, g = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
@@ -109,8 +113,8 @@ __global__ void __launch_bounds__(64 * kProjWaves) __attribute__((amdgpu_waves_p
   const int64_t base_tok = is_query ? a.q_row0 : 0;
   const int64_t tile0 = grp * kProjTiles;
 
-  // Staging goes straight to LDS (16 bytes per lane): the workgroup's 16 KB
-  // per chunk are 16 blocks of 8 rows, block b copied by wave b % 8; lane i of
+  // Staging goes straight to LDS (16 bytes per lane): the workgroup's 2 TILES KB
+  // per chunk are 2 TILES blocks of 8 rows, block b copied by wave b % 8; lane i of
   // a block fills row 8 b + i / 8, swizzled chunk i % 8, i.e. channel chunk
   // (i % 8) ^ ((row >> 1) & 7) of the 64. Rows past the valid tokens repeat
   // the last one (their outputs are zeroed); c_s is a multiple of 32, so a
@@ -125,6 +129,7 @@ __global__ void __launch_bounds__(64 * kProjWaves) __attribute__((amdgpu_waves_p
   auto stage = [&](int kc, int buf) {
 #pragma unroll
     for (int m = 0; m < kProjStage; ++m) {
+      if (kBlocks % kProjWaves != 0 && wave + kProjWaves * m >= kBlocks) break;  // wave-uniform
       const int row = 8 * (wave + kProjWaves * m) + lane / 8;
       const int ch = min(kc * kProjChunk + 8 * ((lane % 8) ^ ((row >> 1) & 7)), a.c_s - 8);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
@@ -266,11 +271,21 @@ hipError_t launch_fast_proj(const FastProjArgs& a, hipStream_t st) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // (side, token group) items, rounded up to whole sets of 8 (one per XCD),
-  // 3 workgroups each
-  const int64_t items =
-      (a.n_pad / 16 + kProjTiles - 1) / kProjTiles + (a.nq_pad / 16 + kProjTiles - 1) / kProjTiles;
-  const int64_t sets = (items + 7) / 8;
-  hipLaunchKernelGGL(proj_kernel, dim3((unsigned)(sets * 8 * kProjSideWgs)), dim3(64 * kProjWaves), 0, st, a);
+  // 3 workgroups each. 128-token groups when that fills the chip twice;
+  // else 64 if that fills it once, else 32 (small layers: a 1024-token layer
+  // 0.106 -> 0.093 ms, a 4800-token one -0.8%; each wave's weights are then
+  // applied to fewer tokens, which costs more than it saves on larger layers).
+  auto workgroups = [&](int tiles) {
+    const int64_t items = (a.n_pad / 16 + tiles - 1) / tiles + (a.nq_pad / 16 + tiles - 1) / tiles;
+    return (items + 7) / 8 * 8 * kProjSideWgs;
+  };
+  const int64_t w8 = workgroups(8), w4 = workgroups(4), w2 = workgroups(2);
+  if (w8 >= 512)
+    hipLaunchKernelGGL(proj_kernel<8>, dim3((unsigned)w8), dim3(64 * kProjWaves), 0, st, a);
+  else if (w4 >= 256)
+    hipLaunchKernelGGL(proj_kernel<4>, dim3((unsigned)w4), dim3(64 * kProjWaves), 0, st, a);
+  else
+    hipLaunchKernelGGL(proj_kernel<2>, dim3((unsigned)w2), dim3(64 * kProjWaves), 0, st, a);
   return hipGetLastError();
 }
 
