@@ -76,6 +76,7 @@ struct FastAttnArgs {
   int32_t n_kb, n_seg;
   float eps;
   float *m_parts, *l_parts, *acc_parts;  // [P][H][n_q], [P][H][n_q], [P][n_q][H][d]
+  int32_t xcd_order;                     // set by the launcher: workgroup numbering (attn_kernel)
 };
 
 struct FastBiasArgs {

@@ -205,10 +205,31 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, n = lane & 15, g = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int64_t n_qt = a.nq_pad / kTileQ;
-  const int64_t qt = (int64_t)blockIdx.x * kWaves + wave;
+  // Workgroup -> (row group, part). The hardware deals workgroups to the 8
+  // XCDs in turn (workgroup i to XCD i % 8). By default row groups vary
+  // fastest, so the resident workgroups of every XCD stream the same part.
+  // With xcd_order (layers of at least 256 row groups), XCD x takes the row
+  // groups rg = x (mod 8), all parts of them, one part after another starting
+  // at part x mod P: each XCD's L2 still serves one part's K/V at a time while
+  // the XCDs stream z at different key positions.
+  int64_t rg;
+  int part;
+  if (a.xcd_order) {
+    const int P = a.n_kb * a.n_seg;
+    const int64_t n_rg = (n_qt + kWaves - 1) / kWaves;
+    const int x = blockIdx.x & 7;
+    const int64_t k = blockIdx.x >> 3;
+    const int64_t cnt = (n_rg - x + 7) / 8;  // row groups of this XCD
+    if (k >= cnt * P) return;                // whole workgroup, before any barrier
+    rg = x + 8 * (k % cnt);
+    part = (int)((x + k / cnt) % P);
+  } else {
+    rg = blockIdx.x;
+    part = blockIdx.y;
+  }
+  const int64_t qt = rg * kWaves + wave;
   const bool active = qt < n_qt;
   const int64_t q0 = (active ? qt : n_qt - 1) * kTileQ;
-  const int part = blockIdx.y;
   int64_t start, end;
   part_range(a.k_len, a.n_kb, a.n_seg, part, &start, &end);
   start += a.k_lo;
@@ -553,8 +574,16 @@ __global__ void __launch_bounds__(64) bias_kernel(FastBiasArgs a) {
 
 hipError_t launch_fast_attn(const FastAttnArgs& a, hipStream_t st) {
   const int64_t n_qt = a.nq_pad / kTileQ;
-  hipLaunchKernelGGL(attn_kernel, dim3((unsigned)((n_qt + kWaves - 1) / kWaves), (unsigned)(a.n_kb * a.n_seg)),
-                     dim3(64 * kWaves), 0, st, a);
+  const int64_t n_rg = (n_qt + kWaves - 1) / kWaves;
+  const int64_t parts = (int64_t)a.n_kb * a.n_seg;
+  FastAttnArgs b = a;
+  // numbered per XCD only where every XCD then holds at least 32 row groups
+  // (a round of its CUs) of each part, which keeps the XCDs evenly loaded
+  b.xcd_order = n_rg >= 256 && parts > 1;
+  if (b.xcd_order)
+    hipLaunchKernelGGL(attn_kernel, dim3((unsigned)(8 * ((n_rg + 7) / 8) * parts)), dim3(64 * kWaves), 0, st, b);
+  else
+    hipLaunchKernelGGL(attn_kernel, dim3((unsigned)n_rg, (unsigned)parts), dim3(64 * kWaves), 0, st, b);
   return hipGetLastError();
 }
 
