@@ -79,8 +79,9 @@ typedef struct {
   const float* ln_beta;  /* [c_z] or NULL (= 0)                                   */
 } dcp_weights;
 /* On the fused bf16 path below (attention and dcp_bias_project), w_q, w_k,
- * w_v, w_g, w_b and ln_gamma must be 16-byte aligned (DCP_ERR_INVALID_ARGUMENT
- * otherwise); the general fp32 path needs 4-byte alignment only. */
+ * w_v, w_g, w_b and ln_gamma (and, for dcp_bias_project, ln_beta) must be
+ * 16-byte aligned (DCP_ERR_INVALID_ARGUMENT otherwise); the general fp32 path
+ * needs 4-byte alignment only. */
 
 /* Supported shapes. A fused MFMA path serves act_dtype = BF16 with c_z = 128,
  * H = 16, d = 24 and c_s a multiple of 32 (at most 4096). A general fp32 path

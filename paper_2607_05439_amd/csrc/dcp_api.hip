@@ -485,8 +485,8 @@ int dcp_bias_project(const dcp_shape* shape, const dcp_weights* w, const void* z
   if (fast) {
     if (!aligned(z_tile, 16) || !aligned(bias_out, 16) || row_stride_elems % 8 != 0)
       return fail(DCP_ERR_INVALID_ARGUMENT, "z_tile and bias_out must be 16-byte aligned, row_stride_elems a multiple of 8");
-    if (!aligned(w->w_b, 16) || !aligned(w->ln_gamma, 16))
-      return fail(DCP_ERR_INVALID_ARGUMENT, "w_b and ln_gamma must be 16-byte aligned");
+    if (!aligned(w->w_b, 16) || !aligned(w->ln_gamma, 16) || !aligned(w->ln_beta, 16))
+      return fail(DCP_ERR_INVALID_ARGUMENT, "w_b, ln_gamma and ln_beta must be 16-byte aligned");
     dcp::FastBiasArgs a{};
     a.z = static_cast<const uint16_t*>(z_tile);
     a.w_b = w->w_b;

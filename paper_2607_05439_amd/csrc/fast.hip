@@ -420,16 +420,32 @@ __global__ void __launch_bounds__(256, 1) attn_kernel(FastAttnArgs a) {
 }
 
 // ----------------------------------------------------------------------------- bias only
-// Per-head constant sum_c W_b[h,c] beta_c + b_b[h] for heads 4g..4g+3.
-__device__ __forceinline__ void bias_constants(const FastBiasArgs& a, int g, float (&cst)[4]) {
+// Per-head constant sum_c W_b[h,c] beta_c + b_b[h] for heads 4g..4g+3. Lane
+// (n, g) forms the partial sums over channels 8n .. 8n+7 (all its loads issued
+// at once: one memory round trip, not one per 16 channels), then the 16 lanes
+// of the group add them in a fixed butterfly, which leaves the same bits in
+// every lane of the group. w_b and beta are 16-byte aligned (host-checked).
+__device__ __forceinline__ void bias_constants(const FastBiasArgs& a, int n, int g, float (&cst)[4]) {
+  float part[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (a.beta) {
+    const float4* bp = reinterpret_cast<const float4*>(a.beta + 8 * n);
+    const float4 b0 = bp[0], b1 = bp[1];
+    const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int h = 4 * g + i;
-    float c0 = a.b_b ? a.b_b[h] : 0.0f;
-    if (a.beta)
-      for (int c = 0; c < kCz; ++c) c0 = fmaf(a.w_b[h * kCz + c], a.beta[c], c0);
-    cst[i] = c0;
+    for (int i = 0; i < 4; ++i) {
+      const float4* wp = reinterpret_cast<const float4*>(a.w_b + (4 * g + i) * kCz + 8 * n);
+      const float4 w0 = wp[0], w1 = wp[1];
+      const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+#pragma unroll
+      for (int k = 0; k < 8; ++k) part[i] = fmaf(wv[k], bv[k], part[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int m = 8; m >= 1; m >>= 1) part[i] += __shfl_xor(part[i], m, 16);
   }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) cst[i] = (a.b_b ? a.b_b[4 * g + i] : 0.0f) + part[i];
 }
 
 constexpr int kBiasRing = 8;               // z slots per wave: 128 KB per workgroup, one per CU
@@ -454,7 +470,7 @@ __global__ void __launch_bounds__(64 * kWaves, 1) bias_ring_kernel(FastBiasArgs 
   bias_weights(a.w_b, a.gamma, 1.0f, lane, whi, wlo);
   const f32x4 wsum = bias_weight_sums(whi, wlo);
   float cst[4];
-  bias_constants(a, g, cst);
+  bias_constants(a, n, g, cst);
 
   // rows r0 .. r0+15 (those past n_rows fall outside the record range: no data)
   const int64_t rows_here = min((int64_t)16, a.n_rows - r0);
@@ -535,7 +551,7 @@ __global__ void __launch_bounds__(64) bias_kernel(FastBiasArgs a) {
   bias_weights(a.w_b, a.gamma, 1.0f, lane, whi, wlo);
   const f32x4 wsum = bias_weight_sums(whi, wlo);
   float cst[4];
-  bias_constants(a, g, cst);
+  bias_constants(a, n, g, cst);
   const int64_t row = r0 + n;
   const int64_t rr = min(row, a.n_rows - 1);
   const u32x4* zrow = reinterpret_cast<const u32x4*>(a.z + rr * a.row_stride) + g;

@@ -161,7 +161,8 @@ def test_bias_project_rejections():
     assert L.dcp_bias_project(ctypes.byref(sh), ctypes.byref(w), 0, 4, 8, 1024, FAKE, None) == E
     assert L.dcp_bias_project(ctypes.byref(sh), ctypes.byref(w), FAKE, -1, 8, 1024, FAKE, None) == E
     assert L.dcp_bias_project(ctypes.byref(sh), ctypes.byref(w), FAKE, 0, 8, 1024, FAKE, None) == dcp.DCP_OK
-    for wb in (dcp.make_weights(FAKE, FAKE, FAKE, FAKE, FAKE + 4), dcp.make_weights(0, 0, 0, 0, FAKE, ln_gamma=FAKE + 4)):
+    for wb in (dcp.make_weights(FAKE, FAKE, FAKE, FAKE, FAKE + 4), dcp.make_weights(0, 0, 0, 0, FAKE, ln_gamma=FAKE + 4),
+               dcp.make_weights(0, 0, 0, 0, FAKE, ln_beta=FAKE + 8)):
         assert L.dcp_bias_project(ctypes.byref(sh), ctypes.byref(wb), FAKE, 4, 8, 1024, FAKE, None) == E
     bad = shape(c_z=1000)
     assert L.dcp_bias_project(ctypes.byref(bad), ctypes.byref(w), FAKE, 4, 8, 8000, FAKE, None) == \
