@@ -949,9 +949,9 @@ def main():
     ap.add_argument("--no-extra-configs", action="store_true",
                     help="skip timing the smaller attention workloads after the default one")
     ap.add_argument("--extra-steps", type=int, default=20)
-    ap.add_argument("--p-form", choices=("dense", "gathered"), default="dense",
-                    help="sparse atom workloads: P as the query stripe's dense rows (default) or as the gathered "
-                         "slices P_sparse[n_q, k, c_ap]")
+    ap.add_argument("--p-form", choices=("dense", "gathered"), default="gathered",
+                    help="sparse atom workloads: P as the gathered slices P_sparse[n_q, k, c_ap] (default; the "
+                         "paper's sparse form) or as the query stripe's dense rows")
     ap.add_argument("--calibrate-bytes", type=int, default=1 << 31,
                     help="bytes for the plain-copy calibration kernel (counter scaling)")
     args = ap.parse_args()
