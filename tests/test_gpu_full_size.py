@@ -67,3 +67,25 @@ def test_asm24000_bias_project_full_rows(big, r0):
     err = rel_err(out.cpu().numpy(), ref)
     log(f"  rel err {err:.3e}")
     assert err <= 1e-4
+
+
+@pytest.mark.parametrize("q_row0,n_q", [(0, 16384), (7000, 16400)])
+def test_asm24000_stripes_numbered_per_xcd(big, q_row0, n_q):
+    """Stripes of 256 and 257 row groups of 64: the smallest for which the
+    attention numbers its workgroups per XCD, and one that leaves XCD 0 one row
+    group more than the others. Against the whole-layer call (fp32 out, 1e-6:
+    the stripe's own segment count may differ) and the fp64 oracle (1e-2, bf16
+    inputs) on the first and last rows of the stripe and of its last row
+    groups."""
+    wl = big.wl
+    log(f"case asm24000_bf16 stripe q_row0={q_row0} n_q={n_q} n_kb={wl.n_key_blocks} (per-XCD numbering)")
+    full = big.attention(0, wl.n_tok, wl.n_key_blocks).cpu().numpy()
+    got = big.attention(q_row0, n_q, wl.n_key_blocks).cpu().numpy()
+    err = rel_err(got, full[q_row0:q_row0 + n_q])
+    log(f"  stripe vs whole layer rel diff {err:.3e}")
+    assert err <= 1e-6
+    local = [0, 1, 63, 64, n_q - 129, n_q - 65, n_q - 64, n_q - 17, n_q - 1]
+    ref = big.oracle_rows([q_row0 + r for r in local])
+    err = rel_err(got[local], ref)
+    log(f"  {len(local)} rows against the oracle rel err {err:.3e}")
+    assert err <= 1e-2
