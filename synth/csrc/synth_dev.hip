@@ -140,14 +140,28 @@ __device__ __forceinline__ void pattern_key_loads(__amdgpu_buffer_rsrc_t r, int 
 }
 
 __global__ void __launch_bounds__(256, 1) read_pattern_kernel(const uint16_t* __restrict__ z, int64_t n_tok,
-                                                              int64_t n_rows, int n_parts, uint32_t* __restrict__ sink) {
+                                                              int64_t n_rows, int n_parts, int xcd_order,
+                                                              uint32_t* __restrict__ sink) {
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
   __shared__ u32x4 ring[4][kPatRing][256];    // 128 KB: 4 KB per key and wave
   __shared__ uint32_t fill[32 * 256 - 16];    // the rest of the CU's LDS
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int64_t r0 = ((int64_t)blockIdx.x * 4 + wave) * 16;
+  // workgroup -> (64-row group, part) as the attention numbers them: row
+  // groups fastest, or (xcd_order) XCD x walking the groups x mod 8 part by
+  // part from part x mod n_parts
+  int64_t rg, p;
+  if (xcd_order) {
+    const int64_t n_rg = (n_rows + 63) / 64, x = blockIdx.x & 7, k = blockIdx.x >> 3, cnt = (n_rg - x + 7) / 8;
+    if (k >= cnt * n_parts) return;  // no barriers below
+    rg = x + 8 * (k % cnt);
+    p = (x + k / cnt) % n_parts;
+  } else {
+    rg = blockIdx.x;
+    p = blockIdx.y;
+  }
+  const int64_t r0 = (rg * 4 + wave) * 16;
   if (r0 + 16 > n_rows) return;  // whole 16-row tiles only; no barriers below
-  const int64_t q = n_tok / n_parts, rem = n_tok % n_parts, p = blockIdx.y;
+  const int64_t q = n_tok / n_parts, rem = n_tok % n_parts;
   const int64_t k0 = p * q + (p < rem ? p : rem), k1 = k0 + q + (p < rem ? 1 : 0);
   const int row_bytes = (int)(n_tok * 256);
   const __amdgpu_buffer_rsrc_t zres = __builtin_amdgcn_make_buffer_rsrc(
@@ -246,8 +260,15 @@ int synth_dev_copy(const void* src, void* dst, int64_t bytes, void* stream) {
 int synth_dev_read_pattern(const void* z, int64_t n_tok, int64_t n_rows, int32_t n_parts, void* sink, void* stream) {
   if (!z || !sink || n_tok <= 0 || n_rows <= 0 || n_parts < 1 || n_parts > n_tok) return -1;
   if (n_tok * 256 * 16 + 4096 > INT32_MAX) return -1;  // 32-bit buffer offsets of 16 rows
-  hipLaunchKernelGGL(read_pattern_kernel, dim3((unsigned)((n_rows + 63) / 64), (unsigned)n_parts), dim3(256), 0,
-                     (hipStream_t)stream, (const uint16_t*)z, n_tok, n_rows, n_parts, (uint32_t*)sink);
+  // the attention's workgroup order: per XCD from 256 row groups and two parts on
+  const int64_t n_rg = (n_rows + 63) / 64;
+  const int xcd_order = n_rg >= 256 && n_parts > 1;
+  if (xcd_order)
+    hipLaunchKernelGGL(read_pattern_kernel, dim3((unsigned)(8 * ((n_rg + 7) / 8) * n_parts)), dim3(256), 0,
+                       (hipStream_t)stream, (const uint16_t*)z, n_tok, n_rows, n_parts, xcd_order, (uint32_t*)sink);
+  else
+    hipLaunchKernelGGL(read_pattern_kernel, dim3((unsigned)n_rg, (unsigned)n_parts), dim3(256), 0,
+                       (hipStream_t)stream, (const uint16_t*)z, n_tok, n_rows, n_parts, xcd_order, (uint32_t*)sink);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
